@@ -1,0 +1,137 @@
+/*
+ * sbvr.h -- C ABI of the MI355X (gfx950) SBVR GEMV library.
+ *
+ * SBVR (Summation of BitVector Representation; Bang et al., Sec. 4.1) stores
+ * each group of 128 consecutive weights along the inner-product dimension as
+ * k bitvectors ("planes") plus k coefficients, so that every decoded weight is
+ * a subset sum of its group's coefficients:
+ *
+ *     w_hat[o][128 g + j] = sum_{i<k} c[o][g][i] * b[o][g][i][j]      (Sec. 4.1)
+ *
+ * and the GEMV is computed directly on that representation (Sec. 4.4):
+ *
+ *     y[o] = sum_g sum_i c[o][g][i] * (sum_{j : b[o][g][i][j] = 1} x[128 g + j])
+ *
+ * Activations x and outputs y are IEEE binary16; accumulation is binary32;
+ * y is rounded to binary16 to nearest-even.
+ *
+ * CANONICAL FORMAT (host-independent, what an encoder writes):
+ *   planes  uint32_t [O][G][k][4], G = I / 128.  Bit t (LSB = 0) of word w is
+ *           element j = 32 w + t of the group.  Plane i pairs with coefficient
+ *           i.  (The paper stores bitvectors "partitioned into 32-bit
+ *           integers" in one contiguous tensor, Sec. 4.4.)
+ *   coeffs  uint16_t [O][G][k], binary16 bit patterns of c[o][g][i].  The
+ *           per-(row, group, plane) coefficient tensor stands in for the
+ *           paper's coefficient cache + index (Sec. 4.4); it holds the same
+ *           values.
+ *
+ * DEVICE FORMAT: an opaque, padded repacking of the canonical tensors that
+ * the GEMV kernels stream with 128-bit coalesced loads.  It is produced by
+ * sbvr_pack and inverted bit-exactly by sbvr_unpack; its size comes from the
+ * two size queries.  Its layout is private to the library and may change.
+ *
+ * CONVENTIONS for every entry point:
+ *   - O (out_features) >= 1; I (in_features) >= 128 and a multiple of 128;
+ *     1 <= k <= 4 planes; 1 <= B <= 8 activation vectors.
+ *   - Pointers named *_dev, x, y, X, Y, planes_canon and coeffs_canon are
+ *     device pointers (HIP global memory) owned by the caller.  The library
+ *     never allocates, frees or synchronises; work is enqueued on `stream`
+ *     (0 = the null stream) and completes asynchronously.  Every call is
+ *     safe to capture in a HIP graph.
+ *   - Alignment: planes_dev, coeffs_dev, planes_canon, x and X 16 bytes;
+ *     coeffs_canon, y and Y 2 bytes.
+ *   - On any error nothing is enqueued and no output is written.  No call
+ *     aborts, throws or prints.
+ *   - Inputs are assumed finite.  Calls on one stream are ordered; calls that
+ *     run concurrently on different streams must not share an output buffer.
+ */
+#ifndef SBVR_H
+#define SBVR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes.  Every entry point returns one of these. */
+enum sbvr_status {
+    SBVR_OK = 0,
+    SBVR_E_INVALID_ARG = -1, /* null pointer, bad shape, B out of range */
+    SBVR_E_UNSUPPORTED = -2, /* valid SBVR parameters this build does not run (k > 4) */
+    SBVR_E_WORKSPACE = -3,   /* workspace smaller than sbvr_workspace_bytes */
+    SBVR_E_ALIGNMENT = -4,   /* a pointer violates the alignment above */
+    SBVR_E_HIP = -5          /* the HIP runtime reported a launch error */
+};
+
+/* Human-readable name of a status code; never NULL, static storage. */
+const char *sbvr_status_string(int status);
+
+/* Library ABI version (major * 100 + minor). */
+int sbvr_version(void);
+
+/*
+ * Size queries (pure host functions, no HIP calls).  Bytes the caller must
+ * provide for the device planes / device coefficients of an O x I matrix
+ * with k planes; 0 if the arguments are invalid.
+ */
+size_t sbvr_packed_plane_bytes(int O, int I, int k);
+size_t sbvr_packed_coeff_bytes(int O, int I, int k);
+
+/*
+ * Workspace a GEMV call needs, in bytes (0 means none: pass workspace = NULL
+ * and ws_bytes = 0).  The current kernels reduce split-K partial sums inside
+ * one workgroup and need no global workspace.
+ */
+size_t sbvr_workspace_bytes(int O, int I, int k, int B);
+
+/*
+ * Repack canonical SBVR tensors into the device format (the storage of
+ * Sec. 4.4, laid out for the GEMV kernels).
+ *   planes_canon  uint32 [O][G][k][4], coeffs_canon uint16 [O][G][k]: input.
+ *   planes_dev    >= sbvr_packed_plane_bytes(O, I, k) bytes: output.
+ *   coeffs_dev    >= sbvr_packed_coeff_bytes(O, I, k) bytes: output.
+ * Every byte of both outputs is written (padding with zeros).  Inputs and
+ * outputs must not overlap.
+ */
+int sbvr_pack(int O, int I, int k, const uint32_t *planes_canon, const uint16_t *coeffs_canon,
+              void *planes_dev, void *coeffs_dev, hipStream_t stream);
+
+/*
+ * Inverse of sbvr_pack: recover the canonical tensors, bit for bit, from the
+ * device format.  Same shapes and ownership as sbvr_pack with the roles of
+ * input and output exchanged.
+ */
+int sbvr_unpack(int O, int I, int k, const void *planes_dev, const void *coeffs_dev,
+                uint32_t *planes_canon, uint16_t *coeffs_canon, hipStream_t stream);
+
+/*
+ * Batch-1 SBVR GEMV (Sec. 4.4 with binary16 activations):
+ *     y[o] = fp16_rne( sum_g sum_i c[o][g][i] * sum_j b[o][g][i][j] x[128 g + j] )
+ *   planes_dev, coeffs_dev  device-format weights from sbvr_pack.
+ *   x  binary16 [I] (input);  y  binary16 [O] (output, every element written).
+ *   workspace / ws_bytes    see sbvr_workspace_bytes (may be NULL / 0).
+ * x must not overlap y.
+ */
+int sbvr_gemv(int O, int I, int k, const void *planes_dev, const void *coeffs_dev,
+              const uint16_t *x, uint16_t *y, void *workspace, size_t ws_bytes,
+              hipStream_t stream);
+
+/*
+ * Small-batch SBVR GEMM: Y[b][o] as sbvr_gemv for each of the B activation
+ * vectors X[b][0..I), with the weights read from memory once for all B.
+ *   X  binary16 [B][I] row-major (input);  Y  binary16 [B][O] row-major (output).
+ *   1 <= B <= 8.
+ */
+int sbvr_gemm_small_batch(int O, int I, int k, const void *planes_dev, const void *coeffs_dev,
+                          const uint16_t *X, uint16_t *Y, int B, void *workspace,
+                          size_t ws_bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SBVR_H */

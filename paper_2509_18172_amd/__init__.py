@@ -1,0 +1,211 @@
+"""SBVR GEMV on MI355X: Python binding of the C ABI in include/sbvr.h.
+
+Argument marshalling only: every step of the computation runs in the HIP
+kernels of ``_lib/libsbvr.so``.  PyTorch supplies device memory and streams.
+If the library is not built, importing this package raises -- there is no
+fallback path.
+
+Functions with the C names take raw integers (device pointers, stream
+handles) and return the C status code.  The tensor helpers below check
+shapes, allocate outputs with torch and raise ``SBVRError`` on a non-zero
+status.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+from .build import library_path
+
+GROUP = 128
+
+SBVR_OK = 0
+SBVR_E_INVALID_ARG = -1
+SBVR_E_UNSUPPORTED = -2
+SBVR_E_WORKSPACE = -3
+SBVR_E_ALIGNMENT = -4
+SBVR_E_HIP = -5
+
+EXPORTED = (
+    "sbvr_status_string", "sbvr_version", "sbvr_packed_plane_bytes", "sbvr_packed_coeff_bytes",
+    "sbvr_workspace_bytes", "sbvr_pack", "sbvr_unpack", "sbvr_gemv", "sbvr_gemm_small_batch",
+)
+
+
+class SBVRError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what}: {sbvr_status_string(status)} ({status})")
+        self.status = status
+
+
+def _load():
+    # PyTorch ships its own HIP runtime (same SONAME as ROCm's).  Loading torch
+    # first makes libsbvr.so bind to that runtime, so device pointers and
+    # stream handles from torch are valid in the library; loading ROCm's copy
+    # first would put two HIP runtimes in the process.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
+    path = library_path()
+    if not os.path.exists(path):
+        raise ImportError(
+            f"SBVR HIP library not built ({path}); run `python -c 'import __graft_entry__ as g; g.build()'`")
+    lib = C.CDLL(path)
+    vp, sz, i32 = C.c_void_p, C.c_size_t, C.c_int
+    sig = {
+        "sbvr_status_string": (C.c_char_p, [i32]),
+        "sbvr_version": (i32, []),
+        "sbvr_packed_plane_bytes": (sz, [i32, i32, i32]),
+        "sbvr_packed_coeff_bytes": (sz, [i32, i32, i32]),
+        "sbvr_workspace_bytes": (sz, [i32, i32, i32, i32]),
+        "sbvr_pack": (i32, [i32, i32, i32, vp, vp, vp, vp, vp]),
+        "sbvr_unpack": (i32, [i32, i32, i32, vp, vp, vp, vp, vp]),
+        "sbvr_gemv": (i32, [i32, i32, i32, vp, vp, vp, vp, vp, sz, vp]),
+        "sbvr_gemm_small_batch": (i32, [i32, i32, i32, vp, vp, vp, vp, i32, vp, sz, vp]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(lib, name)
+        f.restype = res
+        f.argtypes = args
+    return lib
+
+
+_lib = _load()
+
+
+# --------------------------------------------------------------------------
+# C ABI, same names (raw pointers / stream handles as Python ints)
+# --------------------------------------------------------------------------
+
+def sbvr_status_string(status: int) -> str:
+    return _lib.sbvr_status_string(int(status)).decode()
+
+
+def sbvr_version() -> int:
+    return _lib.sbvr_version()
+
+
+def sbvr_packed_plane_bytes(O: int, I: int, k: int) -> int:
+    return _lib.sbvr_packed_plane_bytes(O, I, k)
+
+
+def sbvr_packed_coeff_bytes(O: int, I: int, k: int) -> int:
+    return _lib.sbvr_packed_coeff_bytes(O, I, k)
+
+
+def sbvr_workspace_bytes(O: int, I: int, k: int, B: int = 1) -> int:
+    return _lib.sbvr_workspace_bytes(O, I, k, B)
+
+
+def sbvr_pack(O, I, k, planes_canon, coeffs_canon, planes_dev, coeffs_dev, stream=0) -> int:
+    return _lib.sbvr_pack(O, I, k, planes_canon, coeffs_canon, planes_dev, coeffs_dev, stream)
+
+
+def sbvr_unpack(O, I, k, planes_dev, coeffs_dev, planes_canon, coeffs_canon, stream=0) -> int:
+    return _lib.sbvr_unpack(O, I, k, planes_dev, coeffs_dev, planes_canon, coeffs_canon, stream)
+
+
+def sbvr_gemv(O, I, k, planes_dev, coeffs_dev, x, y, workspace=None, ws_bytes=0, stream=0) -> int:
+    return _lib.sbvr_gemv(O, I, k, planes_dev, coeffs_dev, x, y, workspace, ws_bytes, stream)
+
+
+def sbvr_gemm_small_batch(O, I, k, planes_dev, coeffs_dev, X, Y, B, workspace=None, ws_bytes=0,
+                          stream=0) -> int:
+    return _lib.sbvr_gemm_small_batch(O, I, k, planes_dev, coeffs_dev, X, Y, B, workspace, ws_bytes,
+                                      stream)
+
+
+# --------------------------------------------------------------------------
+# torch tensor helpers
+# --------------------------------------------------------------------------
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream(stream=None) -> int:
+    torch = _torch()
+    s = torch.cuda.current_stream() if stream is None else stream
+    return int(s.cuda_stream)
+
+
+def _check(status: int, what: str):
+    if status != SBVR_OK:
+        raise SBVRError(status, what)
+
+
+class PackedWeight:
+    """An O x I SBVR matrix with k planes, resident in device memory in the
+    library's device format."""
+
+    def __init__(self, O: int, I: int, k: int, planes_dev, coeffs_dev):
+        self.O, self.I, self.k = O, I, k
+        self.planes = planes_dev
+        self.coeffs = coeffs_dev
+
+    @property
+    def nbytes(self) -> int:
+        return self.planes.numel() + self.coeffs.numel()
+
+    @staticmethod
+    def alloc(O: int, I: int, k: int, device="cuda"):
+        torch = _torch()
+        pb, cb = sbvr_packed_plane_bytes(O, I, k), sbvr_packed_coeff_bytes(O, I, k)
+        if pb == 0 or cb == 0:
+            raise SBVRError(SBVR_E_INVALID_ARG, f"shape {O}x{I} k={k}")
+        return PackedWeight(O, I, k, torch.empty(pb, dtype=torch.uint8, device=device),
+                            torch.empty(cb, dtype=torch.uint8, device=device))
+
+
+def pack(planes_canon, coeffs_canon, stream=None) -> PackedWeight:
+    """Repack canonical device tensors (int32/uint32 [O][G][k][4], int16/uint16
+    [O][G][k]) into a PackedWeight."""
+    O, G, k, four = planes_canon.shape
+    assert four == 4 and tuple(coeffs_canon.shape) == (O, G, k)
+    assert planes_canon.is_contiguous() and coeffs_canon.is_contiguous()
+    assert planes_canon.element_size() == 4 and coeffs_canon.element_size() == 2
+    W = PackedWeight.alloc(O, G * GROUP, k, device=planes_canon.device)
+    _check(sbvr_pack(O, G * GROUP, k, planes_canon.data_ptr(), coeffs_canon.data_ptr(),
+                     W.planes.data_ptr(), W.coeffs.data_ptr(), _stream(stream)), "sbvr_pack")
+    return W
+
+
+def unpack(W: PackedWeight, stream=None):
+    """Canonical (planes int32 [O][G][k][4], coeffs int16 [O][G][k]) device tensors."""
+    torch = _torch()
+    G = W.I // GROUP
+    planes = torch.empty((W.O, G, W.k, 4), dtype=torch.int32, device=W.planes.device)
+    coeffs = torch.empty((W.O, G, W.k), dtype=torch.int16, device=W.planes.device)
+    _check(sbvr_unpack(W.O, W.I, W.k, W.planes.data_ptr(), W.coeffs.data_ptr(), planes.data_ptr(),
+                       coeffs.data_ptr(), _stream(stream)), "sbvr_unpack")
+    return planes, coeffs
+
+
+def gemv(W: PackedWeight, x, out=None, stream=None):
+    """y = SBVR(W) x for x fp16 [I]; returns fp16 [O]."""
+    torch = _torch()
+    assert x.dtype == torch.float16 and x.is_contiguous() and x.shape == (W.I,)
+    y = torch.empty(W.O, dtype=torch.float16, device=x.device) if out is None else out
+    _check(sbvr_gemv(W.O, W.I, W.k, W.planes.data_ptr(), W.coeffs.data_ptr(), x.data_ptr(),
+                     y.data_ptr(), None, 0, _stream(stream)), "sbvr_gemv")
+    return y
+
+
+def gemm_small_batch(W: PackedWeight, X, out=None, stream=None):
+    """Y = X SBVR(W)^T for X fp16 [B][I], 1 <= B <= 8; returns fp16 [B][O]."""
+    torch = _torch()
+    assert X.dtype == torch.float16 and X.is_contiguous() and X.dim() == 2 and X.shape[1] == W.I
+    B = X.shape[0]
+    Y = torch.empty((B, W.O), dtype=torch.float16, device=X.device) if out is None else out
+    _check(sbvr_gemm_small_batch(W.O, W.I, W.k, W.planes.data_ptr(), W.coeffs.data_ptr(),
+                                 X.data_ptr(), Y.data_ptr(), B, None, 0, _stream(stream)),
+           "sbvr_gemm_small_batch")
+    return Y
+
+
+def algorithmic_bytes(O: int, I: int, k: int, B: int = 1) -> int:
+    """Bytes the method must move per call: planes k*O*I/8, fp16 coefficients
+    2*k*O*I/128, activations 2*I*B and outputs 2*O*B."""
+    return k * O * I // 8 + 2 * k * O * I // GROUP + 2 * I * B + 2 * O * B

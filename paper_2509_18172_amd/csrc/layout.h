@@ -1,0 +1,89 @@
+// Device layout of SBVR weights for the gfx950 GEMV kernels.
+//
+// The canonical format (include/sbvr.h) stores, per (row o, group g, plane i),
+// 128 plane bits in four 32-bit words plus one binary16 coefficient
+// (Sec. 4.1, Sec. 4.4).  The device format regroups those words so that a
+// wavefront's 128-bit loads are contiguous and so that each loaded word can be
+// turned into matrix-core operands with a handful of bit masks:
+//
+//   tile      TILE_ROWS = 4 consecutive rows
+//   gblock    GB = 4 consecutive groups (512 inner-dimension elements)
+//   block     one (tile, gblock) pair; blocks are stored tile-major:
+//             block index = tile * n_gblocks + gblock
+//
+//   plane block (256 * k bytes): slot s = (b * TILE_ROWS + r) * k + i holds the
+//     four words (16 bytes) of plane i of row 4*tile + r for group 4*gblock + b.
+//   coeff block (32 * k bytes):  entry (r * GB + b) * k + i holds c[o][g][i].
+//
+// Within each device word the bits are transposed as a 4 x 8 bit matrix:
+// element e = 8 v + p (0 <= v < 4, 0 <= p < 8) of the word sits at bit 4 p + v.
+// Then w & (0x11111111 << v) places element 8 v + p in nibble p, which is the
+// matrix-core k-slot 8 v + p of an fp4 operand register v.
+//
+// Rows past O and groups past G are zero padding (zero planes and zero
+// coefficients contribute nothing to y).
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#define SBVR_HD __host__ __device__ __forceinline__
+
+namespace sbvr {
+
+constexpr int GROUP = 128;     // weights per SBVR group (Sec. 4.1)
+constexpr int TILE_ROWS = 4;   // rows per tile
+constexpr int GB = 4;          // groups per gblock
+constexpr int MAX_K = 4;       // planes supported by this build
+
+struct Dims {
+    int O, I, k, G, n_tiles, n_gblocks;
+};
+
+SBVR_HD Dims make_dims(int O, int I, int k)
+{
+    Dims d;
+    d.O = O;
+    d.I = I;
+    d.k = k;
+    d.G = I / GROUP;
+    d.n_tiles = (O + TILE_ROWS - 1) / TILE_ROWS;
+    d.n_gblocks = (d.G + GB - 1) / GB;
+    return d;
+}
+
+SBVR_HD size_t plane_block_words(int k) { return (size_t)GB * TILE_ROWS * k * 4; }
+SBVR_HD size_t coeff_block_entries(int k) { return (size_t)TILE_ROWS * GB * k; }
+
+SBVR_HD size_t plane_bytes(const Dims &d)
+{
+    return (size_t)d.n_tiles * d.n_gblocks * plane_block_words(d.k) * 4;
+}
+
+SBVR_HD size_t coeff_bytes(const Dims &d)
+{
+    return (size_t)d.n_tiles * d.n_gblocks * coeff_block_entries(d.k) * 2;
+}
+
+// canonical bit t (element t of the word) -> device bit position
+SBVR_HD int device_bit_of(int t) { return 4 * (t % 8) + t / 8; }
+// device bit position d -> canonical bit (element index within the word)
+SBVR_HD int canonical_bit_of(int d) { return 8 * (d % 4) + d / 4; }
+
+SBVR_HD uint32_t to_device_word(uint32_t w)
+{
+    uint32_t r = 0;
+    for (int t = 0; t < 32; ++t)
+        r |= ((w >> t) & 1u) << device_bit_of(t);
+    return r;
+}
+
+SBVR_HD uint32_t to_canonical_word(uint32_t w)
+{
+    uint32_t r = 0;
+    for (int d = 0; d < 32; ++d)
+        r |= ((w >> d) & 1u) << canonical_bit_of(d);
+    return r;
+}
+
+}  // namespace sbvr

@@ -1,0 +1,112 @@
+"""C-ABI checks that need no GPU: the library loads, exports every entry point
+declared in include/sbvr.h, and rejects bad arguments on the host before any
+HIP call (so nothing is launched and no output is touched)."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+import paper_2509_18172_amd as sb
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "sbvr.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sbvr_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert len(names) >= 9
+    lib = C.CDLL(sb.library_path())
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sorted(sb.EXPORTED) == names
+
+
+def test_status_strings_and_version():
+    assert sb.sbvr_status_string(0) == "SBVR_OK"
+    for code, name in [(-1, "SBVR_E_INVALID_ARG"), (-2, "SBVR_E_UNSUPPORTED"), (-3, "SBVR_E_WORKSPACE"),
+                       (-4, "SBVR_E_ALIGNMENT"), (-5, "SBVR_E_HIP")]:
+        assert sb.sbvr_status_string(code) == name
+    assert sb.sbvr_status_string(12345) == "SBVR_E_UNKNOWN"
+    assert sb.sbvr_version() >= 100
+
+
+@pytest.mark.parametrize("O,I,k", [(4096, 4096, 4), (1, 128, 1), (1001, 640, 3), (14336, 4096, 2)])
+def test_size_queries(O, I, k):
+    G = I // 128
+    tiles, gblocks = -(-O // 4), -(-G // 4)
+    assert sb.sbvr_packed_plane_bytes(O, I, k) == tiles * gblocks * 4 * 4 * k * 16
+    assert sb.sbvr_packed_coeff_bytes(O, I, k) == tiles * gblocks * 4 * 4 * k * 2
+    # never smaller than the canonical tensors
+    assert sb.sbvr_packed_plane_bytes(O, I, k) >= O * G * k * 16
+    assert sb.sbvr_packed_coeff_bytes(O, I, k) >= O * G * k * 2
+    assert sb.sbvr_workspace_bytes(O, I, k, 1) == 0
+
+
+@pytest.mark.parametrize("O,I,k", [(0, 128, 4), (4, 100, 4), (4, 0, 4), (4, 128, 0), (-1, 128, 2)])
+def test_size_queries_reject_bad_shapes(O, I, k):
+    assert sb.sbvr_packed_plane_bytes(O, I, k) == 0
+    assert sb.sbvr_packed_coeff_bytes(O, I, k) == 0
+
+
+FAKE = 1 << 20  # 16-byte-aligned, never dereferenced: every call below fails validation
+
+
+def gemv(O=16, I=256, k=4, p=FAKE, c=FAKE, x=FAKE, y=FAKE, ws=None, wsb=0):
+    return sb.sbvr_gemv(O, I, k, p, c, x, y, ws, wsb, 0)
+
+
+def test_gemv_validation():
+    assert gemv(O=0) == sb.SBVR_E_INVALID_ARG
+    assert gemv(I=130) == sb.SBVR_E_INVALID_ARG
+    assert gemv(I=64) == sb.SBVR_E_INVALID_ARG
+    assert gemv(k=0) == sb.SBVR_E_INVALID_ARG
+    assert gemv(k=5) == sb.SBVR_E_UNSUPPORTED
+    assert gemv(p=None) == sb.SBVR_E_INVALID_ARG
+    assert gemv(c=None) == sb.SBVR_E_INVALID_ARG
+    assert gemv(x=None) == sb.SBVR_E_INVALID_ARG
+    assert gemv(y=None) == sb.SBVR_E_INVALID_ARG
+    assert gemv(p=FAKE + 4) == sb.SBVR_E_ALIGNMENT
+    assert gemv(c=FAKE + 8) == sb.SBVR_E_ALIGNMENT
+    assert gemv(x=FAKE + 2) == sb.SBVR_E_ALIGNMENT
+    assert gemv(y=FAKE + 1) == sb.SBVR_E_ALIGNMENT
+
+
+def test_small_batch_validation():
+    f = lambda B, **kw: sb.sbvr_gemm_small_batch(kw.get("O", 16), 256, kw.get("k", 4), FAKE, FAKE,
+                                                 kw.get("X", FAKE), FAKE, B, None, 0, 0)
+    assert f(0) == sb.SBVR_E_INVALID_ARG
+    assert f(9) == sb.SBVR_E_INVALID_ARG
+    assert f(-3) == sb.SBVR_E_INVALID_ARG
+    assert f(4, X=None) == sb.SBVR_E_INVALID_ARG
+    assert f(4, X=FAKE + 8) == sb.SBVR_E_ALIGNMENT
+    assert f(4, k=7) == sb.SBVR_E_UNSUPPORTED
+
+
+def test_pack_validation():
+    P = lambda **kw: sb.sbvr_pack(kw.get("O", 8), kw.get("I", 256), kw.get("k", 3), kw.get("pc", FAKE),
+                                  kw.get("cc", FAKE), kw.get("pd", FAKE), kw.get("cd", FAKE), 0)
+    U = lambda **kw: sb.sbvr_unpack(kw.get("O", 8), kw.get("I", 256), kw.get("k", 3), kw.get("pd", FAKE),
+                                    kw.get("cd", FAKE), kw.get("pc", FAKE), kw.get("cc", FAKE), 0)
+    for F in (P, U):
+        assert F(O=0) == sb.SBVR_E_INVALID_ARG
+        assert F(I=129) == sb.SBVR_E_INVALID_ARG
+        assert F(k=6) == sb.SBVR_E_UNSUPPORTED
+        assert F(pc=None) == sb.SBVR_E_INVALID_ARG
+        assert F(cd=None) == sb.SBVR_E_INVALID_ARG
+        assert F(pc=FAKE + 4) == sb.SBVR_E_ALIGNMENT
+        assert F(cc=FAKE + 1) == sb.SBVR_E_ALIGNMENT
+        assert F(pd=FAKE + 8) == sb.SBVR_E_ALIGNMENT
+
+
+def test_algorithmic_bytes_formula():
+    # 0.5625 B/weight at k=4 plus activations and outputs
+    assert sb.algorithmic_bytes(4096, 4096, 4) == 9_453_568
+    assert sb.algorithmic_bytes(14336, 4096, 4) == 33_067_008
+    assert sb.algorithmic_bytes(28672, 8192, 4) == 132_194_304
+    assert sb.algorithmic_bytes(4096, 4096, 4, B=8) == 9_568_256

@@ -1,0 +1,361 @@
+"""GPU parity of the HIP SBVR path against the CPU oracle, through the C ABI.
+
+Gate (per activation vector): max_o |y - y_ref| / max_o |y_ref| <= 1e-3, with
+y_ref the binary64 GEMV of the exactly decompressed matrix.  Repacking is
+checked bit for bit.  Inputs are seeded: Gaussian weights encoded by the
+oracle (Algorithm 1) where encoding is fast enough, and directly drawn SBVR
+tensors (uniform planes, Gaussian fp16 coefficients) at the full Llama-3-8B
+and 70B projection shapes, which are the launch configurations the bench
+times.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-3
+
+
+@pytest.fixture(scope="module")
+def sb():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2509_18172_amd as m
+    return m
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def canon_to_dev(planes, coeffs):
+    return dev(planes.view(np.int32)), dev(coeffs.view(np.int16))
+
+
+def packed(sb, planes, coeffs):
+    p, c = canon_to_dev(planes, coeffs)
+    W = sb.pack(p, c)
+    torch.cuda.synchronize()
+    return W
+
+
+def rel_err(y, y_ref):
+    y = np.asarray(y, dtype=np.float64)
+    den = np.abs(y_ref).max()
+    return float(np.abs(y - y_ref).max() / den) if den > 0 else float(np.abs(y).max())
+
+
+def run_gemv(sb, W, x16):
+    y = sb.gemv(W, dev(x16))
+    torch.cuda.synchronize()
+    return y.cpu().numpy().astype(np.float64)
+
+
+def run_gemm(sb, W, X16):
+    Y = sb.gemm_small_batch(W, dev(X16))
+    torch.cuda.synchronize()
+    return Y.cpu().numpy().astype(np.float64)
+
+
+def log(msg):
+    print(msg, flush=True)
+
+
+# --------------------------------------------------------------------------
+# Repacking: bit-exact round trip
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("O,I,k", [(1, 128, 4), (5, 640, 3), (17, 384, 2), (1000, 1024, 1),
+                                   (4096, 4096, 4), (1024, 14336, 4), (9, 896, 4)])
+def test_pack_unpack_round_trip(sb, O, I, k):
+    planes, coeffs = synth.random_sbvr(O, I, k, seed=O * 31 + I + k)
+    W = packed(sb, planes, coeffs)
+    p2, c2 = sb.unpack(W)
+    torch.cuda.synchronize()
+    assert np.array_equal(p2.cpu().numpy().view(np.uint32), planes)
+    assert np.array_equal(c2.cpu().numpy().view(np.uint16), coeffs)
+    assert W.planes.numel() == sb.sbvr_packed_plane_bytes(O, I, k)
+
+
+# --------------------------------------------------------------------------
+# configs: oracle-encoded Gaussian weights
+# --------------------------------------------------------------------------
+
+def test_cfg1_single_gemv_seed0(sb):
+    """1024 x 1024, k = 4, seed 0: W ~ N(0, 0.02^2) encoded by Algorithm 1."""
+    W = synth.weights(1024, 1024, 0.02, seed=0)
+    planes, coeffs = oracle.encode_matrix(W, 4)
+    x = synth.activations(1024, seed=synth.X_SEED_OFFSET)
+    Wd = packed(sb, planes, coeffs)
+    p2, c2 = sb.unpack(Wd)
+    assert np.array_equal(p2.cpu().numpy().view(np.uint32), planes)
+    y = run_gemv(sb, Wd, x)
+    y_ref = oracle.sbvr_gemv(planes, coeffs, x)
+    err = rel_err(y, y_ref)
+    log(f"cfg1 1024x1024 k=4 err={err:.3e}")
+    assert err <= TOL
+
+
+@pytest.mark.parametrize("k", [4, 3, 2])
+@pytest.mark.parametrize("I", [4096, 14336])
+def test_encoded_llama8b_rows_with_outliers(sb, k, I):
+    """Rows of the Llama-3-8B shapes, N(0, 0.02^2) + 0.1% outliers at +-8 sigma."""
+    O = 48
+    W = synth.weights(O, I, 0.02, seed=synth.seed_for(2, 0, 4 if I == 4096 else 6), outlier_frac=0.001)
+    planes, coeffs = oracle.encode_matrix(W, k)
+    x = synth.activations(I, seed=synth.seed_for(2, 0, 4) + synth.X_SEED_OFFSET)
+    y = run_gemv(sb, packed(sb, planes, coeffs), x)
+    err = rel_err(y, oracle.sbvr_gemv(planes, coeffs, x))
+    log(f"encoded {O}x{I} k={k} err={err:.3e}")
+    assert err <= TOL
+
+
+# --------------------------------------------------------------------------
+# Full-size shapes in the bench's launch configuration
+# --------------------------------------------------------------------------
+
+SHAPES_8B = sorted(set(synth.LLAMA8B.values()))
+SHAPES_70B = sorted(set(synth.LLAMA70B.values()))
+
+
+@pytest.mark.parametrize("O,I", SHAPES_8B + SHAPES_70B)
+def test_full_size_k4(sb, O, I):
+    planes, coeffs = synth.random_sbvr(O, I, 4, seed=O + 7 * I)
+    x = synth.activations(I, seed=O + I + synth.X_SEED_OFFSET)
+    y = run_gemv(sb, packed(sb, planes, coeffs), x)
+    y_ref = oracle.sbvr_gemv(planes, coeffs, x)
+    err = rel_err(y, y_ref)
+    log(f"full {O}x{I} k=4 err={err:.3e}")
+    assert err <= TOL
+
+
+@pytest.mark.parametrize("k", [2, 3])
+@pytest.mark.parametrize("O,I", SHAPES_8B)
+def test_full_size_low_bit(sb, O, I, k):
+    planes, coeffs = synth.random_sbvr(O, I, k, seed=O + 7 * I + k)
+    x = synth.activations(I, seed=O + I + k + synth.X_SEED_OFFSET)
+    y = run_gemv(sb, packed(sb, planes, coeffs), x)
+    err = rel_err(y, oracle.sbvr_gemv(planes, coeffs, x))
+    log(f"full {O}x{I} k={k} err={err:.3e}")
+    assert err <= TOL
+
+
+@pytest.mark.parametrize("B", [1, 2, 3, 4, 5, 6, 8])
+@pytest.mark.parametrize("O,I", SHAPES_8B)
+def test_small_batch_full_size(sb, O, I, B):
+    planes, coeffs = synth.random_sbvr(O, I, 4, seed=O + 3 * I)
+    X = synth.activations(I, seed=B + O + synth.X_SEED_OFFSET, batch=B)
+    W = packed(sb, planes, coeffs)
+    Y = run_gemm(sb, W, X)
+    Y_ref = oracle.sbvr_gemv(planes, coeffs, X)
+    errs = [rel_err(Y[b], Y_ref[b]) for b in range(B)]
+    log(f"small batch {O}x{I} B={B} worst err={max(errs):.3e}")
+    assert max(errs) <= TOL
+    # each vector agrees with the batch-1 kernel to the same bar
+    y0 = run_gemv(sb, W, X[0])
+    assert rel_err(Y[0], y0.astype(np.float64)) <= TOL
+
+
+@pytest.mark.parametrize("k", [1, 2, 3])
+def test_small_batch_low_bit(sb, k):
+    O, I = 520, 1920
+    planes, coeffs = synth.random_sbvr(O, I, k, seed=k)
+    X = synth.activations(I, seed=k + 9, batch=6)
+    Y = run_gemm(sb, packed(sb, planes, coeffs), X)
+    Y_ref = oracle.sbvr_gemv(planes, coeffs, X)
+    assert max(rel_err(Y[b], Y_ref[b]) for b in range(6)) <= TOL
+
+
+# --------------------------------------------------------------------------
+# Structured inputs with closed-form answers
+# --------------------------------------------------------------------------
+
+def fp16_ulp(v):
+    v = np.abs(np.asarray(v, dtype=np.float16))
+    return (np.nextafter(v, np.float16(np.inf)) - v).astype(np.float64)
+
+
+def test_unit_vector_picks_a_column(sb):
+    O, I = 256, 1024
+    planes, coeffs = synth.random_sbvr(O, I, 4, seed=4)
+    What = oracle.decompress(planes, coeffs)
+    W = packed(sb, planes, coeffs)
+    for j in (0, 1, 31, 32, 127, 128, 500, 1023):
+        x = np.zeros(I, dtype=np.float16)
+        x[j] = 1.0
+        y = run_gemv(sb, W, x)
+        col = What[:, j]
+        assert np.all(np.abs(y - col.astype(np.float16)) <= fp16_ulp(col)), j
+
+
+def test_zero_planes_give_positive_zero(sb):
+    O, I = 64, 512
+    planes = np.zeros((O, I // 128, 4, 4), dtype=np.uint32)
+    coeffs = synth.random_sbvr(O, I, 4, seed=1)[1]
+    y = sb.gemv(packed(sb, planes, coeffs), dev(synth.activations(I, seed=2)))
+    torch.cuda.synchronize()
+    assert np.all(y.cpu().numpy().view(np.uint16) == 0)
+
+
+def test_all_ones_planes(sb):
+    O, I = 64, 1024
+    planes = np.full((O, I // 128, 3, 4), 0xFFFFFFFF, dtype=np.uint32)
+    coeffs = synth.random_sbvr(O, I, 3, seed=5)[1]
+    x = synth.activations(I, seed=6)
+    y = run_gemv(sb, packed(sb, planes, coeffs), x)
+    cf = coeffs.view(np.float16).astype(np.float64).sum(axis=2)           # [O][G]
+    xs = x.astype(np.float64).reshape(-1, 128).sum(axis=1)                 # [G]
+    assert rel_err(y, cf @ xs) <= TOL
+
+
+@pytest.mark.parametrize("k", [2, 3, 4])
+def test_power_of_two_coefficients_are_integer_codes(sb, k):
+    """c_i = 2^i * delta makes every weight an unsigned k-bit integer code times
+    delta, so y = delta * (Q x) with Q computed in integer arithmetic."""
+    O, I = 200, 2048
+    planes = synth.random_sbvr(O, I, k, seed=10 + k)[0]
+    delta = 2.0 ** -9
+    coeffs = np.broadcast_to(np.array([np.float16(delta * 2 ** i) for i in range(k)]).view(np.uint16),
+                             (O, I // 128, k)).copy()
+    bits = np.unpackbits(planes.view(np.uint8), bitorder="little").reshape(O, I // 128, k, 128)
+    Q = (bits.astype(np.int64) << np.arange(k)[None, None, :, None]).sum(axis=2).reshape(O, I)
+    x = synth.activations(I, seed=20 + k)
+    y_ref = delta * (Q.astype(np.float64) @ x.astype(np.float64))
+    y = run_gemv(sb, packed(sb, planes, coeffs), x)
+    assert rel_err(y, y_ref) <= TOL
+
+
+def test_twos_complement_coefficients(sb):
+    """Eq. 12-style coefficients {-8, 1, 2, 4} * s: signed 4-bit integer codes."""
+    O, I = 96, 1024
+    planes = synth.random_sbvr(O, I, 4, seed=33)[0]
+    s = 2.0 ** -6
+    coeffs = np.broadcast_to(np.array([np.float16(v * s) for v in (-8, 1, 2, 4)]).view(np.uint16),
+                             (O, I // 128, 4)).copy()
+    # plane order (i = 0..3) pairs with (-8, 1, 2, 4)
+    bits = np.unpackbits(planes.view(np.uint8), bitorder="little").reshape(O, I // 128, 4, 128)
+    Q = (bits.astype(np.int64) * np.array([-8, 1, 2, 4])[None, None, :, None]).sum(axis=2).reshape(O, I)
+    x = synth.activations(I, seed=34)
+    y = run_gemv(sb, packed(sb, planes, coeffs), x)
+    assert rel_err(y, s * (Q.astype(np.float64) @ x.astype(np.float64))) <= TOL
+
+
+def test_linearity_and_determinism(sb):
+    O, I = 4096, 4096
+    planes, coeffs = synth.random_sbvr(O, I, 4, seed=77)
+    W = packed(sb, planes, coeffs)
+    x1 = synth.activations(I, seed=1).astype(np.float32)
+    x2 = synth.activations(I, seed=2).astype(np.float32)
+    x12 = (x1 + x2).astype(np.float16)
+    y1 = run_gemv(sb, W, x1.astype(np.float16))
+    y2 = run_gemv(sb, W, x2.astype(np.float16))
+    y12 = run_gemv(sb, W, x12)
+    ref12 = oracle.sbvr_gemv(planes, coeffs, x12)
+    assert rel_err(y12, ref12) <= TOL
+    assert rel_err(y1 + y2, ref12) <= 5 * TOL  # x1+x2 itself rounds to fp16
+    again = run_gemv(sb, W, x12)
+    assert np.array_equal(again, y12)  # fixed reduction order -> bit-identical reruns
+
+
+# --------------------------------------------------------------------------
+# Edge cases
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("O,I,k", [(1, 128, 4), (3, 128, 1), (1001, 640, 3), (7, 896, 4),
+                                   (4097, 1152, 2), (130, 4224, 4), (2, 30720, 4)])
+def test_ragged_shapes(sb, O, I, k):
+    planes, coeffs = synth.random_sbvr(O, I, k, seed=O + I + k)
+    x = synth.activations(I, seed=O * 3 + 1)
+    W = packed(sb, planes, coeffs)
+    y_ref = oracle.sbvr_gemv(planes, coeffs, x)
+    assert rel_err(run_gemv(sb, W, x), y_ref) <= TOL
+    X = synth.activations(I, seed=O * 5 + 2, batch=3)
+    Y = run_gemm(sb, W, X)
+    Y_ref = oracle.sbvr_gemv(planes, coeffs, X)
+    assert max(rel_err(Y[b], Y_ref[b]) for b in range(3)) <= TOL
+
+
+def test_activation_dynamic_range(sb):
+    O, I = 128, 2048
+    planes, coeffs = synth.random_sbvr(O, I, 4, seed=90, coeff_sigma=1e-4)
+    W = packed(sb, planes, coeffs)
+    rng = np.random.default_rng(0)
+    # (activations, coefficient scale): y stays within the fp16 normal range
+    cases = {
+        "huge": (np.full(I, 60000.0), 1.0),
+        "tiny": (rng.standard_normal(I) * 1e-6, 1e4),          # fp16 subnormal x
+        "mixed": (np.where(rng.random(I) < 0.01, 3000.0, 1e-3) * rng.choice([-1, 1], I), 1.0),
+        "zero": (np.zeros(I), 1.0),
+        "one_big": (np.r_[65504.0, np.full(I - 1, 2.0 ** -24)], 1.0),
+    }
+    W_big = packed(sb, planes, (coeffs.view(np.float16) * np.float16(1e4)).view(np.uint16))
+    for name, (xv, cscale) in cases.items():
+        W = W_big if cscale != 1.0 else packed(sb, planes, coeffs)
+        c_used = coeffs if cscale == 1.0 else (coeffs.view(np.float16) * np.float16(1e4)).view(np.uint16)
+        x = xv.astype(np.float16)
+        y_ref = oracle.sbvr_gemv(planes, c_used, x)
+        y = run_gemv(sb, W, x)
+        if np.abs(y_ref).max() == 0:
+            assert np.all(y == 0), name
+        else:
+            assert rel_err(y, y_ref) <= TOL, (name, rel_err(y, y_ref))
+
+
+def test_output_canary_and_error_paths(sb):
+    O, I = 100, 512
+    planes, coeffs = synth.random_sbvr(O, I, 4, seed=3)
+    W = packed(sb, planes, coeffs)
+    x = dev(synth.activations(I, seed=4))
+    buf = torch.full((O + 64,), 7.0, dtype=torch.float16, device="cuda")
+    st = sb.sbvr_gemv(O, I, 4, W.planes.data_ptr(), W.coeffs.data_ptr(), x.data_ptr(),
+                      buf.data_ptr(), None, 0, 0)
+    torch.cuda.synchronize()
+    assert st == 0
+    assert torch.all(buf[O:] == 7.0)
+    y_ref = oracle.sbvr_gemv(planes, coeffs, synth.activations(I, seed=4))
+    assert rel_err(buf[:O].cpu().numpy().astype(np.float64), y_ref) <= TOL
+    # invalid calls launch nothing: output untouched
+    buf.fill_(5.0)
+    torch.cuda.synchronize()
+    for args in [(O, I, 5), (O, 100, 4), (0, I, 4)]:
+        st = sb.sbvr_gemv(*args, W.planes.data_ptr(), W.coeffs.data_ptr(), x.data_ptr(),
+                          buf.data_ptr(), None, 0, 0)
+        assert st != 0
+    st = sb.sbvr_gemv(O, I, 4, W.planes.data_ptr(), W.coeffs.data_ptr(), x.data_ptr() + 2,
+                      buf.data_ptr(), None, 0, 0)
+    assert st == sb.SBVR_E_ALIGNMENT
+    st = sb.sbvr_gemm_small_batch(O, I, 4, W.planes.data_ptr(), W.coeffs.data_ptr(), x.data_ptr(),
+                                  buf.data_ptr(), 9, None, 0, 0)
+    assert st == sb.SBVR_E_INVALID_ARG
+    torch.cuda.synchronize()
+    assert torch.all(buf == 5.0)
+
+
+def test_graph_capture_replays_match_eager(sb):
+    O, I = 4096, 4096
+    planes, coeffs = synth.random_sbvr(O, I, 4, seed=123)
+    W = packed(sb, planes, coeffs)
+    x = dev(synth.activations(I, seed=124))
+    X = dev(synth.activations(I, seed=125, batch=4))
+    y_eager = sb.gemv(W, x).clone()
+    Y_eager = sb.gemm_small_batch(W, X).clone()
+    y = torch.empty_like(y_eager)
+    Y = torch.empty_like(Y_eager)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        sb.gemv(W, x, out=y)
+        sb.gemm_small_batch(W, X, out=Y)
+    for rep in range(4):
+        y.zero_()
+        Y.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y, y_eager), rep
+        assert torch.equal(Y, Y_eager), rep
+        _ = (x.float() * 2).sum().item()  # eager work between replays
