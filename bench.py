@@ -4,21 +4,25 @@
 A step is one decoder layer's seven SBVR GEMVs (q, k, v, o, gate, up, down)
 at batch 1 with 4-bit SBVR weights (k = 4 planes, 128-weight groups, fp16
 coefficients), fp16 activations and outputs, in the Llama-3-8B projection
-shapes (or 70B with --model llama3-70b).  Steps cycle through L independent
-layers of weights so the rotated working set (~1.9 GiB) exceeds every cache
-and the bytes really come from HBM.  Each layer's seven calls are captured in
-a HIP graph, as decode steps are served.
+shapes (Llama-3-70B with --model llama3-70b).  Steps cycle through L
+independent layers of weights so the rotated working set (~1.9 GiB) exceeds
+every cache and the bytes really come from HBM.  Each layer's seven calls
+are captured in one HIP graph, as decode steps are served.
 
 Weights are drawn directly in SBVR form (uniform bit planes, Gaussian fp16
 coefficients, seeded): GEMV time does not depend on the values.  The parity
 tests run these same shapes and launch configurations against the CPU oracle.
 
-Prints one JSON line:
-  value      aggregate algorithmic HBM throughput (GB/s) over the timed steps
-  roofline   the dominant GEMV kernel: algorithmic bytes per launch / its mean
-             launch duration (HIP events inside the timed graphs), vs 8 TB/s
-  cpu_baseline  the CPU oracle (binary64 decompress + GEMV) on one layer,
-             bounded to ~10 s, in the same units
+One JSON line is printed:
+  value         aggregate algorithmic HBM throughput (GB/s) of the timed steps
+  per_call_us   mean duration of each projection's launch, from HIP events
+                around a graph of L back-to-back launches of that shape (one
+                per layer) on the launch stream
+  roofline      the dominant kernel instance (largest time per step):
+                algorithmic bytes per launch / its mean launch duration, vs the
+                8 TB/s HBM peak
+  cpu_baseline  the CPU oracle (binary64 decompress + GEMV) on layer 0's seven
+                GEMVs, bounded to ~10 s of work, in the same unit
 """
 from __future__ import annotations
 
@@ -46,22 +50,23 @@ def parse():
     ap.add_argument("--k", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
-    ap.add_argument("--no-events", action="store_true", help="plain graphs (for profiler runs)")
     return ap.parse_args()
 
 
-def b1_tiles_per_workgroup(O: int) -> int:
-    """Mirror of the library's batch-1 launch choice (rows per workgroup / 4);
-    it names the kernel instance, gemv_b1_kernel<T>, a launch runs."""
+def b1_kernel_instance(O: int, k: int) -> str:
+    """Name of the batch-1 kernel instance a launch with O rows runs: the
+    library takes T tiles (4T rows) per workgroup, the most of 8/4/2/1 that
+    still leaves >= 256 workgroups."""
     n_tiles = (O + 3) // 4
-    return 4 if n_tiles >= 1024 else (2 if n_tiles >= 512 else 1)
+    T = next((t for t in (8, 4, 2) if n_tiles // t >= 256), 1)
+    return f"gemv_b1_kernel<{k}, {T}>"
 
 
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the SBVR GEMV path "
-              "has no multi-GPU mode in this build.", file=sys.stderr)
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the SBVR GEMV path "
+              "has no multi-GPU mode.", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
@@ -74,7 +79,8 @@ def main():
     dev = torch.device("cuda:0")
     shapes = synth.LLAMA8B if args.model == "llama3-8b" else synth.LLAMA70B
     k = args.k
-    layer_bytes = sum(sb.algorithmic_bytes(O, I, k) for O, I in shapes.values())
+    nbytes = {n: sb.algorithmic_bytes(*shapes[n], k) for n in PROJ_ORDER}
+    layer_bytes = sum(nbytes.values())
     L = args.layers or max(2, int(np.ceil(1.9 * 2 ** 30 / layer_bytes)))
     cfg_index = 1 if args.model == "llama3-8b" else 3
 
@@ -85,116 +91,79 @@ def main():
         lay = {}
         for pi, name in enumerate(PROJ_ORDER):
             O, I = shapes[name]
-            planes, coeffs = synth.random_sbvr(O, I, k, seed=synth.seed_for(cfg_index, li, pi))
+            seed = synth.seed_for(cfg_index, li, pi)
+            planes, coeffs = synth.random_sbvr(O, I, k, seed=seed)
             if li == 0:
                 host_layer0[name] = (planes, coeffs)
             W = sb.pack(torch.from_numpy(planes.view(np.int32)).to(dev),
                         torch.from_numpy(coeffs.view(np.int16)).to(dev))
-            x = torch.from_numpy(synth.activations(
-                I, seed=synth.seed_for(cfg_index, li, pi) + synth.X_SEED_OFFSET)).to(dev)
+            x = torch.from_numpy(synth.activations(I, seed=seed + synth.X_SEED_OFFSET)).to(dev)
             y = torch.empty(O, dtype=torch.float16, device=dev)
             lay[name] = (W, x, y)
         layers.append(lay)
         torch.cuda.synchronize()
 
-    # ---- one graph per timed step slot, with timing events around each call ----
     stream = torch.cuda.Stream()
-    n_graph = L if args.no_events else max(L, args.steps)
-    use_events = not args.no_events
-    graphs, events = [], []
     with torch.cuda.stream(stream):
         for name in PROJ_ORDER:  # eager warm-up of every shape before capture
             W, x, y = layers[0][name]
-            sb.gemv(W, x, out=y)
+            sb.gemv(W, x, out=y, stream=stream)
     torch.cuda.synchronize()
 
-    def capture(lay, with_events):
+    def capture(calls):
         g = torch.cuda.CUDAGraph()
-        evs = []
         with torch.cuda.graph(g, stream=stream):
-            for name in PROJ_ORDER:
-                W, x, y = lay[name]
-                if with_events:
-                    e0 = torch.cuda.Event(enable_timing=True, external=True)
-                    e1 = torch.cuda.Event(enable_timing=True, external=True)
-                    e0.record(stream)
-                    sb.gemv(W, x, out=y, stream=stream)
-                    e1.record(stream)
-                    evs.append((name, e0, e1))
-                else:
-                    sb.gemv(W, x, out=y, stream=stream)
-        return g, evs
+            for W, x, y in calls:
+                sb.gemv(W, x, out=y, stream=stream)
+        return g
 
-    event_note = "HIP events around every GEMV inside the timed graphs"
-    try:
-        for gi in range(n_graph):
-            g, evs = capture(layers[gi % L], use_events)
-            graphs.append(g)
-            events.append(evs)
-    except Exception as exc:  # event nodes unsupported: plain graphs + separate event pass
-        use_events = False
-        event_note = f"plain graphs (event capture failed: {type(exc).__name__}); per-kernel events from eager calls"
-        graphs, events = [], []
-        for gi in range(L):
-            g, _ = capture(layers[gi], False)
-            graphs.append(g)
-        n_graph = L
-    torch.cuda.synchronize()
+    def timed_replays(graphs, n):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(stream):
+            e0.record(stream)
+            for i in range(n):
+                graphs[i % len(graphs)].replay()
+            e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1)  # ms
 
-    # ---- warmup + timed region ----
-    for s in range(args.warmup):
-        graphs[s % n_graph].replay()
+    # ---- timed region: K steps, one layer graph per step ----
+    step_graphs = [capture([layers[li][n] for n in PROJ_ORDER]) for li in range(L)]
     torch.cuda.synchronize()
-    t0 = torch.cuda.Event(enable_timing=True)
-    t1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    with torch.cuda.stream(stream):
-        t0.record(stream)
-        for s in range(args.steps):
-            graphs[s % n_graph].replay()
-        t1.record(stream)
-    torch.cuda.synchronize()
-    total_ms = t0.elapsed_time(t1)
+    if args.warmup:
+        timed_replays(step_graphs, args.warmup)
+    total_ms = timed_replays(step_graphs, args.steps)
     ms_per_step = total_ms / args.steps
     value = layer_bytes * args.steps / (total_ms * 1e-3) / 1e9
 
-    # ---- per-call durations ----
-    per_call = {name: [] for name in PROJ_ORDER}
-    if use_events:
-        for s in range(min(args.steps, n_graph)):
-            for name, e0, e1 in events[s]:
-                per_call[name].append(e0.elapsed_time(e1) * 1e3)
-    else:
-        for rep in range(4):
-            for li in range(L):
-                for name in PROJ_ORDER:
-                    W, x, y = layers[li][name]
-                    e0 = torch.cuda.Event(enable_timing=True)
-                    e1 = torch.cuda.Event(enable_timing=True)
-                    e0.record(stream)
-                    sb.gemv(W, x, out=y, stream=stream)
-                    e1.record(stream)
-                    torch.cuda.synchronize()
-                    per_call[name].append(e0.elapsed_time(e1) * 1e3)
-    per_call_us = {n: float(np.mean(v)) for n, v in per_call.items() if v}
-    per_call_gbps = {n: sb.algorithmic_bytes(*shapes[n], k) / (per_call_us[n] * 1e3)
-                     for n in per_call_us}
+    # ---- per-shape launch durations: L back-to-back launches per graph ----
+    per_call_us = {}
+    for name in PROJ_ORDER:
+        g = capture([layers[li][name] for li in range(L)])
+        timed_replays([g], 1)
+        reps = [timed_replays([g], 1) * 1e3 / L for _ in range(3)]
+        per_call_us[name] = float(np.median(reps))
+        del g
+    per_call_gbps = {n: nbytes[n] / (per_call_us[n] * 1e3) for n in PROJ_ORDER}
 
-    # dominant kernel instance: the one with the largest total time
+    # dominant kernel instance: largest launch time per step
     by_kernel = {}
     for n in PROJ_ORDER:
-        kname = f"gemv_b1_kernel<{b1_tiles_per_workgroup(shapes[n][0])}>"
+        kname = b1_kernel_instance(shapes[n][0], k)
         t, b, c = by_kernel.get(kname, (0.0, 0, 0))
-        by_kernel[kname] = (t + per_call_us[n], b + sb.algorithmic_bytes(*shapes[n], k), c + 1)
+        by_kernel[kname] = (t + per_call_us[n], b + nbytes[n], c + 1)
     dom = max(by_kernel, key=lambda kk: by_kernel[kk][0])
     dt, db, dc = by_kernel[dom]
-    achieved = db / (dt * 1e3)  # bytes per launch / mean duration, GB/s
+    achieved = db / (dt * 1e3)  # (bytes per launch) / (mean launch duration), GB/s
     roofline = {
         "bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_GBPS, "unit": "GB/s",
         "frac": round(achieved / PEAK_GBPS, 4), "traffic": None,
-        "kernel": dom, "launches_per_step": dc,
-        "bytes_per_launch": db / dc, "mean_launch_us": dt / dc,
-        "timing": event_note,
+        "kernel": dom,
+        "launches_per_step": dc,
+        "projections": [n for n in PROJ_ORDER if b1_kernel_instance(shapes[n][0], k) == dom],
+        "bytes_per_launch": round(db / dc),
+        "mean_launch_us": round(dt / dc, 3),
     }
 
     # ---- CPU baseline: the oracle on layer 0, bounded ----
@@ -209,13 +178,13 @@ def main():
                 ts = time.perf_counter()
                 _, threads = oracle.sbvr_gemv(planes, coeffs, x, return_threads=True)
                 elapsed += time.perf_counter() - ts
-                done_bytes += sb.algorithmic_bytes(*shapes[name], k)
+                done_bytes += nbytes[name]
             passes += 1
         cpu = {"value": round(done_bytes / elapsed / 1e9, 4), "unit": "GB/s", "cores": threads,
                "kind": "oracle",
-               "sample": f"{passes} pass(es) over layer 0's seven GEMVs ({args.model}, k={k}, batch 1), "
-                         f"{elapsed:.1f} s; binary64 decompress + GEMV, {threads} threads on "
-                         f"{os.cpu_count()} host CPUs ({platform.processor() or platform.machine()})"}
+               "sample": f"{passes} pass(es) over layer 0's seven GEMVs ({args.model}, k={k}, batch 1): "
+                         f"{elapsed:.1f} s of binary64 decompress + GEMV on {threads} threads "
+                         f"({os.cpu_count()} host CPUs, {platform.machine()})"}
 
     out = {
         "metric": "SBVR GEMV us/call and achieved HBM GB/s (% of MI355X peak), 4-bit, batch 1",
@@ -228,11 +197,11 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "fp16 activations/outputs, fp32 accumulation, SBVR k=%d weights" % k,
-        "data": "synthetic: seeded SBVR planes/coefficients, N(0,1) fp16 activations",
+        "dtype": "f16 in/out, f32 accumulate",
+        "data": "synthetic: seeded SBVR planes and fp16 coefficients, N(0,1) fp16 activations",
         "config": {
             "workload": f"{args.model} decode-layer projections q,k,v,o,gate,up,down; SBVR k={k}, "
-                        f"group 128, batch 1; {L} rotating layers; hipGraph per layer",
+                        f"group 128, batch 1; {L} rotating layers; one hipGraph per layer",
             "bytes_per_step": layer_bytes,
             "layers_rotated": L,
             "shapes": {n: list(shapes[n]) for n in PROJ_ORDER},

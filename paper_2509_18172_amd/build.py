@@ -1,5 +1,6 @@
-"""Build step for the HIP library: compiles csrc/sbvr.hip for gfx950 into
-_lib/libsbvr.so (in-tree, so the built library travels with the source)."""
+"""Build step for the HIP library: compiles csrc/*.hip for gfx950 into
+_lib/libsbvr.so (in-tree, so the built library travels with the source).
+``defines`` (NAME=VALUE) override launch-shape tuning macros for sweeps."""
 from __future__ import annotations
 
 import os
@@ -7,7 +8,7 @@ import subprocess
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
-SRC = os.path.join(HERE, "csrc", "sbvr.hip")
+SOURCES = [os.path.join(HERE, "csrc", f) for f in ("api.hip", "pack.hip", "gemv_b1.hip", "gemm_sb.hip")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [
@@ -22,12 +23,12 @@ def library_path() -> str:
     return os.path.join(HERE, "_lib", "libsbvr.so")
 
 
-def build(verbose: bool = False) -> str:
-    out = library_path()
+def build(verbose: bool = False, out: str | None = None, defines=()) -> str:
+    out = out or library_path()
     os.makedirs(os.path.dirname(out), exist_ok=True)
     tmp = out + ".tmp%d" % os.getpid()
-    cmd = [HIPCC, *FLAGS, "-I", os.path.join(ROOT, "include"), "-I", os.path.join(HERE, "csrc"),
-           SRC, "-o", tmp]
+    cmd = [HIPCC, *FLAGS, *("-D" + d for d in defines), "-I", os.path.join(ROOT, "include"),
+           "-I", os.path.join(HERE, "csrc"), *SOURCES, "-o", tmp]
     if verbose:
         print(" ".join(cmd))
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -1,0 +1,135 @@
+// C ABI of libsbvr (include/sbvr.h): argument validation, then dispatch to the
+// kernel launchers.  Validation happens entirely on the host before any HIP
+// call, so a rejected call enqueues nothing and touches no output.
+#include <stdint.h>
+
+#include "launch.h"
+#include "sbvr.h"
+
+using namespace sbvr;
+
+namespace {
+
+bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+int check_shape(int O, int I, int k)
+{
+    if (O < 1 || I < GROUP || I % GROUP != 0 || k < 1)
+        return SBVR_E_INVALID_ARG;
+    if (k > MAX_K)
+        return SBVR_E_UNSUPPORTED;
+    // element offsets inside the kernels are 32-bit
+    if ((long long)O * I > (1ll << 31) - 1)
+        return SBVR_E_UNSUPPORTED;
+    return SBVR_OK;
+}
+
+int check_repack(int O, int I, int k, const void *planes_canon, const void *coeffs_canon,
+                 const void *planes_dev, const void *coeffs_dev)
+{
+    int st = check_shape(O, I, k);
+    if (st != SBVR_OK)
+        return st;
+    if (!planes_canon || !coeffs_canon || !planes_dev || !coeffs_dev)
+        return SBVR_E_INVALID_ARG;
+    if (!aligned(planes_canon, 16) || !aligned(coeffs_canon, 2) || !aligned(planes_dev, 16) ||
+        !aligned(coeffs_dev, 16))
+        return SBVR_E_ALIGNMENT;
+    return SBVR_OK;
+}
+
+int check_gemv(int O, int I, int k, const void *planes_dev, const void *coeffs_dev,
+               const uint16_t *x, const uint16_t *y, int B, size_t ws_bytes)
+{
+    int st = check_shape(O, I, k);
+    if (st != SBVR_OK)
+        return st;
+    if (B < 1 || B > 8)
+        return SBVR_E_INVALID_ARG;
+    if (!planes_dev || !coeffs_dev || !x || !y)
+        return SBVR_E_INVALID_ARG;
+    if (!aligned(planes_dev, 16) || !aligned(coeffs_dev, 16) || !aligned(x, 16) || !aligned(y, 2))
+        return SBVR_E_ALIGNMENT;
+    if (ws_bytes < sbvr_workspace_bytes(O, I, k, B))
+        return SBVR_E_WORKSPACE;
+    return SBVR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *sbvr_status_string(int status)
+{
+    switch (status) {
+    case SBVR_OK: return "SBVR_OK";
+    case SBVR_E_INVALID_ARG: return "SBVR_E_INVALID_ARG";
+    case SBVR_E_UNSUPPORTED: return "SBVR_E_UNSUPPORTED";
+    case SBVR_E_WORKSPACE: return "SBVR_E_WORKSPACE";
+    case SBVR_E_ALIGNMENT: return "SBVR_E_ALIGNMENT";
+    case SBVR_E_HIP: return "SBVR_E_HIP";
+    default: return "SBVR_E_UNKNOWN";
+    }
+}
+
+int sbvr_version(void) { return 100; }
+
+size_t sbvr_packed_plane_bytes(int O, int I, int k)
+{
+    return check_shape(O, I, k) == SBVR_OK ? plane_bytes(make_dims(O, I, k)) : 0;
+}
+
+size_t sbvr_packed_coeff_bytes(int O, int I, int k)
+{
+    return check_shape(O, I, k) == SBVR_OK ? coeff_bytes(make_dims(O, I, k)) : 0;
+}
+
+size_t sbvr_workspace_bytes(int O, int I, int k, int B)
+{
+    (void)O;
+    (void)I;
+    (void)k;
+    (void)B;
+    return 0;
+}
+
+int sbvr_pack(int O, int I, int k, const uint32_t *planes_canon, const uint16_t *coeffs_canon,
+              void *planes_dev, void *coeffs_dev, hipStream_t stream)
+{
+    int st = check_repack(O, I, k, planes_canon, coeffs_canon, planes_dev, coeffs_dev);
+    if (st != SBVR_OK)
+        return st;
+    return launch_pack(make_dims(O, I, k), planes_canon, coeffs_canon, planes_dev, coeffs_dev, stream);
+}
+
+int sbvr_unpack(int O, int I, int k, const void *planes_dev, const void *coeffs_dev,
+                uint32_t *planes_canon, uint16_t *coeffs_canon, hipStream_t stream)
+{
+    int st = check_repack(O, I, k, planes_canon, coeffs_canon, planes_dev, coeffs_dev);
+    if (st != SBVR_OK)
+        return st;
+    return launch_unpack(make_dims(O, I, k), planes_dev, coeffs_dev, planes_canon, coeffs_canon, stream);
+}
+
+int sbvr_gemv(int O, int I, int k, const void *planes_dev, const void *coeffs_dev,
+              const uint16_t *x, uint16_t *y, void *workspace, size_t ws_bytes, hipStream_t stream)
+{
+    (void)workspace;
+    int st = check_gemv(O, I, k, planes_dev, coeffs_dev, x, y, 1, ws_bytes);
+    if (st != SBVR_OK)
+        return st;
+    return launch_gemv_b1(make_dims(O, I, k), planes_dev, coeffs_dev, x, y, stream);
+}
+
+int sbvr_gemm_small_batch(int O, int I, int k, const void *planes_dev, const void *coeffs_dev,
+                          const uint16_t *X, uint16_t *Y, int B, void *workspace, size_t ws_bytes,
+                          hipStream_t stream)
+{
+    (void)workspace;
+    int st = check_gemv(O, I, k, planes_dev, coeffs_dev, X, Y, B, ws_bytes);
+    if (st != SBVR_OK)
+        return st;
+    return launch_gemm_sb(make_dims(O, I, k), planes_dev, coeffs_dev, X, Y, B, stream);
+}
+
+}  // extern "C"

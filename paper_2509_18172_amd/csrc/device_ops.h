@@ -1,0 +1,219 @@
+// Device-side building blocks of the SBVR GEMV kernels for gfx950.
+//
+// The per-plane masked sums of Sec. 4.4 (S = sum of x over the set bits of a
+// plane) are a bit-matrix times vector product.  Here it runs on the matrix
+// cores as an fp4 x fp8 product:
+//
+//   * A operand (weights): each 32-bit device plane word w becomes four fp4
+//     (E2M1) registers by masking: register v keeps bit v of every nibble, so
+//     nibble p holds element 8v+p of the word as 0 or alpha_v with
+//     alpha = (0.5, 1, 2, 2) (bit 3, the fp4 sign, is shifted down to bit 2).
+//     No per-element work is done on the bits.
+//   * B operand (activations): each binary16 activation, scaled by a power of
+//     two 2^sigma / alpha_v, is split exactly into three fp8 (E4M3) limbs
+//     hi + mid + lo (each limb is the round-to-nearest E4M3 value of what the
+//     previous limbs left), so alpha_v * (hi + mid + lo) = 2^sigma * x.
+//   * v_mfma_scale_f32_16x16x128_f8f6f4 with unit scales multiplies and sums
+//     128 k-slots per row in fp32.
+#pragma once
+
+#include <hip/hip_fp16.h>
+#include <hip/hip_runtime.h>
+
+#include "layout.h"
+
+namespace sbvr {
+
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+// fp4 A operand of one device plane word (registers 4..7 unused by fp4).
+__device__ __forceinline__ v8i fp4_operand(uint32_t w)
+{
+    v8i a;
+    a[0] = (int)(w & 0x11111111u);
+    a[1] = (int)(w & 0x22222222u);
+    a[2] = (int)(w & 0x44444444u);
+    a[3] = (int)((w >> 1) & 0x44444444u);
+    a[4] = 0;
+    a[5] = 0;
+    a[6] = 0;
+    a[7] = 0;
+    return a;
+}
+
+// log2(1 / alpha_v) for the elements of register v = (element in word) / 8.
+__device__ __forceinline__ int inv_alpha_exp(int v) { return v == 0 ? 1 : (v == 1 ? 0 : -1); }
+
+__device__ __forceinline__ float half_bits_to_float(uint32_t bits16)
+{
+    return __half2float(__ushort_as_half((unsigned short)bits16));
+}
+
+__device__ __forceinline__ float absmax8(uint4 v)
+{
+    float m = 0.f;
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        m = fmaxf(m, fabsf(half_bits_to_float(w[i] & 0xffffu)));
+        m = fmaxf(m, fabsf(half_bits_to_float(w[i] >> 16)));
+    }
+    return m;
+}
+
+// DPP lane exchange within rows of 16 lanes.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v)
+{
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xf, 0xf, false));
+}
+constexpr int DPP_QUAD_XOR1 = 0xB1;       // quad_perm [1,0,3,2]
+constexpr int DPP_QUAD_XOR2 = 0x4E;       // quad_perm [2,3,0,1]
+constexpr int DPP_ROW_HALF_MIRROR = 0x141;
+constexpr int DPP_ROW_MIRROR = 0x140;
+
+// Sum over each row of 16 lanes; every lane of the row gets the row sum,
+// always added in the same order for a given lane.
+__device__ __forceinline__ float row16_sum(float v)
+{
+    v += dpp_f32<DPP_QUAD_XOR1>(v);
+    v += dpp_f32<DPP_QUAD_XOR2>(v);
+    v += dpp_f32<DPP_ROW_HALF_MIRROR>(v);
+    v += dpp_f32<DPP_ROW_MIRROR>(v);
+    return v;
+}
+
+// Maximum over the wavefront, returned uniformly.
+__device__ __forceinline__ float wave_max(float v)
+{
+    v = fmaxf(v, dpp_f32<DPP_QUAD_XOR1>(v));
+    v = fmaxf(v, dpp_f32<DPP_QUAD_XOR2>(v));
+    v = fmaxf(v, dpp_f32<DPP_ROW_HALF_MIRROR>(v));
+    v = fmaxf(v, dpp_f32<DPP_ROW_MIRROR>(v));
+    const float m0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+    const float m1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
+    const float m2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+    const float m3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+    return fmaxf(fmaxf(m0, m1), fmaxf(m2, m3));
+}
+
+// Wavefront index within the workgroup as a scalar (uniform) value.
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
+
+// Power-of-two exponent sigma with max|x| * 2^sigma in [64, 128): scaled
+// activations times 1/alpha (<= 2) stay below the E4M3 maximum of 448.
+__device__ __forceinline__ int scale_exponent(float amax)
+{
+    if (!(amax > 0.f))
+        return 0;
+    int e;
+    frexpf(amax, &e);
+    return 7 - e;
+}
+
+// Three E4M3 limbs of eight scaled activations, two words each (bytes in
+// element order).
+struct Limbs {
+    uint32_t hi[2], mid[2], lo[2];
+};
+
+__device__ __forceinline__ void pack8_fp8(const float *v, uint32_t *out)
+{
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        int w = __builtin_amdgcn_cvt_pk_fp8_f32(v[4 * h + 0], v[4 * h + 1], 0, false);
+        w = __builtin_amdgcn_cvt_pk_fp8_f32(v[4 * h + 2], v[4 * h + 3], w, true);
+        out[h] = (uint32_t)w;
+    }
+}
+
+__device__ __forceinline__ void sub_fp8(float *v, const uint32_t *q)
+{
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int w = (int)q[h];
+        v[4 * h + 0] -= __builtin_amdgcn_cvt_f32_fp8(w, 0);
+        v[4 * h + 1] -= __builtin_amdgcn_cvt_f32_fp8(w, 1);
+        v[4 * h + 2] -= __builtin_amdgcn_cvt_f32_fp8(w, 2);
+        v[4 * h + 3] -= __builtin_amdgcn_cvt_f32_fp8(w, 3);
+    }
+}
+
+// Eight binary16 activations (one uint4) times `scale` -> three limbs.
+__device__ __forceinline__ Limbs make_limbs(uint4 xv, float scale)
+{
+    float y[8];
+    const uint32_t w[4] = {xv.x, xv.y, xv.z, xv.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        y[2 * i] = half_bits_to_float(w[i] & 0xffffu) * scale;
+        y[2 * i + 1] = half_bits_to_float(w[i] >> 16) * scale;
+    }
+    Limbs L;
+    pack8_fp8(y, L.hi);
+    sub_fp8(y, L.hi);
+    pack8_fp8(y, L.mid);
+    sub_fp8(y, L.mid);
+    pack8_fp8(y, L.lo);
+    return L;
+}
+
+__device__ __forceinline__ v4f mfma_fp4_fp8(const v8i &a, const v8i &b, const v4f &c)
+{
+    // A: fp4 E2M1 (cbsz = 4), B: fp8 E4M3 (blgp = 0), unit E8M0 scales (127).
+    return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 4, 0, 0, 127, 0, 127);
+}
+
+// An 8-register fp8 B operand from two 16-byte LDS chunks (k-slot halves).
+__device__ __forceinline__ v8i lds_operand(const unsigned char *lo, const unsigned char *hi)
+{
+    const uint4 l = *(const uint4 *)lo;
+    const uint4 h = *(const uint4 *)hi;
+    v8i r;
+    r[0] = (int)l.x;
+    r[1] = (int)l.y;
+    r[2] = (int)l.z;
+    r[3] = (int)l.w;
+    r[4] = (int)h.x;
+    r[5] = (int)h.y;
+    r[6] = (int)h.z;
+    r[7] = (int)h.w;
+    return r;
+}
+
+// K coefficients of one (row, group) of a device coefficient block, as raw
+// binary16 words (c0 | c1 << 16, c2 | c3 << 16); planes >= K read as zero.
+template <int K>
+__device__ __forceinline__ uint2 load_coeffs(const uint16_t *p)
+{
+    if constexpr (K == 4) {
+        return *(const uint2 *)p;
+    } else if constexpr (K == 2) {
+        return make_uint2(*(const uint32_t *)p, 0u);
+    } else if constexpr (K == 3) {
+        return make_uint2((uint32_t)p[0] | ((uint32_t)p[1] << 16), (uint32_t)p[2]);
+    } else {
+        return make_uint2((uint32_t)p[0], 0u);
+    }
+}
+
+// sum_r c_r * d_r over the four D rows (planes) of a lane.
+__device__ __forceinline__ float apply_coeffs(uint2 c, const v4f &d)
+{
+    float s = half_bits_to_float(c.x & 0xffffu) * d[0];
+    s = fmaf(half_bits_to_float(c.x >> 16), d[1], s);
+    s = fmaf(half_bits_to_float(c.y & 0xffffu), d[2], s);
+    s = fmaf(half_bits_to_float(c.y >> 16), d[3], s);
+    return s;
+}
+
+struct GemvArgs {
+    const uint4 *planes;    // device plane blocks
+    const uint16_t *coeffs; // device coefficient blocks
+    const uint16_t *x;      // binary16 [B][I]
+    uint16_t *y;            // binary16 [B][O]
+    int O, I, k, n_tiles, n_gblocks, gpw, B;
+};
+
+}  // namespace sbvr

@@ -1,0 +1,28 @@
+// Host-side launchers of the SBVR kernels (internal to libsbvr).  Arguments
+// are validated by the C ABI layer before these are called; each returns an
+// sbvr_status and enqueues work on `stream` only.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "layout.h"
+#include "sbvr.h"
+
+namespace sbvr {
+
+inline int launch_kernel(const void *fn, dim3 grid, dim3 block, size_t lds, hipStream_t stream,
+                         void **args)
+{
+    return hipLaunchKernel(fn, grid, block, args, lds, stream) == hipSuccess ? SBVR_OK : SBVR_E_HIP;
+}
+
+int launch_pack(const Dims &d, const uint32_t *planes_canon, const uint16_t *coeffs_canon,
+                void *planes_dev, void *coeffs_dev, hipStream_t stream);
+int launch_unpack(const Dims &d, const void *planes_dev, const void *coeffs_dev,
+                  uint32_t *planes_canon, uint16_t *coeffs_canon, hipStream_t stream);
+int launch_gemv_b1(const Dims &d, const void *planes_dev, const void *coeffs_dev,
+                   const uint16_t *x, uint16_t *y, hipStream_t stream);
+int launch_gemm_sb(const Dims &d, const void *planes_dev, const void *coeffs_dev,
+                   const uint16_t *X, uint16_t *Y, int B, hipStream_t stream);
+
+}  // namespace sbvr

@@ -1,0 +1,109 @@
+// Repacking between the canonical SBVR tensors and the device format
+// (layout.h), one thread per 32-bit plane word / coefficient.  Every byte of
+// the device buffers is written (padding with zeros), so they need no prior
+// clearing.
+#include "launch.h"
+
+namespace sbvr {
+
+__global__ void pack_planes_kernel(Dims d, const uint32_t *__restrict__ canon,
+                                   uint32_t *__restrict__ dev, size_t total)
+{
+    size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= total)
+        return;
+    const size_t bw = plane_block_words(d.k);
+    const size_t blk = idx / bw;
+    const int within = (int)(idx % bw);
+    const int slot = within / 4, w = within % 4;
+    const int i = slot % d.k, br = slot / d.k;
+    const int r = br % TILE_ROWS, b = br / TILE_ROWS;
+    const int o = (int)(blk / d.n_gblocks) * TILE_ROWS + r;
+    const int g = (int)(blk % d.n_gblocks) * GB + b;
+    uint32_t v = 0;
+    if (o < d.O && g < d.G)
+        v = to_device_word(canon[(((size_t)o * d.G + g) * d.k + i) * 4 + w]);
+    dev[idx] = v;
+}
+
+__global__ void unpack_planes_kernel(Dims d, const uint32_t *__restrict__ dev,
+                                     uint32_t *__restrict__ canon, size_t total)
+{
+    size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= total)
+        return;
+    const int w = (int)(idx % 4);
+    const size_t rest = idx / 4;
+    const int i = (int)(rest % d.k);
+    const size_t og = rest / d.k;
+    const int g = (int)(og % d.G), o = (int)(og / d.G);
+    const size_t blk = (size_t)(o / TILE_ROWS) * d.n_gblocks + g / GB;
+    const int slot = ((g % GB) * TILE_ROWS + o % TILE_ROWS) * d.k + i;
+    canon[idx] = to_canonical_word(dev[blk * plane_block_words(d.k) + slot * 4 + w]);
+}
+
+__global__ void pack_coeffs_kernel(Dims d, const uint16_t *__restrict__ canon,
+                                   uint16_t *__restrict__ dev, size_t total)
+{
+    size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= total)
+        return;
+    const size_t be = coeff_block_entries(d.k);
+    const size_t blk = idx / be;
+    const int within = (int)(idx % be);
+    const int i = within % d.k, rb = within / d.k;
+    const int b = rb % GB, r = rb / GB;
+    const int o = (int)(blk / d.n_gblocks) * TILE_ROWS + r;
+    const int g = (int)(blk % d.n_gblocks) * GB + b;
+    uint16_t v = 0;
+    if (o < d.O && g < d.G)
+        v = canon[((size_t)o * d.G + g) * d.k + i];
+    dev[idx] = v;
+}
+
+__global__ void unpack_coeffs_kernel(Dims d, const uint16_t *__restrict__ dev,
+                                     uint16_t *__restrict__ canon, size_t total)
+{
+    size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= total)
+        return;
+    const int i = (int)(idx % d.k);
+    const size_t og = idx / d.k;
+    const int g = (int)(og % d.G), o = (int)(og / d.G);
+    const size_t blk = (size_t)(o / TILE_ROWS) * d.n_gblocks + g / GB;
+    canon[idx] = dev[blk * coeff_block_entries(d.k) + ((o % TILE_ROWS) * GB + g % GB) * d.k + i];
+}
+
+static unsigned grid_for(size_t total) { return (unsigned)((total + 255) / 256); }
+
+int launch_pack(const Dims &d0, const uint32_t *planes_canon, const uint16_t *coeffs_canon,
+                void *planes_dev, void *coeffs_dev, hipStream_t stream)
+{
+    Dims d = d0;
+    size_t pw = plane_bytes(d) / 4, ce = coeff_bytes(d) / 2;
+    uint32_t *pd = (uint32_t *)planes_dev;
+    uint16_t *cd = (uint16_t *)coeffs_dev;
+    void *pargs[] = {&d, &planes_canon, &pd, &pw};
+    int st = launch_kernel((const void *)pack_planes_kernel, dim3(grid_for(pw)), dim3(256), 0, stream, pargs);
+    if (st != SBVR_OK)
+        return st;
+    void *cargs[] = {&d, &coeffs_canon, &cd, &ce};
+    return launch_kernel((const void *)pack_coeffs_kernel, dim3(grid_for(ce)), dim3(256), 0, stream, cargs);
+}
+
+int launch_unpack(const Dims &d0, const void *planes_dev, const void *coeffs_dev,
+                  uint32_t *planes_canon, uint16_t *coeffs_canon, hipStream_t stream)
+{
+    Dims d = d0;
+    size_t pw = (size_t)d.O * d.G * d.k * 4, ce = (size_t)d.O * d.G * d.k;
+    const uint32_t *pd = (const uint32_t *)planes_dev;
+    const uint16_t *cd = (const uint16_t *)coeffs_dev;
+    void *pargs[] = {&d, &pd, &planes_canon, &pw};
+    int st = launch_kernel((const void *)unpack_planes_kernel, dim3(grid_for(pw)), dim3(256), 0, stream, pargs);
+    if (st != SBVR_OK)
+        return st;
+    void *cargs[] = {&d, &cd, &coeffs_canon, &ce};
+    return launch_kernel((const void *)unpack_coeffs_kernel, dim3(grid_for(ce)), dim3(256), 0, stream, cargs);
+}
+
+}  // namespace sbvr
