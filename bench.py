@@ -4,10 +4,10 @@
 A step is one decoder layer's seven SBVR GEMVs (q, k, v, o, gate, up, down)
 at batch 1 with 4-bit SBVR weights (k = 4 planes, 128-weight groups, fp16
 coefficients), fp16 activations and outputs, in the Llama-3-8B projection
-shapes (Llama-3-70B with --model llama3-70b).  Steps cycle through L
-independent layers of weights so the rotated working set (~1.9 GiB) exceeds
-every cache and the bytes really come from HBM.  Each layer's seven calls
-are captured in one HIP graph, as decode steps are served.
+shapes (Llama-3-70B with --model llama3-70b).  L independent layers of weights
+(~1.9 GiB, more than every cache) are captured into one HIP graph, layer after
+layer on one stream, as a decode step is served; K steps replay that graph
+K // L times and the first K % L layers once more.
 
 Weights are drawn directly in SBVR form (uniform bit planes, Gaussian fp16
 coefficients, seeded): GEMV time does not depend on the values.  The parity
@@ -16,20 +16,33 @@ tests run these same shapes and launch configurations against the CPU oracle.
 One JSON line is printed:
   value         aggregate algorithmic HBM throughput (GB/s) of the timed steps
   per_call_us   mean duration of each projection's launch, from HIP events
-                around a graph of L back-to-back launches of that shape (one
-                per layer) on the launch stream
+                around a graph of >= 64 back-to-back launches of that shape
+                (cycling through the layers) on the launch stream
   roofline      the dominant kernel instance (largest time per step):
                 algorithmic bytes per launch / its mean launch duration, vs the
-                8 TB/s HBM peak
+                8 TB/s HBM peak; traffic = calibrated FETCH_SIZE + WRITE_SIZE
+                bytes per launch from the recorded counter runs, when they were
+                taken on the current kernel sources (else null)
   cpu_baseline  the CPU oracle (binary64 decompress + GEMV) on layer 0's seven
                 GEMVs, bounded to ~10 s of work, in the same unit
+
+--traffic-probe runs, eagerly, four launches of every projection shape and an
+elementwise negation over 256 MiB of float32 (reads and writes 256 MiB: the
+counter calibration), for
+  rocprofv3 --pmc FETCH_SIZE -- python3 bench.py --traffic-probe   (and WRITE_SIZE);
+--traffic-summary FETCH_CSV WRITE_CSV turns the two counter files into the
+record kept under profiles/.
 """
 from __future__ import annotations
 
 import argparse
+import csv
+import glob
+import hashlib
 import json
 import os
 import platform
+import re
 import sys
 import time
 
@@ -38,6 +51,9 @@ sys.path.insert(0, ROOT)
 
 PEAK_GBPS = 8000.0
 PROJ_ORDER = ("q", "k", "v", "o", "gate", "up", "down")
+TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "hbm_traffic_llama3-8b_k4.md")
+CALIB_BYTES = 256 << 20
+PROBE_LAUNCHES = 4
 
 
 def parse():
@@ -50,20 +66,100 @@ def parse():
     ap.add_argument("--k", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--traffic-probe", action="store_true",
+                    help="eager launches of every shape plus a calibration copy, for counter runs")
+    ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="summarise two rocprofv3 --pmc counter files (no GPU needed)")
     return ap.parse_args()
 
 
-def b1_kernel_instance(O: int, k: int) -> str:
-    """Name of the batch-1 kernel instance a launch with O rows runs: the
-    library takes T tiles (4T rows) per workgroup, the most of 8/4/2/1 that
-    still leaves >= 256 workgroups."""
-    n_tiles = (O + 3) // 4
+def kernel_source_digest() -> str:
+    """sha256 over the HIP sources of the library: identifies the kernels a
+    counter record was taken on."""
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2509_18172_amd", "csrc")
+    for f in sorted(glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.h"))):
+        h.update(os.path.basename(f).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def short_kernel_name(full: str) -> str:
+    m = re.search(r"sbvr::(gemv_b1s?_kernel<[^>]*>)", full)
+    return m.group(1) if m else full
+
+
+def read_counter_csv(path: str, counter: str):
+    """{kernel name: [per-dispatch value of `counter`]} from a rocprofv3
+    counter-collection CSV."""
+    out = {}
+    with open(path) as fh:
+        for r in csv.DictReader(fh):
+            if r["Counter_Name"] == counter:
+                out.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+    return out
+
+
+def traffic_summary(fetch_csv: str, write_csv: str) -> str:
+    """The profiles/ record: per-launch FETCH_SIZE and WRITE_SIZE of every GEMV
+    kernel, scaled by what the same counters read for a copy of known size."""
+    import numpy as np
+    fetch, write = read_counter_csv(fetch_csv, "FETCH_SIZE"), read_counter_csv(write_csv, "WRITE_SIZE")
+    copy = next(n for n in fetch if "neg_kernel" in n)
+    # KiB per dispatch; the copy reads and writes CALIB_BYTES
+    f_scale = CALIB_BYTES / (np.median(fetch[copy]) * 1024)
+    w_scale = CALIB_BYTES / (np.median(write[copy]) * 1024)
+    rec = {"source_sha256": kernel_source_digest(), "calibration": {
+        "copy_bytes": CALIB_BYTES, "fetch_kib": float(np.median(fetch[copy])),
+        "write_kib": float(np.median(write[copy])), "fetch_scale": f_scale, "write_scale": w_scale},
+        "kernels": {}}
+    for name in fetch:
+        if "gemv_b1" not in name:
+            continue
+        short = short_kernel_name(name)
+        fk, wk = float(np.median(fetch[name])), float(np.median(write.get(name, [0.0])))
+        rec["kernels"][short] = {"dispatches": len(fetch[name]), "fetch_kib": fk, "write_kib": wk,
+                                 "bytes_per_launch": round(fk * 1024 * f_scale + wk * 1024 * w_scale)}
+    lines = ["traffic-record: " + json.dumps(rec, sort_keys=True)]
+    return "\n".join(lines)
+
+
+def load_traffic(kernel: str):
+    """Calibrated HBM bytes per launch of `kernel` from the committed counter
+    record, or None when there is none or it predates the current sources."""
+    try:
+        with open(TRAFFIC_RECORD) as fh:
+            m = re.search(r"^traffic-record: (\{.*\})$", fh.read(), re.M)
+        rec = json.loads(m.group(1))
+    except (OSError, AttributeError, ValueError):
+        return None
+    if rec.get("source_sha256") != kernel_source_digest():
+        return None
+    k = rec["kernels"].get(kernel)
+    return None if k is None else k["bytes_per_launch"]
+
+
+def b1_kernel_instance(O: int, I: int, k: int) -> str:
+    """Name of the batch-1 kernel instance the library launches for an O x I
+    matrix: the streaming kernel (ring depth D, several gblocks per wavefront
+    or one) when a row has more than 16 gblocks of 512 elements or the matrix
+    has at least 24576 (4-row tile, gblock) blocks; otherwise the one-shot
+    kernel with T tiles per workgroup, the most of 8/4/2/1 that still leaves
+    >= 256 workgroups."""
+    n_tiles, n_gblocks = (O + 3) // 4, (I + 511) // 512
+    if n_gblocks > 16 or n_tiles * n_gblocks >= 24576:
+        multi = n_gblocks > 16
+        return f"gemv_b1s_kernel<{k}, {3 if multi else 2}, {'true' if multi else 'false'}>"
     T = next((t for t in (8, 4, 2) if n_tiles // t >= 256), 1)
     return f"gemv_b1_kernel<{k}, {T}>"
 
 
 def main():
     args = parse()
+    if args.traffic_summary:
+        print(traffic_summary(*args.traffic_summary))
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the SBVR GEMV path "
               "has no multi-GPU mode.", file=sys.stderr)
@@ -82,6 +178,8 @@ def main():
     nbytes = {n: sb.algorithmic_bytes(*shapes[n], k) for n in PROJ_ORDER}
     layer_bytes = sum(nbytes.values())
     L = args.layers or max(2, int(np.ceil(1.9 * 2 ** 30 / layer_bytes)))
+    if args.traffic_probe:
+        L = PROBE_LAUNCHES
     cfg_index = 1 if args.model == "llama3-8b" else 3
 
     # ---- weights: L layers x 7 projections, packed into the device format ----
@@ -110,6 +208,20 @@ def main():
             sb.gemv(W, x, out=y, stream=stream)
     torch.cuda.synchronize()
 
+    if args.traffic_probe:
+        with torch.cuda.stream(stream):
+            for name in PROJ_ORDER:
+                for li in range(L):
+                    W, x, y = layers[li][name]
+                    sb.gemv(W, x, out=y, stream=stream)
+            # calibration: an elementwise kernel that reads and writes CALIB_BYTES
+            src = torch.ones(CALIB_BYTES // 4, dtype=torch.float32, device=dev)
+            dst = torch.empty_like(src)
+            torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        print(json.dumps({"traffic_probe": True, "launches_per_shape": L, "copy_bytes": CALIB_BYTES}))
+        return
+
     def capture(calls):
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g, stream=stream):
@@ -117,32 +229,44 @@ def main():
                 sb.gemv(W, x, out=y, stream=stream)
         return g
 
-    def timed_replays(graphs, n):
-        e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+
+    def timed(fn):
         with torch.cuda.stream(stream):
             e0.record(stream)
-            for i in range(n):
-                graphs[i % len(graphs)].replay()
+            fn()
             e1.record(stream)
         torch.cuda.synchronize()
         return e0.elapsed_time(e1)  # ms
 
-    # ---- timed region: K steps, one layer graph per step ----
-    step_graphs = [capture([layers[li][n] for n in PROJ_ORDER]) for li in range(L)]
+    # ---- timed region: K steps = K // L replays of the L-layer decode graph,
+    # then the first K % L layers' graphs ----
+    decode_graph = capture([layers[li][n] for li in range(L) for n in PROJ_ORDER])
+    layer_graphs = [capture([layers[li][n] for n in PROJ_ORDER]) for li in range(L)]
     torch.cuda.synchronize()
+
+    def run_steps(n):
+        full, rem = divmod(n, L)
+        for _ in range(full):
+            decode_graph.replay()
+        for li in range(rem):
+            layer_graphs[li].replay()
+
     if args.warmup:
-        timed_replays(step_graphs, args.warmup)
-    total_ms = timed_replays(step_graphs, args.steps)
+        timed(lambda: run_steps(args.warmup))
+    total_ms = timed(lambda: run_steps(args.steps))
     ms_per_step = total_ms / args.steps
     value = layer_bytes * args.steps / (total_ms * 1e-3) / 1e9
+    del decode_graph, layer_graphs
 
-    # ---- per-shape launch durations: L back-to-back launches per graph ----
+    # ---- per-shape launch durations: >= 64 back-to-back launches per graph ----
+    n_launch = max(64, L)
     per_call_us = {}
     for name in PROJ_ORDER:
-        g = capture([layers[li][name] for li in range(L)])
-        timed_replays([g], 1)
-        reps = [timed_replays([g], 1) * 1e3 / L for _ in range(3)]
+        g = capture([layers[i % L][name] for i in range(n_launch)])
+        timed(g.replay)
+        reps = [timed(g.replay) * 1e3 / n_launch for _ in range(3)]
         per_call_us[name] = float(np.median(reps))
         del g
     per_call_gbps = {n: nbytes[n] / (per_call_us[n] * 1e3) for n in PROJ_ORDER}
@@ -150,7 +274,7 @@ def main():
     # dominant kernel instance: largest launch time per step
     by_kernel = {}
     for n in PROJ_ORDER:
-        kname = b1_kernel_instance(shapes[n][0], k)
+        kname = b1_kernel_instance(*shapes[n], k)
         t, b, c = by_kernel.get(kname, (0.0, 0, 0))
         by_kernel[kname] = (t + per_call_us[n], b + nbytes[n], c + 1)
     dom = max(by_kernel, key=lambda kk: by_kernel[kk][0])
@@ -158,10 +282,10 @@ def main():
     achieved = db / (dt * 1e3)  # (bytes per launch) / (mean launch duration), GB/s
     roofline = {
         "bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_GBPS, "unit": "GB/s",
-        "frac": round(achieved / PEAK_GBPS, 4), "traffic": None,
+        "frac": round(achieved / PEAK_GBPS, 4), "traffic": load_traffic(dom) if k == 4 and args.model == "llama3-8b" else None,
         "kernel": dom,
         "launches_per_step": dc,
-        "projections": [n for n in PROJ_ORDER if b1_kernel_instance(shapes[n][0], k) == dom],
+        "projections": [n for n in PROJ_ORDER if b1_kernel_instance(*shapes[n], k) == dom],
         "bytes_per_launch": round(db / dc),
         "mean_launch_us": round(dt / dc, 3),
     }
@@ -201,7 +325,7 @@ def main():
         "data": "synthetic: seeded SBVR planes and fp16 coefficients, N(0,1) fp16 activations",
         "config": {
             "workload": f"{args.model} decode-layer projections q,k,v,o,gate,up,down; SBVR k={k}, "
-                        f"group 128, batch 1; {L} rotating layers; one hipGraph per layer",
+                        f"group 128, batch 1; {L} layers in one hipGraph on one stream",
             "bytes_per_step": layer_bytes,
             "layers_rotated": L,
             "shapes": {n: list(shapes[n]) for n in PROJ_ORDER},

@@ -182,15 +182,27 @@ __device__ __forceinline__ v8i lds_operand(const unsigned char *lo, const unsign
     return r;
 }
 
+// Weight loads: 16-byte plane slots and coefficient words are streamed once,
+// so they are loaded non-temporally (no reuse expected in the caches).
+typedef unsigned v4u_t __attribute__((ext_vector_type(4)));
+typedef unsigned v2u_t __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ uint4 load_nt16(const uint4 *p)
+{
+    const v4u_t v = __builtin_nontemporal_load((const v4u_t *)p);
+    return make_uint4(v[0], v[1], v[2], v[3]);
+}
+
 // K coefficients of one (row, group) of a device coefficient block, as raw
 // binary16 words (c0 | c1 << 16, c2 | c3 << 16); planes >= K read as zero.
 template <int K>
 __device__ __forceinline__ uint2 load_coeffs(const uint16_t *p)
 {
     if constexpr (K == 4) {
-        return *(const uint2 *)p;
+        const v2u_t v = __builtin_nontemporal_load((const v2u_t *)p);
+        return make_uint2(v[0], v[1]);
     } else if constexpr (K == 2) {
-        return make_uint2(*(const uint32_t *)p, 0u);
+        return make_uint2(__builtin_nontemporal_load((const uint32_t *)p), 0u);
     } else if constexpr (K == 3) {
         return make_uint2((uint32_t)p[0] | ((uint32_t)p[1] << 16), (uint32_t)p[2]);
     } else {
@@ -208,12 +220,51 @@ __device__ __forceinline__ float apply_coeffs(uint2 c, const v4f &d)
     return s;
 }
 
+// Buffer-resource loads.  A descriptor bounds a byte range; a lane whose
+// offset falls outside it reads zero and issues no memory access, which lets
+// a software pipeline prefetch past the end of its range unconditionally.
+typedef __amdgpu_buffer_rsrc_t buf_rsrc;
+constexpr unsigned BUF_DWORD3 = 0x00020000u;  // raw (untyped) buffer, gfx9 family
+constexpr int BUF_NT = 2;                     // non-temporal cache policy
+constexpr unsigned BUF_OOB = 0x80000000u;     // an offset beyond every range used here
+
+__device__ __forceinline__ buf_rsrc make_rsrc(const void *base, unsigned bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, (int)bytes, BUF_DWORD3);
+}
+
+__device__ __forceinline__ uint4 buf_load16(buf_rsrc r, unsigned off)
+{
+    const v4u_t v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, BUF_NT);
+    return make_uint4(v[0], v[1], v[2], v[3]);
+}
+
+// load_coeffs through a descriptor (byte offset of the (row, group) entry).
+template <int K>
+__device__ __forceinline__ uint2 buf_coeffs(buf_rsrc r, unsigned off)
+{
+    if constexpr (K == 4) {
+        const v2u_t v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, BUF_NT);
+        return make_uint2(v[0], v[1]);
+    } else if constexpr (K == 2) {
+        return make_uint2(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, BUF_NT), 0u);
+    } else if constexpr (K == 3) {
+        const unsigned c0 = __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, BUF_NT);
+        const unsigned c1 = __builtin_amdgcn_raw_buffer_load_b16(r, off + 2, 0, BUF_NT);
+        const unsigned c2 = __builtin_amdgcn_raw_buffer_load_b16(r, off + 4, 0, BUF_NT);
+        return make_uint2(c0 | (c1 << 16), c2);
+    } else {
+        return make_uint2((unsigned)__builtin_amdgcn_raw_buffer_load_b16(r, off, 0, BUF_NT), 0u);
+    }
+}
+
 struct GemvArgs {
     const uint4 *planes;    // device plane blocks
     const uint16_t *coeffs; // device coefficient blocks
     const uint16_t *x;      // binary16 [B][I]
     uint16_t *y;            // binary16 [B][O]
     int O, I, k, n_tiles, n_gblocks, gpw, B;
+    int tpw;                // tiles per workgroup (streaming kernel)
 };
 
 }  // namespace sbvr

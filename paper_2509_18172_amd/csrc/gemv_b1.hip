@@ -1,10 +1,11 @@
 // Batch-1 SBVR GEMV (Sec. 4.4): y[o] = sum_g sum_i c[o][g][i] * S[o][g][i].
 //
-// Work decomposition.  A workgroup owns T tiles (4T consecutive rows); its
-// wavefront w owns gblocks [w*gpw, (w+1)*gpw) of the inner dimension (split-K
-// inside the workgroup).  Partial row sums are reduced across wavefronts in
-// LDS in a fixed order: results are deterministic and there is no global
-// workspace.
+// One-shot kernel, for matrices whose loads can all be in flight at once.
+// A workgroup owns T tiles (4T consecutive rows); its wavefront w owns gblock
+// w (512 inner elements; at most 16 per row: split-K inside the workgroup).
+// Partial row sums are reduced across wavefronts in LDS in a fixed order:
+// results are deterministic and there is no global workspace.  Larger
+// matrices go to the streaming kernel.
 //
 // Block-diagonal activation operand.  One 16x16x128 instruction takes, in its
 // four 32-slot k-blocks, word q of four different groups (the four groups of a
@@ -15,11 +16,11 @@
 // applied once per four instructions: D rows are (tile row, plane), so a lane
 // multiplies its four D values by the four coefficients of one (row, group).
 //
-// Latency hiding.  The activations of the first gblock are loaded first and
-// the T tiles' plane and coefficient blocks right after, so the wait for the
-// activations leaves every weight load in flight.  Two register sets
-// alternate: while one gblock is computed from set A, the next gblock's loads
-// land in set B.
+// Latency hiding.  Every load a wavefront needs -- its 1 KiB of activations,
+// then the T tiles' plane and coefficient blocks -- is issued before any
+// arithmetic, and scheduling barriers keep the compiler from sinking weight
+// loads below the activation work (left alone it does, to save registers,
+// which serialises DRAM latency behind arithmetic).
 #include "device_ops.h"
 #include "launch.h"
 
@@ -35,7 +36,7 @@ struct B1Regs {
 };
 
 template <int K, int T>
-__global__ void __launch_bounds__(512) gemv_b1_kernel(GemvArgs a)
+__global__ void __launch_bounds__(1024) gemv_b1_kernel(GemvArgs a)
 {
     extern __shared__ __align__(16) unsigned char smem[];
     const int lane = threadIdx.x & 63;
@@ -45,8 +46,7 @@ __global__ void __launch_bounds__(512) gemv_b1_kernel(GemvArgs a)
     float *red = (float *)(smem + nw * B1_WAVE_LDS);
 
     const int tile0 = blockIdx.x * T;
-    const int gb_begin = wv * a.gpw;
-    const int gb_end = min(a.n_gblocks, gb_begin + a.gpw);
+    const int gb = wv;
 
     // A operand: row m = lane%16 = (tile row r, plane i), k-block = group slot.
     // Lanes of planes >= K read a valid slot and zero it.
@@ -65,27 +65,18 @@ __global__ void __launch_bounds__(512) gemv_b1_kernel(GemvArgs a)
     for (int t = 0; t < T; ++t)
         tblk[t] = min(tile0 + t, a.n_tiles - 1) * a.n_gblocks;
 
-    auto fetch = [&](int gb, B1Regs<K, T> &R) {
-        // activations first; a gblock past I (ragged end) reads as zero
-        const int e0 = gb * (GB * GROUP);
-        if (e0 + GB * GROUP <= a.I) {
-            R.x = *(const uint4 *)(a.x + e0 + lane * 8);
-        } else {
-            const int e = e0 + lane * 8;
-            const uint4 v = *(const uint4 *)(a.x + min(e, a.I - 8));
-            R.x = e < a.I ? v : make_uint4(0u, 0u, 0u, 0u);
-        }
+    auto fetch = [&](B1Regs<K, T> &R) {
+        // activations first; lanes past I (ragged end) read a valid address
+        // and are zeroed before use
+        R.x = *(const uint4 *)(a.x + min(gb * (GB * GROUP) + lane * 8, a.I - 8));
 #pragma unroll
         for (int t = 0; t < T; ++t) {
             const size_t blk = (size_t)(tblk[t] + gb);
-            const uint4 v = (a.planes + blk * PBLK)[a_off];
+            const uint4 v = load_nt16(a.planes + blk * PBLK + a_off);
             R.p[t] = a_ok ? v : make_uint4(0u, 0u, 0u, 0u);
             R.c[t] = load_coeffs<K>(a.coeffs + blk * CBLK + c_off);
         }
     };
-
-    // zero the limb-3 chunks: they feed the unused 4th column of each slot
-    *(uint2 *)(lds + ((lane >> 2) * 4 + 3) * 32 + 8 * (lane & 3)) = make_uint2(0u, 0u);
 
     // limb writes: lane owns elements 8*lane .. 8*lane+7 of the gblock:
     // group slot lane/16, word (lane%16)/4, k-slots 8*(lane%4) ..
@@ -107,20 +98,23 @@ __global__ void __launch_bounds__(512) gemv_b1_kernel(GemvArgs a)
     for (int t = 0; t < T; ++t)
         acc[t] = 0.f;
 
-    // One gblock from register set R.
-    auto compute = [&](const B1Regs<K, T> &R) {
-        // per-gblock power-of-two activation scale and exact fp8 limbs
-        const int sigma = scale_exponent(wave_max(absmax8(R.x)));
-        const float inv_scale = ldexpf(1.0f, -sigma);
-        const Limbs L = make_limbs(R.x, ldexpf(1.0f, sigma + inv_alpha));
+    // Activation limbs of the gblock in R -> LDS -> the four B operands;
+    // returns 2^-sigma, the factor that undoes the activation scaling.
+    auto operands = [&](const B1Regs<K, T> &R, v8i *Bq) -> float {
+        const uint4 xv = gb * (GB * GROUP) + lane * 8 < a.I ? R.x : make_uint4(0u, 0u, 0u, 0u);
+        const int sigma = scale_exponent(wave_max(absmax8(xv)));
+        const Limbs L = make_limbs(xv, ldexpf(1.0f, sigma + inv_alpha));
         // same wavefront: the LDS writes complete before the reads below
         *(uint2 *)(lds + wr_off + 0 * 32) = make_uint2(L.hi[0], L.hi[1]);
         *(uint2 *)(lds + wr_off + 1 * 32) = make_uint2(L.mid[0], L.mid[1]);
         *(uint2 *)(lds + wr_off + 2 * 32) = make_uint2(L.lo[0], L.lo[1]);
-        v8i Bq[4];
 #pragma unroll
         for (int q = 0; q < 4; ++q)
             Bq[q] = lds_operand(lds + lo_off + q * 512, lds + hi_off + q * 512);
+        return ldexpf(1.0f, -sigma);
+    };
+    // The T tiles of the gblock in R.
+    auto tiles = [&](const B1Regs<K, T> &R, const v8i *Bq, float inv_scale) {
 #pragma unroll
         for (int t = 0; t < T; ++t) {
             v4f d = {0.f, 0.f, 0.f, 0.f};
@@ -132,21 +126,17 @@ __global__ void __launch_bounds__(512) gemv_b1_kernel(GemvArgs a)
         }
     };
 
-    if (gb_begin < gb_end) {
-        B1Regs<K, T> RA, RB;
-        fetch(gb_begin, RA);
-        for (int gb = gb_begin;; gb += 2) {
-            if (gb + 1 < gb_end)
-                fetch(gb + 1, RB);
-            compute(RA);
-            if (gb + 1 >= gb_end)
-                break;
-            if (gb + 2 < gb_end)
-                fetch(gb + 2, RA);
-            compute(RB);
-            if (gb + 2 >= gb_end)
-                break;
-        }
+    // zero the limb-3 chunks: they feed the unused 4th column of each slot
+    *(uint2 *)(lds + ((lane >> 2) * 4 + 3) * 32 + 8 * (lane & 3)) = make_uint2(0u, 0u);
+
+    {
+        B1Regs<K, T> R;
+        fetch(R);
+        __builtin_amdgcn_sched_barrier(0);  // all loads issued before arithmetic
+        v8i Bq[4];
+        const float inv_scale = operands(R, Bq);
+        __builtin_amdgcn_sched_barrier(0);
+        tiles(R, Bq, inv_scale);
     }
 
     // sum the 16 columns (group slot x limb) of each row ...
@@ -183,43 +173,20 @@ __global__ void __launch_bounds__(512) gemv_b1_kernel(GemvArgs a)
     }
 }
 
-struct B1Config {
-    int T, gpw, waves;
-};
-
 // Launch shape.  T tiles (4T rows) per workgroup: the most (<= 8) that still
-// leaves >= 256 workgroups for 256 CUs.  gpw gblocks per wavefront: enough
-// that the grid's wavefronts fit in about one residency round, and at most 8
-// wavefronts per workgroup.
-#ifndef SBVR_RESIDENT_WAVES
-#define SBVR_RESIDENT_WAVES 3072
-#endif
+// leaves >= 256 workgroups for 256 CUs; one wavefront per gblock.
+constexpr int B1_MAX_WAVES = 16;
 
-static B1Config choose_b1(const Dims &d)
+static int choose_b1_tiles(const Dims &d)
 {
-    B1Config c;
-    c.T = 1;
-    for (int t = 8; t > 1; t >>= 1)
-        if (d.n_tiles / t >= 256) {
-            c.T = t;
-            break;
-        }
 #ifdef SBVR_TUNE_T
-    c.T = SBVR_TUNE_T;
+    return SBVR_TUNE_T;
+#else
+    for (int t = 8; t > 1; t >>= 1)
+        if (d.n_tiles / t >= 256)
+            return t;
+    return 1;
 #endif
-    const long grid = (d.n_tiles + c.T - 1) / c.T;
-    int gpw = (int)((grid * d.n_gblocks + SBVR_RESIDENT_WAVES - 1) / SBVR_RESIDENT_WAVES);
-#ifdef SBVR_TUNE_GPW
-    gpw = SBVR_TUNE_GPW;
-#endif
-    const int min_gpw = (d.n_gblocks + 7) / 8;
-    if (gpw < min_gpw)
-        gpw = min_gpw;
-    if (gpw < 1)
-        gpw = 1;
-    c.gpw = gpw;
-    c.waves = (d.n_gblocks + gpw - 1) / gpw;
-    return c;
 }
 
 template <int K>
@@ -233,21 +200,29 @@ static const void *b1_kernel_for(int T)
     }
 }
 
+// Matrices with more (tile, gblock) blocks than this, or more than 16
+// gblocks per row, stream through the pipelined kernel.
+#ifndef SBVR_B1S_MIN_BLOCKS
+#define SBVR_B1S_MIN_BLOCKS 24576
+#endif
+
 int launch_gemv_b1(const Dims &d, const void *planes_dev, const void *coeffs_dev,
                    const uint16_t *x, uint16_t *y, hipStream_t stream)
 {
+    if (d.n_gblocks > B1_MAX_WAVES || (long)d.n_tiles * d.n_gblocks >= SBVR_B1S_MIN_BLOCKS)
+        return launch_gemv_b1s(d, planes_dev, coeffs_dev, x, y, stream);
+    const int T = choose_b1_tiles(d);
+    const int waves = d.n_gblocks;
     GemvArgs a = {(const uint4 *)planes_dev, (const uint16_t *)coeffs_dev, x, y, d.O, d.I, d.k,
-                  d.n_tiles, d.n_gblocks, 1, 1};
-    const B1Config c = choose_b1(d);
-    a.gpw = c.gpw;
-    const int grid = (d.n_tiles + c.T - 1) / c.T;
-    const size_t lds = (size_t)c.waves * B1_WAVE_LDS + (size_t)c.waves * c.T * TILE_ROWS * 4;
-    const void *fn = d.k == 4   ? b1_kernel_for<4>(c.T)
-                     : d.k == 3 ? b1_kernel_for<3>(c.T)
-                     : d.k == 2 ? b1_kernel_for<2>(c.T)
-                                : b1_kernel_for<1>(c.T);
+                  d.n_tiles, d.n_gblocks, 1, 1, 0};
+    const int grid = (d.n_tiles + T - 1) / T;
+    const size_t lds = (size_t)waves * B1_WAVE_LDS + (size_t)waves * T * TILE_ROWS * 4;
+    const void *fn = d.k == 4   ? b1_kernel_for<4>(T)
+                     : d.k == 3 ? b1_kernel_for<3>(T)
+                     : d.k == 2 ? b1_kernel_for<2>(T)
+                                : b1_kernel_for<1>(T);
     void *args[] = {&a};
-    return launch_kernel(fn, dim3(grid), dim3(64 * c.waves), lds, stream, args);
+    return launch_kernel(fn, dim3(grid), dim3(64 * waves), lds, stream, args);
 }
 
 }  // namespace sbvr

@@ -1,0 +1,237 @@
+// Streaming batch-1 SBVR GEMV (Sec. 4.4) for matrices too large to hold in
+// flight at once.
+//
+// A workgroup owns tpw consecutive tiles (4 rows each) and every gblock
+// (512 inner elements) of them; its W wavefronts split the gblocks, wavefront
+// w taking w, w+W, w+2W, ...  A wavefront's work is the sequence of items
+// (gblock, tile): for each of its gblocks, the workgroup's tiles in order.
+// The activation operand of a gblock is built once (same block-diagonal fp8
+// operand and fp4 plane operand as the one-shot kernel), then the items stream
+// through a D-deep ring of registers: the loads of item m+D are issued right
+// after item m is consumed, crossing into the next gblock without a pause.
+//
+// The ring is loaded through buffer descriptors bounded by the workgroup's
+// tile range, so the loads a wavefront issues past its last item read zero and
+// touch no memory: every ring slot is reloaded unconditionally and the
+// compiler keeps each slot in fixed registers with counted waits.
+//
+// Row sums of each (tile, gblock) item are added into an LDS array
+// [tile][wavefront][row] in gblock order; at the end the workgroup sums the
+// wavefronts in order, so the result is deterministic and no global
+// workspace is used.
+//
+// Memory behaviour: with D = 2 a wavefront keeps about 2.3 KB of weights in
+// flight and 32 wavefronts per CU keep ~70 KB per CU outstanding: enough to
+// cover DRAM latency, while each workgroup's requests stay in a narrow,
+// advancing address window.  Deeper rings or more workgroups measured slower
+// (more requests in flight than the memory system serves efficiently).
+#include "device_ops.h"
+#include "launch.h"
+
+namespace sbvr {
+
+constexpr int B1S_WAVE_LDS = 2048;  // per wavefront: [q][s][l][32 B]
+// Ring depth: one gblock per wavefront keeps 64 VGPRs (8 wavefronts per
+// SIMD) at depth 2; with several gblocks the workgroups are fewer and a
+// deeper ring keeps enough bytes in flight.
+#ifndef SBVR_B1S_DEPTH
+#define SBVR_B1S_DEPTH 2
+#endif
+#ifndef SBVR_B1S_DEPTH_MULTI
+#define SBVR_B1S_DEPTH_MULTI 3
+#endif
+#ifndef SBVR_B1S_MAX_WAVES
+#define SBVR_B1S_MAX_WAVES 16
+#endif
+// Workgroups per launch: two resident per CU with one gblock per wavefront;
+// one per CU (longer item streams per wavefront) with several.
+#ifndef SBVR_B1S_GROUPS
+#define SBVR_B1S_GROUPS 512
+#endif
+#ifndef SBVR_B1S_GROUPS_MULTI
+#define SBVR_B1S_GROUPS_MULTI 256
+#endif
+
+template <int K, int D, bool MULTI>
+__global__ void __launch_bounds__(1024) gemv_b1s_kernel(GemvArgs a)
+{
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int lane = threadIdx.x & 63;
+    const int wv = wave_id();
+    const int nw = blockDim.x >> 6;
+    unsigned char *lds = smem + wv * B1S_WAVE_LDS;
+    float *red = (float *)(smem + nw * B1S_WAVE_LDS);  // [tpw][nw][TILE_ROWS]
+
+    const int tile0 = blockIdx.x * a.tpw;
+    const int ntl = min(a.tpw, a.n_tiles - tile0);
+    // MULTI: several gblocks per wavefront; otherwise exactly one (wv)
+    const int n_items = MULTI ? ((a.n_gblocks - wv + nw - 1) / nw) * ntl : ntl;
+
+    // A operand lane mapping: row m = lane%16 = (tile row r, plane i),
+    // k-block = group slot; planes >= K read a valid slot and are zeroed.
+    const int a_r = (lane & 15) >> 2, a_i = lane & 3, a_b = lane >> 4;
+    const bool a_ok = a_i < K;
+    const unsigned a_off = (unsigned)((a_b * TILE_ROWS + a_r) * K + (a_ok ? a_i : 0));
+    // coefficients of the lane's D rows: tile row lane/16, planes 0..3
+    const unsigned c_off = (unsigned)(((lane >> 4) * GB + ((lane & 15) >> 2)) * K);
+    constexpr unsigned PBLK_B = GB * TILE_ROWS * K * 16;  // bytes per plane block
+    constexpr unsigned CBLK_B = TILE_ROWS * GB * K * 2;   // bytes per coefficient block
+    const unsigned pstep = (unsigned)a.n_gblocks * PBLK_B;  // next tile, same gblock
+    const unsigned cstep = (unsigned)a.n_gblocks * CBLK_B;
+    const size_t blk0 = (size_t)tile0 * a.n_gblocks;
+    const buf_rsrc prs = make_rsrc((const unsigned char *)a.planes + blk0 * PBLK_B, (unsigned)ntl * pstep);
+    const buf_rsrc crs = make_rsrc((const unsigned char *)a.coeffs + blk0 * CBLK_B, (unsigned)ntl * cstep);
+    const unsigned p_lane = a_off * 16, c_lane = c_off * 2;
+
+    // Prefetch cursor (wavefront-uniform): next item whose loads are issued.
+    int pf_i = 0, pf_gb = wv;
+    uint4 P[D];
+    uint2 C[D];
+    auto issue = [&](int j) {
+        unsigned po, co;
+        if constexpr (MULTI) {
+            po = co = BUF_OOB;
+            if (pf_gb < a.n_gblocks) {
+                po = (unsigned)pf_i * pstep + (unsigned)pf_gb * PBLK_B;
+                co = (unsigned)pf_i * cstep + (unsigned)pf_gb * CBLK_B;
+            }
+            if (++pf_i == ntl) {
+                pf_i = 0;
+                pf_gb += nw;
+            }
+        } else {
+            // items past the last tile fall outside the descriptors' range
+            po = (unsigned)pf_i * pstep + (unsigned)wv * PBLK_B;
+            co = (unsigned)pf_i * cstep + (unsigned)wv * CBLK_B;
+            ++pf_i;
+        }
+        P[j] = buf_load16(prs, p_lane + po);
+        C[j] = buf_coeffs<K>(crs, c_lane + co);
+    };
+    // Activations of a gblock; lanes past I (ragged end) read a valid address
+    // and are zeroed when the operand is built.
+    auto load_x = [&](int gb) {
+        const int e = gb * (GB * GROUP) + lane * 8;
+        return *(const uint4 *)(a.x + min(e, a.I - 8));
+    };
+
+    uint4 x_cur = load_x(wv);
+#pragma unroll
+    for (int j = 0; j < D; ++j)
+        issue(j);
+    uint4 x_next;
+    if constexpr (MULTI)
+        x_next = load_x(wv + nw);
+    __builtin_amdgcn_sched_barrier(0);
+
+    // B operand lane mapping (see the one-shot kernel): column n = lane%16 =
+    // (slot s, limb l), k-block lane/16.
+    const int wr_off = ((((lane & 15) >> 2) * 4 + (lane >> 4)) * 4) * 32 + 8 * (lane & 3);
+    const int n = lane & 15, kb = lane >> 4;
+    const int s = n >> 2, l = n & 3;
+    const bool act = (l < 3) && ((kb >> 1) == (s & 1));
+    const int data_off = (s * 4 + l) * 32 + 16 * (kb & 1);
+    const int zero_off = (s * 4 + 3) * 32;
+    const int lo_off = (act && s < 2) ? data_off : zero_off;
+    const int hi_off = (act && s >= 2) ? data_off : zero_off;
+    const int inv_alpha = inv_alpha_exp(lane & 3);
+    // zero the limb-3 chunks: they feed the unused 4th column of each slot
+    *(uint2 *)(lds + ((lane >> 2) * 4 + 3) * 32 + 8 * (lane & 3)) = make_uint2(0u, 0u);
+
+    v8i Bq[4];
+    float inv_scale;
+    auto build = [&](uint4 xr, int gb) {
+        const uint4 xv = gb * (GB * GROUP) + lane * 8 < a.I ? xr : make_uint4(0u, 0u, 0u, 0u);
+        const int sigma = scale_exponent(wave_max(absmax8(xv)));
+        inv_scale = ldexpf(1.0f, -sigma);
+        const Limbs L = make_limbs(xv, ldexpf(1.0f, sigma + inv_alpha));
+        // same wavefront: these writes land before the reads below, and after
+        // the reads of the previous gblock's operand
+        *(uint2 *)(lds + wr_off + 0 * 32) = make_uint2(L.hi[0], L.hi[1]);
+        *(uint2 *)(lds + wr_off + 1 * 32) = make_uint2(L.mid[0], L.mid[1]);
+        *(uint2 *)(lds + wr_off + 2 * 32) = make_uint2(L.lo[0], L.lo[1]);
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            Bq[q] = lds_operand(lds + lo_off + q * 512, lds + hi_off + q * 512);
+    };
+    build(x_cur, wv);
+    __builtin_amdgcn_sched_barrier(0);
+
+    float *red_w = red + wv * TILE_ROWS + (lane >> 4);
+    int cur_i = 0, cur_gb = wv;
+    for (int m0 = 0; m0 < n_items; m0 += D) {
+#pragma unroll
+        for (int j = 0; j < D; ++j) {
+            const int m = m0 + j;
+            if (m < n_items) {
+                if constexpr (MULTI) {
+                    if (cur_i == 0 && m > 0) {  // first item of the next gblock
+                        build(x_next, cur_gb);
+                        x_next = load_x(cur_gb + nw);
+                    }
+                }
+                const uint4 pw = a_ok ? P[j] : make_uint4(0u, 0u, 0u, 0u);
+                v4f d = {0.f, 0.f, 0.f, 0.f};
+                d = mfma_fp4_fp8(fp4_operand(pw.x), Bq[0], d);
+                d = mfma_fp4_fp8(fp4_operand(pw.y), Bq[1], d);
+                d = mfma_fp4_fp8(fp4_operand(pw.z), Bq[2], d);
+                d = mfma_fp4_fp8(fp4_operand(pw.w), Bq[3], d);
+                const float v = row16_sum(apply_coeffs(C[j], d) * inv_scale);
+                if ((lane & 15) == 0) {
+                    float *r = red_w + cur_i * nw * TILE_ROWS;
+                    if (!MULTI || cur_gb == wv)
+                        *r = v;
+                    else
+                        *r += v;
+                }
+                if (++cur_i == ntl && MULTI) {
+                    cur_i = 0;
+                    cur_gb += nw;
+                }
+            }
+            issue(j);
+        }
+    }
+
+    __syncthreads();
+    const int row_base = tile0 * TILE_ROWS;
+    for (int idx = threadIdx.x; idx < ntl * TILE_ROWS; idx += blockDim.x) {
+        const int o = row_base + idx;
+        if (o < a.O) {
+            const float *r = red + (idx / TILE_ROWS) * nw * TILE_ROWS + (idx % TILE_ROWS);
+            float v = 0.f;
+            for (int w = 0; w < nw; ++w)
+                v += r[w * TILE_ROWS];
+            a.y[o] = __half_as_ushort(__float2half_rn(v));
+        }
+    }
+}
+
+template <int K>
+static const void *b1s_kernel_for(bool multi)
+{
+    return multi ? (const void *)gemv_b1s_kernel<K, SBVR_B1S_DEPTH_MULTI, true>
+                 : (const void *)gemv_b1s_kernel<K, SBVR_B1S_DEPTH, false>;
+}
+
+int launch_gemv_b1s(const Dims &d, const void *planes_dev, const void *coeffs_dev,
+                    const uint16_t *x, uint16_t *y, hipStream_t stream)
+{
+    const int gpw = (d.n_gblocks + SBVR_B1S_MAX_WAVES - 1) / SBVR_B1S_MAX_WAVES;
+    const int waves = (d.n_gblocks + gpw - 1) / gpw;
+    const int groups = gpw > 1 ? SBVR_B1S_GROUPS_MULTI : SBVR_B1S_GROUPS;
+    const int tpw = (d.n_tiles + groups - 1) / groups;
+    const int grid = (d.n_tiles + tpw - 1) / tpw;
+    GemvArgs a = {(const uint4 *)planes_dev, (const uint16_t *)coeffs_dev, x, y, d.O, d.I, d.k,
+                  d.n_tiles, d.n_gblocks, gpw, 1, tpw};
+    const size_t lds = (size_t)waves * B1S_WAVE_LDS + (size_t)tpw * waves * TILE_ROWS * 4;
+    const bool multi = gpw > 1;
+    const void *fn = d.k == 4   ? b1s_kernel_for<4>(multi)
+                     : d.k == 3 ? b1s_kernel_for<3>(multi)
+                     : d.k == 2 ? b1s_kernel_for<2>(multi)
+                                : b1s_kernel_for<1>(multi);
+    void *args[] = {&a};
+    return launch_kernel(fn, dim3(grid), dim3(64 * waves), lds, stream, args);
+}
+
+}  // namespace sbvr

@@ -22,6 +22,8 @@ int launch_unpack(const Dims &d, const void *planes_dev, const void *coeffs_dev,
                   uint32_t *planes_canon, uint16_t *coeffs_canon, hipStream_t stream);
 int launch_gemv_b1(const Dims &d, const void *planes_dev, const void *coeffs_dev,
                    const uint16_t *x, uint16_t *y, hipStream_t stream);
+int launch_gemv_b1s(const Dims &d, const void *planes_dev, const void *coeffs_dev,
+                    const uint16_t *x, uint16_t *y, hipStream_t stream);
 int launch_gemm_sb(const Dims &d, const void *planes_dev, const void *coeffs_dev,
                    const uint16_t *X, uint16_t *Y, int B, hipStream_t stream);
 

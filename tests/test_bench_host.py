@@ -1,0 +1,52 @@
+"""Host-side logic of bench.py (no GPU): kernel-instance naming and the
+counter-record summary."""
+import csv
+import os
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+import bench  # noqa: E402
+
+
+@pytest.mark.parametrize("O,I,name", [
+    (4096, 4096, "gemv_b1_kernel<4, 4>"),      # 8192 blocks: one-shot, 1024 tiles -> T = 4
+    (1024, 4096, "gemv_b1_kernel<4, 1>"),
+    (14336, 4096, "gemv_b1s_kernel<4, 2, false>"),  # 28672 blocks: streaming
+    (4096, 14336, "gemv_b1s_kernel<4, 3, true>"),   # 28 gblocks per row
+    (8192, 8192, "gemv_b1s_kernel<4, 2, false>"),
+    (1024, 8192, "gemv_b1_kernel<4, 1>"),
+])
+def test_kernel_instance_names(O, I, name):
+    assert bench.b1_kernel_instance(O, I, 4) == name
+
+
+def _write_counter_csv(path, counter, rows):
+    cols = ["Correlation_Id", "Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value"]
+    with open(path, "w", newline="") as fh:
+        w = csv.DictWriter(fh, fieldnames=cols)
+        w.writeheader()
+        for i, (kernel, value) in enumerate(rows):
+            w.writerow({"Correlation_Id": i, "Dispatch_Id": i, "Kernel_Name": kernel,
+                        "Counter_Name": counter, "Counter_Value": value})
+
+
+def test_traffic_summary_scales_by_copy(tmp_path):
+    copy = "void at::native::vectorized_elementwise_kernel<4, at::native::neg_kernel_cuda(at::TensorIteratorBase&)::{lambda()#1}>"
+    kern = "void sbvr::gemv_b1s_kernel<4, 2, false>(sbvr::GemvArgs)"
+    calib_kib = bench.CALIB_BYTES / 1024
+    # counters that see half of what moves: the scale must double them back
+    _write_counter_csv(tmp_path / "f.csv", "FETCH_SIZE",
+                       [(kern, 16000.0), (kern, 16200.0), (kern, 16100.0), (copy, calib_kib / 2)])
+    _write_counter_csv(tmp_path / "w.csv", "WRITE_SIZE",
+                       [(kern, 7.0), (kern, 7.0), (kern, 7.0), (copy, calib_kib / 2)])
+    text = bench.traffic_summary(str(tmp_path / "f.csv"), str(tmp_path / "w.csv"))
+    import json
+    import re
+    rec = json.loads(re.search(r"^traffic-record: (\{.*\})$", text, re.M).group(1))
+    k = rec["kernels"]["gemv_b1s_kernel<4, 2, false>"]
+    assert k["dispatches"] == 3
+    assert k["bytes_per_launch"] == round(16100.0 * 1024 * 2 + 7.0 * 1024 * 2)
+    assert rec["source_sha256"] == bench.kernel_source_digest()
