@@ -129,7 +129,10 @@ int sbvr_gemm_small_batch(int O, int I, int k, const void *planes_dev, const voi
     int st = check_gemv(O, I, k, planes_dev, coeffs_dev, X, Y, B, ws_bytes);
     if (st != SBVR_OK)
         return st;
-    return launch_gemm_sb(make_dims(O, I, k), planes_dev, coeffs_dev, X, Y, B, stream);
+    const Dims d = make_dims(O, I, k);
+    if (B == 1)
+        return launch_gemv_b1(d, planes_dev, coeffs_dev, X, Y, stream);
+    return launch_gemm_sbs(d, planes_dev, coeffs_dev, X, Y, B, stream);
 }
 
 }  // extern "C"

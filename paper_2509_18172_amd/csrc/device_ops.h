@@ -159,6 +159,82 @@ __device__ __forceinline__ Limbs make_limbs(uint4 xv, float scale)
     return L;
 }
 
+// Three E4M3 limbs by splitting in binary16 (cheaper than make_limbs).
+// The truncation split hi = x with its mantissa cut to 3 bits, mid = the same
+// cut of x - hi, lo = x - hi - mid is exact in binary16 (every difference is
+// representable), and each piece has at most 4 significant bits, so the
+// scaled conversion fp8(piece / scale_div) is exact while the scaled value
+// lies in the E4M3 range.  scale_div = 2^-(sigma + log2(1/alpha)).
+typedef _Float16 h2_t __attribute__((ext_vector_type(2)));
+typedef short s2_t __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ uint32_t h2_sub(uint32_t a, uint32_t b)
+{
+    return __builtin_bit_cast(uint32_t, __builtin_bit_cast(h2_t, a) - __builtin_bit_cast(h2_t, b));
+}
+
+__device__ __forceinline__ uint32_t cvt2_fp8(uint32_t lo_pair, uint32_t hi_pair, float scale_div)
+{
+    s2_t r = __builtin_amdgcn_cvt_scalef32_pk_fp8_f16(s2_t{0, 0}, __builtin_bit_cast(h2_t, lo_pair),
+                                                       scale_div, false);
+    r = __builtin_amdgcn_cvt_scalef32_pk_fp8_f16(r, __builtin_bit_cast(h2_t, hi_pair), scale_div, true);
+    return __builtin_bit_cast(uint32_t, r);
+}
+
+__device__ __forceinline__ Limbs split_limbs(uint4 xv, float scale_div)
+{
+    constexpr uint32_t CUT = 0xFF80FF80u;  // sign, exponent and 3 mantissa bits of each half
+    const uint32_t w[4] = {xv.x, xv.y, xv.z, xv.w};
+    uint32_t hi[4], mid[4], lo[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        hi[i] = w[i] & CUT;
+        const uint32_t r = h2_sub(w[i], hi[i]);
+        mid[i] = r & CUT;
+        lo[i] = h2_sub(r, mid[i]);
+    }
+    Limbs L;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        L.hi[h] = cvt2_fp8(hi[2 * h], hi[2 * h + 1], scale_div);
+        L.mid[h] = cvt2_fp8(mid[2 * h], mid[2 * h + 1], scale_div);
+        L.lo[h] = cvt2_fp8(lo[2 * h], lo[2 * h + 1], scale_div);
+    }
+    return L;
+}
+
+// max |x| over the wavefront's binary16 activations (eight per lane), as a
+// float: the magnitudes' bit patterns order like unsigned integers.
+__device__ __forceinline__ float wave_absmax_h(uint4 v)
+{
+    typedef unsigned short u2_t __attribute__((ext_vector_type(2)));
+    const u2_t a = __builtin_bit_cast(u2_t, v.x & 0x7fff7fffu), b = __builtin_bit_cast(u2_t, v.y & 0x7fff7fffu);
+    const u2_t c = __builtin_bit_cast(u2_t, v.z & 0x7fff7fffu), d = __builtin_bit_cast(u2_t, v.w & 0x7fff7fffu);
+    const u2_t m2 = __builtin_elementwise_max(__builtin_elementwise_max(a, b), __builtin_elementwise_max(c, d));
+    int m = (int)(m2[0] > m2[1] ? m2[0] : m2[1]);
+    m = max(m, __builtin_amdgcn_update_dpp(0, m, DPP_QUAD_XOR1, 0xf, 0xf, false));
+    m = max(m, __builtin_amdgcn_update_dpp(0, m, DPP_QUAD_XOR2, 0xf, 0xf, false));
+    m = max(m, __builtin_amdgcn_update_dpp(0, m, DPP_ROW_HALF_MIRROR, 0xf, 0xf, false));
+    m = max(m, __builtin_amdgcn_update_dpp(0, m, DPP_ROW_MIRROR, 0xf, 0xf, false));
+    const int r = max(max(__builtin_amdgcn_readlane(m, 0), __builtin_amdgcn_readlane(m, 16)),
+                      max(__builtin_amdgcn_readlane(m, 32), __builtin_amdgcn_readlane(m, 48)));
+    return half_bits_to_float((uint32_t)r);
+}
+
+// 4 x 4 transpose of 32-bit words across the lanes l, l+16, l+32, l+48 of a
+// wavefront: lane l + 16 b holds words (w[b][0], ..., w[b][3]) on entry and
+// (w[0][b], ..., w[3][b]) on exit.  permlane32_swap exchanges the upper half
+// of its first operand with the lower half of its second; permlane16_swap
+// does the same between odd and even rows of 16 lanes.
+__device__ __forceinline__ uint4 transpose_rows4(uint4 w)
+{
+    const auto s02 = __builtin_amdgcn_permlane32_swap(w.x, w.z, false, false);
+    const auto s13 = __builtin_amdgcn_permlane32_swap(w.y, w.w, false, false);
+    const auto t01 = __builtin_amdgcn_permlane16_swap(s02[0], s13[0], false, false);
+    const auto t23 = __builtin_amdgcn_permlane16_swap(s02[1], s13[1], false, false);
+    return make_uint4(t01[0], t01[1], t23[0], t23[1]);
+}
+
 __device__ __forceinline__ v4f mfma_fp4_fp8(const v8i &a, const v8i &b, const v4f &c)
 {
     // A: fp4 E2M1 (cbsz = 4), B: fp8 E4M3 (blgp = 0), unit E8M0 scales (127).
@@ -227,6 +303,7 @@ typedef __amdgpu_buffer_rsrc_t buf_rsrc;
 constexpr unsigned BUF_DWORD3 = 0x00020000u;  // raw (untyped) buffer, gfx9 family
 constexpr int BUF_NT = 2;                     // non-temporal cache policy
 constexpr unsigned BUF_OOB = 0x80000000u;     // an offset beyond every range used here
+constexpr unsigned LANE_OOB = 0x40000000u;    // per-lane offset that reads zero (ranges stay below 2^30)
 
 __device__ __forceinline__ buf_rsrc make_rsrc(const void *base, unsigned bytes)
 {

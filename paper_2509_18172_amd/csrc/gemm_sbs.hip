@@ -1,0 +1,321 @@
+// Small-batch SBVR GEMM (2 <= B <= 8 activation vectors; Sec. 4.4 applied to
+// each vector), streaming the weights once for all B vectors.
+//
+// Work decomposition (as the batch-1 streaming kernel): a workgroup owns tpw
+// consecutive tiles (4 rows) and every gblock (512 inner elements) of them;
+// wavefront w takes gblocks w, w+W, ...  Its items (gblock, tile) stream
+// through a D-deep register ring loaded with buffer descriptors bounded by
+// the workgroup's tile range (loads past the end read zero, no traffic).
+//
+// Matrix-core formulation.  One 16x16x128 fp4 x fp8 instruction per (tile,
+// group, column set): the 128 k-slots are one whole group (its four plane
+// words, one per 32-slot k-block), rows are (tile row, plane) and the 16
+// columns are (vector, limb) with four columns per vector -- three E4M3 limbs
+// and a zero column -- so a column set serves four vectors (B <= 4: one set,
+// B <= 8: two).  The device layout gives lane (row m, k-block b) the four
+// words of group b; a 4 x 4 cross-lane transpose turns that into word b of
+// the four groups, i.e. the A operands of the four instructions of an item.
+//
+// Each lane applies its tile row's coefficients to its four D rows (planes)
+// for every group, the four limb columns of a vector are summed by a quad
+// reduction, and one lane per (row, vector) adds the item's partial sum to
+// LDS; the workgroup sums the wavefronts in order at the end (deterministic,
+// no global workspace).
+#include "device_ops.h"
+#include "launch.h"
+
+namespace sbvr {
+
+#ifndef SBVR_SBS_DEPTH
+#define SBVR_SBS_DEPTH 3
+#endif
+#ifndef SBVR_SBS_MAX_WAVES
+#define SBVR_SBS_MAX_WAVES 8
+#endif
+#ifndef SBVR_SBS_GROUPS
+#define SBVR_SBS_GROUPS 256
+#endif
+
+// vectors per column set and LDS staging of one set's limbs per wavefront:
+// [group][vector][limb][128 bytes], then 32 zero bytes
+constexpr int SBS_VPS = 4;
+__host__ __device__ constexpr int sbs_sets(int nb) { return (nb + SBS_VPS - 1) / SBS_VPS; }
+__host__ __device__ constexpr int sbs_vps(int nb) { return nb < SBS_VPS ? nb : SBS_VPS; }
+__host__ __device__ constexpr int sbs_stage_bytes(int nb) { return GB * sbs_vps(nb) * 3 * GROUP + 32; }
+
+// The 4K binary16 coefficients of one tile row over the four groups of a
+// gblock, (group, plane) order, as 2K words.
+template <int K>
+struct CoefRow {
+    uint32_t w[2 * K];
+};
+
+template <int K>
+__device__ __forceinline__ CoefRow<K> buf_coef_row(buf_rsrc r, unsigned off)
+{
+    CoefRow<K> c;
+    if constexpr (K >= 2) {
+        const v4u_t v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, BUF_NT);
+        c.w[0] = v[0];
+        c.w[1] = v[1];
+        c.w[2] = v[2];
+        c.w[3] = v[3];
+    }
+    if constexpr (K == 4) {
+        const v4u_t v = __builtin_amdgcn_raw_buffer_load_b128(r, off + 16, 0, BUF_NT);
+        c.w[4] = v[0];
+        c.w[5] = v[1];
+        c.w[6] = v[2];
+        c.w[7] = v[3];
+    } else if constexpr (K == 3) {
+        const v2u_t v = __builtin_amdgcn_raw_buffer_load_b64(r, off + 16, 0, BUF_NT);
+        c.w[4] = v[0];
+        c.w[5] = v[1];
+    } else if constexpr (K == 1) {
+        const v2u_t v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, BUF_NT);
+        c.w[0] = v[0];
+        c.w[1] = v[1];
+    }
+    return c;
+}
+
+template <int K>
+__device__ __forceinline__ float coef(const CoefRow<K> &c, int g, int i)
+{
+    const int e = g * K + i;
+    return half_bits_to_float(e & 1 ? c.w[e >> 1] >> 16 : c.w[e >> 1] & 0xffffu);
+}
+
+template <int K, int NB, int D, bool MULTI>
+__global__ void __launch_bounds__(512) gemm_sbs_kernel(GemvArgs a)
+{
+    constexpr int NS = sbs_sets(NB);
+    constexpr int VPS = sbs_vps(NB);
+    constexpr int STAGE = sbs_stage_bytes(NB);
+    constexpr int ZERO = STAGE - 32;
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int lane = threadIdx.x & 63;
+    const int wv = wave_id();
+    const int nw = blockDim.x >> 6;
+    const int B = a.B;  // vectors actually present (<= NB)
+    unsigned char *stage = smem + wv * STAGE;
+    float *red = (float *)(smem + nw * STAGE);  // [tpw][nw][NS][4 rows][4 vectors]
+
+    const int tile0 = blockIdx.x * a.tpw;
+    const int ntl = min(a.tpw, a.n_tiles - tile0);
+    const int n_items = MULTI ? ((a.n_gblocks - wv + nw - 1) / nw) * ntl : ntl;
+
+    // A: lane (row m = lane%16 = (tile row, plane), k-block lane/16) loads the
+    // 16 bytes of group lane/16; lanes of planes >= K read zero.
+    const int a_r = (lane & 15) >> 2, a_i = lane & 3, a_b = lane >> 4;
+    const unsigned p_lane = a_i < K ? (unsigned)((a_b * TILE_ROWS + a_r) * K + a_i) * 16u : LANE_OOB;
+    // coefficients: the lane's D rows are tile row lane/16, planes 0..3
+    const unsigned c_lane = (unsigned)((lane >> 4) * GB * K) * 2u;
+    constexpr unsigned PBLK_B = GB * TILE_ROWS * K * 16;
+    constexpr unsigned CBLK_B = TILE_ROWS * GB * K * 2;
+    const unsigned pstep = (unsigned)a.n_gblocks * PBLK_B;
+    const unsigned cstep = (unsigned)a.n_gblocks * CBLK_B;
+    const size_t blk0 = (size_t)tile0 * a.n_gblocks;
+    const buf_rsrc prs = make_rsrc((const unsigned char *)a.planes + blk0 * PBLK_B, (unsigned)ntl * pstep);
+    const buf_rsrc crs = make_rsrc((const unsigned char *)a.coeffs + blk0 * CBLK_B, (unsigned)ntl * cstep);
+
+    int pf_i = 0, pf_gb = wv;
+    uint4 P[D];
+    CoefRow<K> C[D];
+    auto issue = [&](int j) {
+        unsigned po, co;
+        if constexpr (MULTI) {
+            po = co = BUF_OOB;
+            if (pf_gb < a.n_gblocks) {
+                po = (unsigned)pf_i * pstep + (unsigned)pf_gb * PBLK_B;
+                co = (unsigned)pf_i * cstep + (unsigned)pf_gb * CBLK_B;
+            }
+            if (++pf_i == ntl) {
+                pf_i = 0;
+                pf_gb += nw;
+            }
+        } else {
+            po = (unsigned)pf_i * pstep + (unsigned)wv * PBLK_B;
+            co = (unsigned)pf_i * cstep + (unsigned)wv * CBLK_B;
+            ++pf_i;
+        }
+        P[j] = buf_load16(prs, p_lane + po);
+        C[j] = buf_coef_row<K>(crs, c_lane + co);
+    };
+    // The lane's eight activations of gblock gb for every vector present;
+    // lanes past I (ragged end) and vectors >= B read zero.
+    auto load_x = [&](uint4 *X, int gb) {
+        const int e = gb * (GB * GROUP) + lane * 8;
+        const bool in = e < a.I;
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+            X[b] = (in && b < B) ? *(const uint4 *)(a.x + (size_t)b * a.I + e) : make_uint4(0u, 0u, 0u, 0u);
+    };
+
+    uint4 Xc[NB];
+    load_x(Xc, wv);
+#pragma unroll
+    for (int j = 0; j < D; ++j)
+        issue(j);
+    __builtin_amdgcn_sched_barrier(0);
+
+    if (lane < 2)
+        *(uint4 *)(stage + ZERO + 16 * lane) = make_uint4(0u, 0u, 0u, 0u);
+    // B operand reads: lane (column n = lane%16 = (vector n/4, limb n%4),
+    // k-block lane/16) takes k = 16 kb + [0,16) and 64 + 16 kb + [0,16) of
+    // its vector's limb; limb 3 and absent vectors read the zero chunk.
+    const int n = lane & 15, kb = lane >> 4;
+    const int vb = n >> 2, limb = n & 3;
+    // limb writes: lane owns elements 8*lane.. of the gblock = group lane/16,
+    // elements 8*(lane%16).. of it
+    const int wr_off = (lane >> 4) * (VPS * 3 * GROUP) + 8 * (lane & 15);
+    const int inv_alpha = inv_alpha_exp(lane & 3);
+
+    v8i Bop[NS][GB];
+    float oscale[NS];  // 2^-sigma of the lane's vector, per set
+    auto build = [&](const uint4 *X) {
+#pragma unroll
+        for (int st = 0; st < NS; ++st) {
+            float inv_scale[VPS];
+#pragma unroll
+            for (int v = 0; v < VPS; ++v) {
+                const int b = st * SBS_VPS + v;
+                inv_scale[v] = 1.0f;
+                if (b < NB && b < B) {
+                    const int sigma = scale_exponent(wave_absmax_h(X[b]));
+                    inv_scale[v] = ldexpf(1.0f, -sigma);
+                    const Limbs L = split_limbs(X[b], ldexpf(1.0f, -(sigma + inv_alpha)));
+                    unsigned char *dst = stage + wr_off + v * 3 * GROUP;
+                    *(uint2 *)(dst + 0 * GROUP) = make_uint2(L.hi[0], L.hi[1]);
+                    *(uint2 *)(dst + 1 * GROUP) = make_uint2(L.mid[0], L.mid[1]);
+                    *(uint2 *)(dst + 2 * GROUP) = make_uint2(L.lo[0], L.lo[1]);
+                }
+            }
+            const bool act = limb < 3 && vb < VPS && st * SBS_VPS + vb < B;
+            float os = inv_scale[0];
+#pragma unroll
+            for (int v = 1; v < VPS; ++v)
+                os = vb == v ? inv_scale[v] : os;
+            oscale[st] = os;
+#pragma unroll
+            for (int g = 0; g < GB; ++g) {
+                const int lo = act ? ((g * VPS + vb) * 3 + limb) * GROUP + 16 * kb : ZERO;
+                const int hi = act ? lo + 64 : ZERO;
+                Bop[st][g] = lds_operand(stage + lo, stage + hi);
+            }
+        }
+    };
+    build(Xc);
+    uint4 Xn[MULTI ? NB : 1];
+    if constexpr (MULTI)
+        load_x(Xn, wv + nw);
+    __builtin_amdgcn_sched_barrier(0);
+
+    // red offset of this lane's (row, vector) partial; written by limb-0 lanes
+    float *red_w = red + (wv * NS * TILE_ROWS + (lane >> 4)) * SBS_VPS + vb;
+    const int red_tile = nw * NS * TILE_ROWS * SBS_VPS;
+    int cur_i = 0, cur_gb = wv;
+    for (int m0 = 0; m0 < n_items; m0 += D) {
+#pragma unroll
+        for (int j = 0; j < D; ++j) {
+            const int m = m0 + j;
+            if (m < n_items) {
+                if constexpr (MULTI) {
+                    if (cur_i == 0 && m > 0) {  // first item of the next gblock
+                        build(Xn);
+                        load_x(Xn, cur_gb + nw);
+                    }
+                }
+                const uint4 pw = transpose_rows4(P[j]);
+                const uint32_t words[GB] = {pw.x, pw.y, pw.z, pw.w};
+                float acc[NS];
+#pragma unroll
+                for (int st = 0; st < NS; ++st)
+                    acc[st] = 0.f;
+#pragma unroll
+                for (int g = 0; g < GB; ++g) {
+                    const v8i A = fp4_operand(words[g]);
+#pragma unroll
+                    for (int st = 0; st < NS; ++st) {
+                        const v4f d = mfma_fp4_fp8(A, Bop[st][g], v4f{0.f, 0.f, 0.f, 0.f});
+#pragma unroll
+                        for (int i = 0; i < K; ++i)
+                            acc[st] = fmaf(coef<K>(C[j], g, i), d[i], acc[st]);
+                    }
+                }
+#pragma unroll
+                for (int st = 0; st < NS; ++st) {
+                    float v = acc[st] * oscale[st];
+                    v += dpp_f32<DPP_QUAD_XOR1>(v);
+                    v += dpp_f32<DPP_QUAD_XOR2>(v);
+                    if (limb == 0) {
+                        float *r = red_w + cur_i * red_tile + st * TILE_ROWS * SBS_VPS;
+                        if (!MULTI || cur_gb == wv)
+                            *r = v;
+                        else
+                            *r += v;
+                    }
+                }
+                if (++cur_i == ntl && MULTI) {
+                    cur_i = 0;
+                    cur_gb += nw;
+                }
+            }
+            issue(j);
+        }
+    }
+
+    __syncthreads();
+    const int row_base = tile0 * TILE_ROWS;
+    const int rows = ntl * TILE_ROWS;
+    for (int idx = threadIdx.x; idx < rows * B; idx += blockDim.x) {
+        const int b = idx / rows, lr = idx % rows;
+        const int o = row_base + lr;
+        if (o < a.O) {
+            const int st = b / SBS_VPS, v = b % SBS_VPS;
+            const float *r = red + (lr / TILE_ROWS) * red_tile + (st * TILE_ROWS + lr % TILE_ROWS) * SBS_VPS + v;
+            float s = 0.f;
+            for (int w = 0; w < nw; ++w)
+                s += r[w * NS * TILE_ROWS * SBS_VPS];
+            a.y[(size_t)b * a.O + o] = __half_as_ushort(__float2half_rn(s));
+        }
+    }
+}
+
+// Kernels are compiled for NB = 2, 4 and 8 vectors; a call with B vectors
+// runs the smallest NB >= B (absent vectors are neither read nor written).
+template <int K, int NB>
+static const void *sbs_kernel_for(bool multi)
+{
+    return multi ? (const void *)gemm_sbs_kernel<K, NB, SBVR_SBS_DEPTH, true>
+                 : (const void *)gemm_sbs_kernel<K, NB, SBVR_SBS_DEPTH, false>;
+}
+
+template <int K>
+static const void *sbs_kernel_k(int nb, bool multi)
+{
+    return nb == 2 ? sbs_kernel_for<K, 2>(multi) : nb == 4 ? sbs_kernel_for<K, 4>(multi) : sbs_kernel_for<K, 8>(multi);
+}
+
+int launch_gemm_sbs(const Dims &d, const void *planes_dev, const void *coeffs_dev,
+                    const uint16_t *X, uint16_t *Y, int B, hipStream_t stream)
+{
+    const int nb = B <= 2 ? 2 : (B <= 4 ? 4 : 8);
+    const int gpw = (d.n_gblocks + SBVR_SBS_MAX_WAVES - 1) / SBVR_SBS_MAX_WAVES;
+    const int waves = (d.n_gblocks + gpw - 1) / gpw;
+    const int tpw = (d.n_tiles + SBVR_SBS_GROUPS - 1) / SBVR_SBS_GROUPS;
+    const int grid = (d.n_tiles + tpw - 1) / tpw;
+    const bool multi = gpw > 1;
+    GemvArgs a = {(const uint4 *)planes_dev, (const uint16_t *)coeffs_dev, X, Y, d.O, d.I, d.k,
+                  d.n_tiles, d.n_gblocks, gpw, B, tpw};
+    const size_t lds = (size_t)waves * sbs_stage_bytes(nb) +
+                       (size_t)tpw * waves * sbs_sets(nb) * TILE_ROWS * SBS_VPS * 4;
+    const void *fn = d.k == 4   ? sbs_kernel_k<4>(nb, multi)
+                     : d.k == 3 ? sbs_kernel_k<3>(nb, multi)
+                     : d.k == 2 ? sbs_kernel_k<2>(nb, multi)
+                                : sbs_kernel_k<1>(nb, multi);
+    void *args[] = {&a};
+    return launch_kernel(fn, dim3(grid), dim3(64 * waves), lds, stream, args);
+}
+
+}  // namespace sbvr
