@@ -4,10 +4,11 @@
 A step is one decoder layer's seven SBVR GEMVs (q, k, v, o, gate, up, down)
 at batch 1 with 4-bit SBVR weights (k = 4 planes, 128-weight groups, fp16
 coefficients), fp16 activations and outputs, in the Llama-3-8B projection
-shapes (Llama-3-70B with --model llama3-70b).  L independent layers of weights
-(~1.9 GiB, more than every cache) are captured into one HIP graph, layer after
-layer on one stream, as a decode step is served; K steps replay that graph
-K // L times and the first K % L layers once more.
+shapes (Llama-3-70B with --model llama3-70b).  The weights of L = 32 decoder
+layers (224 GEMVs, 3.93 GB at 4 bits: a full decode step of a 32-layer
+model, more than every cache) are captured into one HIP graph, layer after
+layer on one stream; K steps replay that graph K // L times and the first
+K % L layers once more.
 
 Weights are drawn directly in SBVR form (uniform bit planes, Gaussian fp16
 coefficients, seeded): GEMV time does not depend on the values.  The parity
@@ -15,14 +16,19 @@ tests run these same shapes and launch configurations against the CPU oracle.
 
 One JSON line is printed:
   value         aggregate algorithmic HBM throughput (GB/s) of the timed steps
+  decode_step   the L-layer graph alone: microseconds per token, GB/s
   per_call_us   mean duration of each projection's launch, from HIP events
-                around a graph of >= 64 back-to-back launches of that shape
-                (cycling through the layers) on the launch stream
+                around a graph of 64 back-to-back launches of that shape
+                cycling through >= 320 MB of distinct weight copies
   roofline      the dominant kernel instance (largest time per step):
                 algorithmic bytes per launch / its mean launch duration, vs the
                 8 TB/s HBM peak; traffic = calibrated FETCH_SIZE + WRITE_SIZE
                 bytes per launch from the recorded counter runs, when they were
                 taken on the current kernel sources (else null)
+  small_batch   per projection at B = 2, 4, 8 activation vectors
+                (sbvr_gemm_small_batch), same timing
+  low_bit       per projection at k = 2 and 3 planes, same timing
+  llama3_70b    per projection of the Llama-3-70B shapes, same timing
   cpu_baseline  the CPU oracle (binary64 decompress + GEMV) on layer 0's seven
                 GEMVs, bounded to ~10 s of work, in the same unit
 
@@ -62,7 +68,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=64)
     ap.add_argument("--warmup", type=int, default=16)
     ap.add_argument("--model", choices=("llama3-8b", "llama3-70b"), default="llama3-8b")
-    ap.add_argument("--layers", type=int, default=0, help="distinct weight sets (0: ~1.9 GiB)")
+    ap.add_argument("--layers", type=int, default=0, help="decoder layers in the decode-step graph (0: 32)")
+    ap.add_argument("--quick", action="store_true", help="skip the small-batch, k = 2/3 and other-model tables")
     ap.add_argument("--k", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
@@ -155,6 +162,9 @@ def b1_kernel_instance(O: int, I: int, k: int) -> str:
     return f"gemv_b1_kernel<{k}, {T}>"
 
 
+ROTATE_BYTES = 320e6  # > 256 MB MALL + 8 x 4 MB L2
+
+
 def main():
     args = parse()
     if args.traffic_summary:
@@ -177,10 +187,13 @@ def main():
     k = args.k
     nbytes = {n: sb.algorithmic_bytes(*shapes[n], k) for n in PROJ_ORDER}
     layer_bytes = sum(nbytes.values())
-    L = args.layers or max(2, int(np.ceil(1.9 * 2 ** 30 / layer_bytes)))
+    L = args.layers or 32
     if args.traffic_probe:
         L = PROBE_LAUNCHES
     cfg_index = 1 if args.model == "llama3-8b" else 3
+
+    def to_dev(planes, coeffs):
+        return (torch.from_numpy(planes.view(np.int32)).to(dev), torch.from_numpy(coeffs.view(np.int16)).to(dev))
 
     # ---- weights: L layers x 7 projections, packed into the device format ----
     host_layer0 = {}
@@ -193,8 +206,7 @@ def main():
             planes, coeffs = synth.random_sbvr(O, I, k, seed=seed)
             if li == 0:
                 host_layer0[name] = (planes, coeffs)
-            W = sb.pack(torch.from_numpy(planes.view(np.int32)).to(dev),
-                        torch.from_numpy(coeffs.view(np.int16)).to(dev))
+            W = sb.pack(*to_dev(planes, coeffs))
             x = torch.from_numpy(synth.activations(I, seed=seed + synth.X_SEED_OFFSET)).to(dev)
             y = torch.empty(O, dtype=torch.float16, device=dev)
             lay[name] = (W, x, y)
@@ -223,10 +235,11 @@ def main():
         return
 
     def capture(calls):
+        """One graph of (fn, args) launches on the bench stream."""
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g, stream=stream):
-            for W, x, y in calls:
-                sb.gemv(W, x, out=y, stream=stream)
+            for fn, a in calls:
+                fn(*a, stream=stream)
         return g
 
     e0 = torch.cuda.Event(enable_timing=True)
@@ -240,10 +253,13 @@ def main():
         torch.cuda.synchronize()
         return e0.elapsed_time(e1)  # ms
 
+    def gemv_call(W, x, y):
+        return (lambda W, x, y, stream: sb.gemv(W, x, out=y, stream=stream)), (W, x, y)
+
     # ---- timed region: K steps = K // L replays of the L-layer decode graph,
     # then the first K % L layers' graphs ----
-    decode_graph = capture([layers[li][n] for li in range(L) for n in PROJ_ORDER])
-    layer_graphs = [capture([layers[li][n] for n in PROJ_ORDER]) for li in range(L)]
+    decode_graph = capture([gemv_call(*layers[li][n]) for li in range(L) for n in PROJ_ORDER])
+    layer_graphs = [capture([gemv_call(*layers[li][n]) for n in PROJ_ORDER]) for li in range(L)]
     torch.cuda.synchronize()
 
     def run_steps(n):
@@ -258,17 +274,48 @@ def main():
     total_ms = timed(lambda: run_steps(args.steps))
     ms_per_step = total_ms / args.steps
     value = layer_bytes * args.steps / (total_ms * 1e-3) / 1e9
+    # the decode step alone (configs: one token through all L layers)
+    step_reps = [timed(decode_graph.replay) * 1e3 for _ in range(5)]
+    decode_us = float(np.median(step_reps))
+    decode_step = {"layers": L, "gemvs": 7 * L, "bytes": layer_bytes * L, "us_per_token": round(decode_us, 2),
+                   "gbps": round(layer_bytes * L / (decode_us * 1e3), 1),
+                   "replays": len(step_reps)}
     del decode_graph, layer_graphs
 
-    # ---- per-shape launch durations: >= 64 back-to-back launches per graph ----
-    n_launch = max(64, L)
+    # ---- per-launch durations: >= 64 back-to-back launches per graph, cycling
+    # through distinct weight copies totalling >= ROTATE_BYTES ----
+    def launch_us(calls, n_launch=64):
+        g = capture([calls[i % len(calls)] for i in range(max(n_launch, len(calls)))])
+        n = max(n_launch, len(calls))
+        timed(g.replay)
+        reps = [timed(g.replay) * 1e3 / n for _ in range(5)]
+        del g
+        return float(np.median(reps))
+
+    def copies(O, I, kk, planes, coeffs, have):
+        """Extra packed copies (same content, distinct memory) so that `have`
+        copies plus these rotate through >= ROTATE_BYTES."""
+        per = sb.algorithmic_bytes(O, I, kk)
+        need = max(0, int(np.ceil(ROTATE_BYTES / per)) - have)
+        if need == 0:
+            return []
+        p, c = to_dev(planes, coeffs)
+        return [sb.pack(p, c) for _ in range(need)]
+
+    weights = {}  # projection -> list of packed copies (the L layers first)
+    for name in PROJ_ORDER:
+        O, I = shapes[name]
+        extra = copies(O, I, k, *host_layer0[name], have=L)
+        weights[name] = [layers[li][name][0] for li in range(L)] + extra
+    torch.cuda.synchronize()
+
     per_call_us = {}
     for name in PROJ_ORDER:
-        g = capture([layers[i % L][name] for i in range(n_launch)])
-        timed(g.replay)
-        reps = [timed(g.replay) * 1e3 / n_launch for _ in range(3)]
-        per_call_us[name] = float(np.median(reps))
-        del g
+        O, I = shapes[name]
+        ws = weights[name]
+        xs = [torch.from_numpy(synth.activations(I, seed=900 + i)).to(dev) for i in range(min(len(ws), 64))]
+        ys = [torch.empty(O, dtype=torch.float16, device=dev) for _ in range(len(xs))]
+        per_call_us[name] = launch_us([gemv_call(w, xs[i % len(xs)], ys[i % len(ys)]) for i, w in enumerate(ws)])
     per_call_gbps = {n: nbytes[n] / (per_call_us[n] * 1e3) for n in PROJ_ORDER}
 
     # dominant kernel instance: largest launch time per step
@@ -282,13 +329,61 @@ def main():
     achieved = db / (dt * 1e3)  # (bytes per launch) / (mean launch duration), GB/s
     roofline = {
         "bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_GBPS, "unit": "GB/s",
-        "frac": round(achieved / PEAK_GBPS, 4), "traffic": load_traffic(dom) if k == 4 and args.model == "llama3-8b" else None,
+        "frac": round(achieved / PEAK_GBPS, 4),
+        "traffic": load_traffic(dom) if k == 4 and args.model == "llama3-8b" else None,
         "kernel": dom,
         "launches_per_step": dc,
         "projections": [n for n in PROJ_ORDER if b1_kernel_instance(*shapes[n], k) == dom],
         "bytes_per_launch": round(db / dc),
         "mean_launch_us": round(dt / dc, 3),
     }
+
+    def gemm_call(W, X, Y):
+        return (lambda W, X, Y, stream: sb.gemm_small_batch(W, X, out=Y, stream=stream)), (W, X, Y)
+
+    # ---- small batch (B = 2, 4, 8) on the same weight copies ----
+    small_batch = {}
+    if not args.quick:
+        for B in (2, 4, 8):
+            res = {}
+            for name in PROJ_ORDER:
+                O, I = shapes[name]
+                ws = weights[name]
+                Xs = [torch.from_numpy(synth.activations(I, seed=700 + i, batch=B)).to(dev) for i in range(8)]
+                Ys = [torch.empty((B, O), dtype=torch.float16, device=dev) for _ in range(8)]
+                us = launch_us([gemm_call(w, Xs[i % 8], Ys[i % 8]) for i, w in enumerate(ws)])
+                bb = sb.algorithmic_bytes(O, I, k, B)
+                res[name] = {"us": round(us, 3), "gbps": round(bb / (us * 1e3), 1)}
+            small_batch[str(B)] = res
+
+    # ---- fewer planes (k = 2, 3) and the other model's shapes ----
+    def shape_table(shp, kk, seed_cfg):
+        res = {}
+        for pi, name in enumerate(PROJ_ORDER):
+            O, I = shp[name]
+            if name in res or any(shp[m] == (O, I) and m in res for m in res):
+                same = next(m for m in res if shp[m] == (O, I))
+                res[name] = res[same]
+                continue
+            planes, coeffs = synth.random_sbvr(O, I, kk, seed=synth.seed_for(seed_cfg, 0, pi))
+            ws = copies(O, I, kk, planes, coeffs, have=0)
+            x = torch.from_numpy(synth.activations(I, seed=seed_cfg + pi + synth.X_SEED_OFFSET)).to(dev)
+            y = torch.empty(O, dtype=torch.float16, device=dev)
+            us = launch_us([gemv_call(w, x, y) for w in ws])
+            bb = sb.algorithmic_bytes(O, I, kk)
+            res[name] = {"us": round(us, 3), "gbps": round(bb / (us * 1e3), 1), "copies": len(ws)}
+            del ws
+            torch.cuda.empty_cache()
+        return res
+
+    low_bit, other_model = {}, None
+    if not args.quick:
+        if args.model == "llama3-8b" and k == 4:
+            for kk in (2, 3):
+                low_bit[str(kk)] = shape_table(shapes, kk, 2)
+            other_model = shape_table(synth.LLAMA70B, 4, 3)
+        elif args.model == "llama3-70b":
+            other_model = shape_table(synth.LLAMA8B, k, 1)
 
     # ---- CPU baseline: the oracle on layer 0, bounded ----
     cpu = None
@@ -325,7 +420,7 @@ def main():
         "data": "synthetic: seeded SBVR planes and fp16 coefficients, N(0,1) fp16 activations",
         "config": {
             "workload": f"{args.model} decode-layer projections q,k,v,o,gate,up,down; SBVR k={k}, "
-                        f"group 128, batch 1; {L} layers in one hipGraph on one stream",
+                        f"group 128, batch 1; {L} layers ({7 * L} GEMVs) in one hipGraph on one stream",
             "bytes_per_step": layer_bytes,
             "layers_rotated": L,
             "shapes": {n: list(shapes[n]) for n in PROJ_ORDER},
@@ -334,6 +429,10 @@ def main():
         "per_call_us": {n: round(v, 3) for n, v in per_call_us.items()},
         "per_call_gbps": {n: round(v, 1) for n, v in per_call_gbps.items()},
         "roofline": roofline,
+        "decode_step": decode_step,
+        "small_batch": small_batch or None,
+        "low_bit": low_bit or None,
+        ("llama3_70b" if args.model == "llama3-8b" else "llama3_8b"): other_model,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

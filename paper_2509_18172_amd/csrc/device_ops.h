@@ -160,17 +160,25 @@ __device__ __forceinline__ Limbs make_limbs(uint4 xv, float scale)
 }
 
 // Three E4M3 limbs by splitting in binary16 (cheaper than make_limbs).
-// The truncation split hi = x with its mantissa cut to 3 bits, mid = the same
-// cut of x - hi, lo = x - hi - mid is exact in binary16 (every difference is
-// representable), and each piece has at most 4 significant bits, so the
-// scaled conversion fp8(piece / scale_div) is exact while the scaled value
-// lies in the E4M3 range.  scale_div = 2^-(sigma + log2(1/alpha)).
+// The activations are first multiplied by 2^s1, s1 = min(sigma, 15) (a
+// binary16 power of two: exact), which makes every element that matters
+// (above 2^-9 of the block maximum) a normal binary16 number.  The truncation
+// split hi = x' with its mantissa cut to 3 bits, mid = the same cut of x' - hi,
+// lo = x' - hi - mid is then exact (every difference is representable) and
+// each piece has at most 4 significant bits, so the scaled conversion
+// fp8(piece * 2^(sigma - s1 + log2(1/alpha))) is exact while the result lies
+// in the E4M3 range.
 typedef _Float16 h2_t __attribute__((ext_vector_type(2)));
 typedef short s2_t __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ uint32_t h2_sub(uint32_t a, uint32_t b)
 {
     return __builtin_bit_cast(uint32_t, __builtin_bit_cast(h2_t, a) - __builtin_bit_cast(h2_t, b));
+}
+
+__device__ __forceinline__ uint32_t h2_mul(uint32_t a, h2_t f)
+{
+    return __builtin_bit_cast(uint32_t, __builtin_bit_cast(h2_t, a) * f);
 }
 
 __device__ __forceinline__ uint32_t cvt2_fp8(uint32_t lo_pair, uint32_t hi_pair, float scale_div)
@@ -181,10 +189,16 @@ __device__ __forceinline__ uint32_t cvt2_fp8(uint32_t lo_pair, uint32_t hi_pair,
     return __builtin_bit_cast(uint32_t, r);
 }
 
-__device__ __forceinline__ Limbs split_limbs(uint4 xv, float scale_div)
+// sigma: the block's scale exponent (scale_exponent); inv_alpha: log2(1/alpha)
+// of the lane's elements.
+__device__ __forceinline__ Limbs split_limbs(uint4 xv, int sigma, int inv_alpha)
 {
     constexpr uint32_t CUT = 0xFF80FF80u;  // sign, exponent and 3 mantissa bits of each half
-    const uint32_t w[4] = {xv.x, xv.y, xv.z, xv.w};
+    const int s1 = min(sigma, 15);
+    const _Float16 f = (_Float16)ldexpf(1.0f, s1);
+    const h2_t f2 = {f, f};
+    const float scale_div = ldexpf(1.0f, -(sigma - s1 + inv_alpha));
+    const uint32_t w[4] = {h2_mul(xv.x, f2), h2_mul(xv.y, f2), h2_mul(xv.z, f2), h2_mul(xv.w, f2)};
     uint32_t hi[4], mid[4], lo[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {

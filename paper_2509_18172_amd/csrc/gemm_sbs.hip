@@ -184,7 +184,7 @@ __global__ void __launch_bounds__(512) gemm_sbs_kernel(GemvArgs a)
                 if (b < NB && b < B) {
                     const int sigma = scale_exponent(wave_absmax_h(X[b]));
                     inv_scale[v] = ldexpf(1.0f, -sigma);
-                    const Limbs L = split_limbs(X[b], ldexpf(1.0f, -(sigma + inv_alpha)));
+                    const Limbs L = split_limbs(X[b], sigma, inv_alpha);
                     unsigned char *dst = stage + wr_off + v * 3 * GROUP;
                     *(uint2 *)(dst + 0 * GROUP) = make_uint2(L.hi[0], L.hi[1]);
                     *(uint2 *)(dst + 1 * GROUP) = make_uint2(L.mid[0], L.mid[1]);
@@ -219,49 +219,56 @@ __global__ void __launch_bounds__(512) gemm_sbs_kernel(GemvArgs a)
 #pragma unroll
         for (int j = 0; j < D; ++j) {
             const int m = m0 + j;
-            if (m < n_items) {
-                if constexpr (MULTI) {
-                    if (cur_i == 0 && m > 0) {  // first item of the next gblock
-                        build(Xn);
-                        load_x(Xn, cur_gb + nw);
-                    }
+            // Items past the end read zero planes and coefficients; only
+            // their stores are skipped, so the unrolled body has no branch
+            // (apart from the rebuild at a gblock change).
+            const bool valid = m < n_items;
+            if constexpr (MULTI) {
+                if (valid && cur_i == 0 && m > 0) {  // first item of the next gblock
+                    build(Xn);
+                    load_x(Xn, cur_gb + nw);
                 }
-                const uint4 pw = transpose_rows4(P[j]);
-                const uint32_t words[GB] = {pw.x, pw.y, pw.z, pw.w};
-                float acc[NS];
+            }
+            const uint4 pw = transpose_rows4(P[j]);
+            const uint32_t words[GB] = {pw.x, pw.y, pw.z, pw.w};
+            v4f d[GB][NS];
+#pragma unroll
+            for (int g = 0; g < GB; ++g) {
+                const v8i A = fp4_operand(words[g]);
 #pragma unroll
                 for (int st = 0; st < NS; ++st)
-                    acc[st] = 0.f;
+                    d[g][st] = mfma_fp4_fp8(A, Bop[st][g], v4f{0.f, 0.f, 0.f, 0.f});
+            }
+            const CoefRow<K> cr = C[j];
+            issue(j);
+#pragma unroll
+            for (int st = 0; st < NS; ++st) {
+                float part[GB];
 #pragma unroll
                 for (int g = 0; g < GB; ++g) {
-                    const v8i A = fp4_operand(words[g]);
+                    float t = coef<K>(cr, g, 0) * d[g][st][0];
 #pragma unroll
-                    for (int st = 0; st < NS; ++st) {
-                        const v4f d = mfma_fp4_fp8(A, Bop[st][g], v4f{0.f, 0.f, 0.f, 0.f});
-#pragma unroll
-                        for (int i = 0; i < K; ++i)
-                            acc[st] = fmaf(coef<K>(C[j], g, i), d[i], acc[st]);
-                    }
+                    for (int i = 1; i < K; ++i)
+                        t = fmaf(coef<K>(cr, g, i), d[g][st][i], t);
+                    part[g] = t;
                 }
-#pragma unroll
-                for (int st = 0; st < NS; ++st) {
-                    float v = acc[st] * oscale[st];
-                    v += dpp_f32<DPP_QUAD_XOR1>(v);
-                    v += dpp_f32<DPP_QUAD_XOR2>(v);
-                    if (limb == 0) {
-                        float *r = red_w + cur_i * red_tile + st * TILE_ROWS * SBS_VPS;
-                        if (!MULTI || cur_gb == wv)
-                            *r = v;
-                        else
-                            *r += v;
-                    }
+                float v = ((part[0] + part[1]) + (part[2] + part[3])) * oscale[st];
+                v += dpp_f32<DPP_QUAD_XOR1>(v);
+                v += dpp_f32<DPP_QUAD_XOR2>(v);
+                if (valid && limb == 0) {
+                    float *r = red_w + cur_i * red_tile + st * TILE_ROWS * SBS_VPS;
+                    if (!MULTI || cur_gb == wv)
+                        *r = v;
+                    else
+                        *r += v;
                 }
+            }
+            if (valid) {
                 if (++cur_i == ntl && MULTI) {
                     cur_i = 0;
                     cur_gb += nw;
                 }
             }
-            issue(j);
         }
     }
 
@@ -303,13 +310,16 @@ int launch_gemm_sbs(const Dims &d, const void *planes_dev, const void *coeffs_de
     const int nb = B <= 2 ? 2 : (B <= 4 ? 4 : 8);
     const int gpw = (d.n_gblocks + SBVR_SBS_MAX_WAVES - 1) / SBVR_SBS_MAX_WAVES;
     const int waves = (d.n_gblocks + gpw - 1) / gpw;
-    const int tpw = (d.n_tiles + SBVR_SBS_GROUPS - 1) / SBVR_SBS_GROUPS;
+    // tiles per workgroup, capped so that dynamic LDS stays within 64 KiB
+    const size_t fixed = (size_t)waves * sbs_stage_bytes(nb);
+    const size_t per_tile = (size_t)waves * sbs_sets(nb) * TILE_ROWS * SBS_VPS * 4;
+    const int max_tpw = (int)((SBVR_MAX_DYN_LDS - fixed) / per_tile);
+    const int tpw = min((d.n_tiles + SBVR_SBS_GROUPS - 1) / SBVR_SBS_GROUPS, max_tpw);
     const int grid = (d.n_tiles + tpw - 1) / tpw;
     const bool multi = gpw > 1;
     GemvArgs a = {(const uint4 *)planes_dev, (const uint16_t *)coeffs_dev, X, Y, d.O, d.I, d.k,
                   d.n_tiles, d.n_gblocks, gpw, B, tpw};
-    const size_t lds = (size_t)waves * sbs_stage_bytes(nb) +
-                       (size_t)tpw * waves * sbs_sets(nb) * TILE_ROWS * SBS_VPS * 4;
+    const size_t lds = fixed + (size_t)tpw * per_tile;
     const void *fn = d.k == 4   ? sbs_kernel_k<4>(nb, multi)
                      : d.k == 3 ? sbs_kernel_k<3>(nb, multi)
                      : d.k == 2 ? sbs_kernel_k<2>(nb, multi)

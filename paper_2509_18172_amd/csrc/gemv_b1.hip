@@ -102,8 +102,8 @@ __global__ void __launch_bounds__(1024) gemv_b1_kernel(GemvArgs a)
     // returns 2^-sigma, the factor that undoes the activation scaling.
     auto operands = [&](const B1Regs<K, T> &R, v8i *Bq) -> float {
         const uint4 xv = gb * (GB * GROUP) + lane * 8 < a.I ? R.x : make_uint4(0u, 0u, 0u, 0u);
-        const int sigma = scale_exponent(wave_max(absmax8(xv)));
-        const Limbs L = make_limbs(xv, ldexpf(1.0f, sigma + inv_alpha));
+        const int sigma = scale_exponent(wave_absmax_h(xv));
+        const Limbs L = split_limbs(xv, sigma, inv_alpha);
         // same wavefront: the LDS writes complete before the reads below
         *(uint2 *)(lds + wr_off + 0 * 32) = make_uint2(L.hi[0], L.hi[1]);
         *(uint2 *)(lds + wr_off + 1 * 32) = make_uint2(L.mid[0], L.mid[1]);

@@ -142,9 +142,9 @@ __global__ void __launch_bounds__(1024) gemv_b1s_kernel(GemvArgs a)
     float inv_scale;
     auto build = [&](uint4 xr, int gb) {
         const uint4 xv = gb * (GB * GROUP) + lane * 8 < a.I ? xr : make_uint4(0u, 0u, 0u, 0u);
-        const int sigma = scale_exponent(wave_max(absmax8(xv)));
+        const int sigma = scale_exponent(wave_absmax_h(xv));
         inv_scale = ldexpf(1.0f, -sigma);
-        const Limbs L = make_limbs(xv, ldexpf(1.0f, sigma + inv_alpha));
+        const Limbs L = split_limbs(xv, sigma, inv_alpha);
         // same wavefront: these writes land before the reads below, and after
         // the reads of the previous gblock's operand
         *(uint2 *)(lds + wr_off + 0 * 32) = make_uint2(L.hi[0], L.hi[1]);

@@ -10,6 +10,10 @@
 
 namespace sbvr {
 
+// Dynamic LDS per workgroup that a launch may request without raising the
+// kernel's attribute; launch shapes are capped to stay within it.
+constexpr size_t SBVR_MAX_DYN_LDS = 64 * 1024;
+
 inline int launch_kernel(const void *fn, dim3 grid, dim3 block, size_t lds, hipStream_t stream,
                          void **args)
 {

@@ -159,6 +159,21 @@ def test_small_batch_full_size(sb, O, I, B):
     assert rel_err(Y[0], y0.astype(np.float64)) <= TOL
 
 
+@pytest.mark.parametrize("B", [2, 8])
+@pytest.mark.parametrize("O,I", SHAPES_70B)
+def test_small_batch_70b_full_size(sb, O, I, B):
+    """Llama-3-70B shapes at B = 2 and 8: the 28672-row shapes need more LDS
+    per workgroup than a launch may request unless tiles per workgroup are
+    capped."""
+    planes, coeffs = synth.random_sbvr(O, I, 4, seed=O + 5 * I + B)
+    X = synth.activations(I, seed=B + 3 * O + synth.X_SEED_OFFSET, batch=B)
+    Y = run_gemm(sb, packed(sb, planes, coeffs), X)
+    Y_ref = oracle.sbvr_gemv(planes, coeffs, X)
+    errs = [rel_err(Y[b], Y_ref[b]) for b in range(B)]
+    log(f"small batch 70b {O}x{I} B={B} worst err={max(errs):.3e}")
+    assert max(errs) <= TOL
+
+
 @pytest.mark.parametrize("k", [1, 2, 3])
 def test_small_batch_low_bit(sb, k):
     O, I = 520, 1920
@@ -291,10 +306,11 @@ def test_activation_dynamic_range(sb):
         "zero": (np.zeros(I), 1.0),
         "one_big": (np.r_[65504.0, np.full(I - 1, 2.0 ** -24)], 1.0),
     }
-    W_big = packed(sb, planes, (coeffs.view(np.float16) * np.float16(1e4)).view(np.uint16))
+    c_big = (coeffs.view(np.float16) * np.float16(1e4)).view(np.uint16)
+    W_big = packed(sb, planes, c_big)
+    W_one = packed(sb, planes, coeffs)
     for name, (xv, cscale) in cases.items():
-        W = W_big if cscale != 1.0 else packed(sb, planes, coeffs)
-        c_used = coeffs if cscale == 1.0 else (coeffs.view(np.float16) * np.float16(1e4)).view(np.uint16)
+        W, c_used = (W_big, c_big) if cscale != 1.0 else (W_one, coeffs)
         x = xv.astype(np.float16)
         y_ref = oracle.sbvr_gemv(planes, c_used, x)
         y = run_gemv(sb, W, x)
@@ -302,6 +318,19 @@ def test_activation_dynamic_range(sb):
             assert np.all(y == 0), name
         else:
             assert rel_err(y, y_ref) <= TOL, (name, rel_err(y, y_ref))
+    # the same cases through the small-batch kernels, one vector each (each
+    # vector has its own activation scale), for 2-, 4- and 8-vector kernels
+    for cscale, W, c_used in ((1.0, W_one, coeffs), (1e4, W_big, c_big)):
+        xs = [v.astype(np.float16) for v, c in cases.values() if c == cscale]
+        for B in (2, 4, 8):
+            X = np.stack([xs[b % len(xs)] if b % 3 else (xs[b % len(xs)] * np.float16(0.5)) for b in range(B)])
+            Y = run_gemm(sb, W, X)
+            Y_ref = oracle.sbvr_gemv(planes, c_used, X)
+            for b in range(B):
+                if np.abs(Y_ref[b]).max() == 0:
+                    assert np.all(Y[b] == 0), (cscale, B, b)
+                else:
+                    assert rel_err(Y[b], Y_ref[b]) <= TOL, (cscale, B, b, rel_err(Y[b], Y_ref[b]))
 
 
 def test_output_canary_and_error_paths(sb):
