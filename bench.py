@@ -151,10 +151,12 @@ def b1_kernel_instance(O: int, I: int, k: int) -> str:
     """Name of the batch-1 kernel instance the library launches for an O x I
     matrix: the streaming kernel (ring depth D, several gblocks per wavefront
     or one) when a row has more than 16 gblocks of 512 elements or the matrix
-    has at least 24576 (4-row tile, gblock) blocks; otherwise the one-shot
+    has at least 24576 (tile, gblock) blocks (tiles of 16/k rows, 4 at k = 3);
+    otherwise the one-shot
     kernel with T tiles per workgroup, the most of 8/4/2/1 that still leaves
     >= 256 workgroups."""
-    n_tiles, n_gblocks = (O + 3) // 4, (I + 511) // 512
+    tr = {1: 16, 2: 8}.get(k, 4)  # rows per tile: 16 matrix-core rows of (row, plane)
+    n_tiles, n_gblocks = (O + tr - 1) // tr, (I + 511) // 512
     if n_gblocks > 16 or n_tiles * n_gblocks >= 24576:
         multi = n_gblocks > 16
         return f"gemv_b1s_kernel<{k}, {3 if multi else 2}, {'true' if multi else 'false'}>"

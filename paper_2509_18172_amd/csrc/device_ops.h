@@ -283,31 +283,60 @@ __device__ __forceinline__ uint4 load_nt16(const uint4 *p)
     return make_uint4(v[0], v[1], v[2], v[3]);
 }
 
-// K coefficients of one (row, group) of a device coefficient block, as raw
-// binary16 words (c0 | c1 << 16, c2 | c3 << 16); planes >= K read as zero.
+// Coefficients of a lane's four D rows.  A lane of a 16x16 result holds the
+// rows m = 4q .. 4q+3 (q = lane / 16) of one column; for one group slot b
+// their coefficients are the contiguous entries (q * GB + b) * CPL + j of the
+// coefficient block (j < CPL = 4 coefficients, 3 for K = 3), returned as raw
+// binary16 words (c0 | c1 << 16, c2 | c3 << 16); missing ones read zero.
 template <int K>
-__device__ __forceinline__ uint2 load_coeffs(const uint16_t *p)
+__host__ __device__ constexpr int coefs_per_lane() { return coefs_per_quad(K); }
+
+template <int K>
+__device__ __forceinline__ uint2 load_coefs4(const uint16_t *p)
 {
-    if constexpr (K == 4) {
-        const v2u_t v = __builtin_nontemporal_load((const v2u_t *)p);
-        return make_uint2(v[0], v[1]);
-    } else if constexpr (K == 2) {
-        return make_uint2(__builtin_nontemporal_load((const uint32_t *)p), 0u);
-    } else if constexpr (K == 3) {
+    if constexpr (K == 3) {
         return make_uint2((uint32_t)p[0] | ((uint32_t)p[1] << 16), (uint32_t)p[2]);
     } else {
-        return make_uint2((uint32_t)p[0], 0u);
+        const v2u_t v = __builtin_nontemporal_load((const v2u_t *)p);
+        return make_uint2(v[0], v[1]);
     }
 }
 
-// sum_r c_r * d_r over the four D rows (planes) of a lane.
-__device__ __forceinline__ float apply_coeffs(uint2 c, const v4f &d)
+// Row partial sums of a lane: the coefficients times its four D values,
+// grouped by output row.  A rows m = r * RS + i (RS = row slots), so a lane's
+// four rows belong to NP = 4 / RS tile rows: rows q * NP + p, p < NP.
+template <int K>
+__host__ __device__ constexpr int partials_per_lane() { return 4 / row_slots(K); }
+
+template <int K>
+__device__ __forceinline__ void apply_coefs(uint2 c, const v4f &d, float *p)
 {
-    float s = half_bits_to_float(c.x & 0xffffu) * d[0];
-    s = fmaf(half_bits_to_float(c.x >> 16), d[1], s);
-    s = fmaf(half_bits_to_float(c.y & 0xffffu), d[2], s);
-    s = fmaf(half_bits_to_float(c.y >> 16), d[3], s);
-    return s;
+    const float c0 = half_bits_to_float(c.x & 0xffffu), c1 = half_bits_to_float(c.x >> 16);
+    const float c2 = half_bits_to_float(c.y & 0xffffu), c3 = half_bits_to_float(c.y >> 16);
+    if constexpr (row_slots(K) == 4) {
+        p[0] = fmaf(c3, d[3], fmaf(c2, d[2], fmaf(c1, d[1], c0 * d[0])));
+    } else if constexpr (row_slots(K) == 2) {
+        p[0] = fmaf(c1, d[1], c0 * d[0]);
+        p[1] = fmaf(c3, d[3], c2 * d[2]);
+    } else {
+        p[0] = c0 * d[0];
+        p[1] = c1 * d[1];
+        p[2] = c2 * d[2];
+        p[3] = c3 * d[3];
+    }
+}
+
+// A-operand slot of a lane within a plane block: lane (row m = lane % 16,
+// k-block b = lane / 16) takes the 16 bytes of (group slot b, tile row
+// m / RS, plane m % RS); `ok` is false for the empty plane slots of K = 3.
+template <int K>
+__device__ __forceinline__ unsigned a_slot_bytes(int lane, bool &ok)
+{
+    constexpr int RS = row_slots(K), TR = tile_rows(K);
+    const int m = lane & 15, b = lane >> 4;
+    const int r = m / RS, i = m % RS;
+    ok = i < K;
+    return (unsigned)((b * TR + r) * K + (ok ? i : 0)) * 16u;
 }
 
 // Buffer-resource loads.  A descriptor bounds a byte range; a lane whose
@@ -330,22 +359,18 @@ __device__ __forceinline__ uint4 buf_load16(buf_rsrc r, unsigned off)
     return make_uint4(v[0], v[1], v[2], v[3]);
 }
 
-// load_coeffs through a descriptor (byte offset of the (row, group) entry).
+// load_coefs4 through a descriptor (byte offset of the lane's first entry).
 template <int K>
-__device__ __forceinline__ uint2 buf_coeffs(buf_rsrc r, unsigned off)
+__device__ __forceinline__ uint2 buf_coefs4(buf_rsrc r, unsigned off)
 {
-    if constexpr (K == 4) {
-        const v2u_t v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, BUF_NT);
-        return make_uint2(v[0], v[1]);
-    } else if constexpr (K == 2) {
-        return make_uint2(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, BUF_NT), 0u);
-    } else if constexpr (K == 3) {
+    if constexpr (K == 3) {
         const unsigned c0 = __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, BUF_NT);
         const unsigned c1 = __builtin_amdgcn_raw_buffer_load_b16(r, off + 2, 0, BUF_NT);
         const unsigned c2 = __builtin_amdgcn_raw_buffer_load_b16(r, off + 4, 0, BUF_NT);
         return make_uint2(c0 | (c1 << 16), c2);
     } else {
-        return make_uint2((unsigned)__builtin_amdgcn_raw_buffer_load_b16(r, off, 0, BUF_NT), 0u);
+        const v2u_t v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, BUF_NT);
+        return make_uint2(v[0], v[1]);
     }
 }
 

@@ -2,7 +2,7 @@
 // each vector), streaming the weights once for all B vectors.
 //
 // Work decomposition (as the batch-1 streaming kernel): a workgroup owns tpw
-// consecutive tiles (4 rows) and every gblock (512 inner elements) of them;
+// consecutive tiles (TR rows) and every gblock (512 inner elements) of them;
 // wavefront w takes gblocks w, w+W, ...  Its items (gblock, tile) stream
 // through a D-deep register ring loaded with buffer descriptors bounded by
 // the workgroup's tile range (loads past the end read zero, no traffic).
@@ -16,9 +16,9 @@
 // words of group b; a 4 x 4 cross-lane transpose turns that into word b of
 // the four groups, i.e. the A operands of the four instructions of an item.
 //
-// Each lane applies its tile row's coefficients to its four D rows (planes)
-// for every group, the four limb columns of a vector are summed by a quad
-// reduction, and one lane per (row, vector) adds the item's partial sum to
+// Each lane applies the coefficients of its four D rows (the planes of 1, 2 or
+// 4 tile rows) for every group, the four limb columns of a vector are summed
+// by a quad reduction, and one lane per (row, vector) adds the item's sum to
 // LDS; the workgroup sums the wavefronts in order at the end (deterministic,
 // no global workspace).
 #include "device_ops.h"
@@ -43,47 +43,46 @@ __host__ __device__ constexpr int sbs_sets(int nb) { return (nb + SBS_VPS - 1) /
 __host__ __device__ constexpr int sbs_vps(int nb) { return nb < SBS_VPS ? nb : SBS_VPS; }
 __host__ __device__ constexpr int sbs_stage_bytes(int nb) { return GB * sbs_vps(nb) * 3 * GROUP + 32; }
 
-// The 4K binary16 coefficients of one tile row over the four groups of a
-// gblock, (group, plane) order, as 2K words.
+// The coefficients of a lane's four D rows for the four groups of a gblock:
+// 4 * CPL contiguous binary16 entries (q * GB * CPL ..), group g's at g * CPL.
 template <int K>
-struct CoefRow {
-    uint32_t w[2 * K];
+struct CoefGroups {
+    uint32_t w[2 * coefs_per_lane<K>()];
 };
 
 template <int K>
-__device__ __forceinline__ CoefRow<K> buf_coef_row(buf_rsrc r, unsigned off)
+__device__ __forceinline__ CoefGroups<K> buf_coef_groups(buf_rsrc r, unsigned off)
 {
-    CoefRow<K> c;
-    if constexpr (K >= 2) {
-        const v4u_t v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, BUF_NT);
-        c.w[0] = v[0];
-        c.w[1] = v[1];
-        c.w[2] = v[2];
-        c.w[3] = v[3];
-    }
-    if constexpr (K == 4) {
-        const v4u_t v = __builtin_amdgcn_raw_buffer_load_b128(r, off + 16, 0, BUF_NT);
-        c.w[4] = v[0];
-        c.w[5] = v[1];
-        c.w[6] = v[2];
-        c.w[7] = v[3];
-    } else if constexpr (K == 3) {
-        const v2u_t v = __builtin_amdgcn_raw_buffer_load_b64(r, off + 16, 0, BUF_NT);
-        c.w[4] = v[0];
-        c.w[5] = v[1];
-    } else if constexpr (K == 1) {
-        const v2u_t v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, BUF_NT);
-        c.w[0] = v[0];
-        c.w[1] = v[1];
+    CoefGroups<K> c;
+    const v4u_t v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, BUF_NT);
+    c.w[0] = v[0];
+    c.w[1] = v[1];
+    c.w[2] = v[2];
+    c.w[3] = v[3];
+    if constexpr (coefs_per_lane<K>() == 4) {
+        const v4u_t u = __builtin_amdgcn_raw_buffer_load_b128(r, off + 16, 0, BUF_NT);
+        c.w[4] = u[0];
+        c.w[5] = u[1];
+        c.w[6] = u[2];
+        c.w[7] = u[3];
+    } else {
+        const v2u_t u = __builtin_amdgcn_raw_buffer_load_b64(r, off + 16, 0, BUF_NT);
+        c.w[4] = u[0];
+        c.w[5] = u[1];
     }
     return c;
 }
 
+// group g's coefficients as apply_coefs takes them
 template <int K>
-__device__ __forceinline__ float coef(const CoefRow<K> &c, int g, int i)
+__device__ __forceinline__ uint2 coef_group(const CoefGroups<K> &c, int g)
 {
-    const int e = g * K + i;
-    return half_bits_to_float(e & 1 ? c.w[e >> 1] >> 16 : c.w[e >> 1] & 0xffffu);
+    if constexpr (coefs_per_lane<K>() == 4) {
+        return make_uint2(c.w[2 * g], c.w[2 * g + 1]);
+    } else {
+        auto h = [&](int e) { return e & 1 ? c.w[e >> 1] >> 16 : c.w[e >> 1] & 0xffffu; };
+        return make_uint2(h(3 * g) | (h(3 * g + 1) << 16), h(3 * g + 2));
+    }
 }
 
 template <int K, int NB, int D, bool MULTI>
@@ -99,20 +98,22 @@ __global__ void __launch_bounds__(512) gemm_sbs_kernel(GemvArgs a)
     const int nw = blockDim.x >> 6;
     const int B = a.B;  // vectors actually present (<= NB)
     unsigned char *stage = smem + wv * STAGE;
-    float *red = (float *)(smem + nw * STAGE);  // [tpw][nw][NS][4 rows][4 vectors]
+    constexpr int TR = tile_rows(K), NP = partials_per_lane<K>();
+    float *red = (float *)(smem + nw * STAGE);  // [tpw][nw][NS][TR rows][4 vectors]
 
     const int tile0 = blockIdx.x * a.tpw;
     const int ntl = min(a.tpw, a.n_tiles - tile0);
     const int n_items = MULTI ? ((a.n_gblocks - wv + nw - 1) / nw) * ntl : ntl;
 
     // A: lane (row m = lane%16 = (tile row, plane), k-block lane/16) loads the
-    // 16 bytes of group lane/16; lanes of planes >= K read zero.
-    const int a_r = (lane & 15) >> 2, a_i = lane & 3, a_b = lane >> 4;
-    const unsigned p_lane = a_i < K ? (unsigned)((a_b * TILE_ROWS + a_r) * K + a_i) * 16u : LANE_OOB;
-    // coefficients: the lane's D rows are tile row lane/16, planes 0..3
-    const unsigned c_lane = (unsigned)((lane >> 4) * GB * K) * 2u;
-    constexpr unsigned PBLK_B = GB * TILE_ROWS * K * 16;
-    constexpr unsigned CBLK_B = TILE_ROWS * GB * K * 2;
+    // 16 bytes of group lane/16; lanes of empty plane slots (K = 3) read zero.
+    bool a_ok;
+    const unsigned a_slot = a_slot_bytes<K>(lane, a_ok);
+    const unsigned p_lane = a_ok ? a_slot : LANE_OOB;
+    // coefficients of the lane's D rows for the four group slots
+    const unsigned c_lane = (unsigned)((lane >> 4) * GB * coefs_per_lane<K>()) * 2u;
+    constexpr unsigned PBLK_B = GB * TR * K * 16;
+    constexpr unsigned CBLK_B = GB * TR * K * 2;
     const unsigned pstep = (unsigned)a.n_gblocks * PBLK_B;
     const unsigned cstep = (unsigned)a.n_gblocks * CBLK_B;
     const size_t blk0 = (size_t)tile0 * a.n_gblocks;
@@ -121,7 +122,7 @@ __global__ void __launch_bounds__(512) gemm_sbs_kernel(GemvArgs a)
 
     int pf_i = 0, pf_gb = wv;
     uint4 P[D];
-    CoefRow<K> C[D];
+    CoefGroups<K> C[D];
     auto issue = [&](int j) {
         unsigned po, co;
         if constexpr (MULTI) {
@@ -140,7 +141,7 @@ __global__ void __launch_bounds__(512) gemm_sbs_kernel(GemvArgs a)
             ++pf_i;
         }
         P[j] = buf_load16(prs, p_lane + po);
-        C[j] = buf_coef_row<K>(crs, c_lane + co);
+        C[j] = buf_coef_groups<K>(crs, c_lane + co);
     };
     // The lane's eight activations of gblock gb for every vector present;
     // lanes past I (ragged end) and vectors >= B read zero.
@@ -211,9 +212,9 @@ __global__ void __launch_bounds__(512) gemm_sbs_kernel(GemvArgs a)
         load_x(Xn, wv + nw);
     __builtin_amdgcn_sched_barrier(0);
 
-    // red offset of this lane's (row, vector) partial; written by limb-0 lanes
-    float *red_w = red + (wv * NS * TILE_ROWS + (lane >> 4)) * SBS_VPS + vb;
-    const int red_tile = nw * NS * TILE_ROWS * SBS_VPS;
+    // red offset of this lane's (row, vector) partials; written by limb-0 lanes
+    float *red_w = red + (wv * NS * TR + (lane >> 4) * NP) * SBS_VPS + vb;
+    const int red_tile = nw * NS * TR * SBS_VPS;
     int cur_i = 0, cur_gb = wv;
     for (int m0 = 0; m0 < n_items; m0 += D) {
 #pragma unroll
@@ -239,28 +240,38 @@ __global__ void __launch_bounds__(512) gemm_sbs_kernel(GemvArgs a)
                 for (int st = 0; st < NS; ++st)
                     d[g][st] = mfma_fp4_fp8(A, Bop[st][g], v4f{0.f, 0.f, 0.f, 0.f});
             }
-            const CoefRow<K> cr = C[j];
+            const CoefGroups<K> cr = C[j];
             issue(j);
 #pragma unroll
             for (int st = 0; st < NS; ++st) {
-                float part[GB];
+                float acc[NP];
+#pragma unroll
+                for (int p = 0; p < NP; ++p)
+                    acc[p] = 0.f;
 #pragma unroll
                 for (int g = 0; g < GB; ++g) {
-                    float t = coef<K>(cr, g, 0) * d[g][st][0];
+                    float part[NP];
+                    apply_coefs<K>(coef_group<K>(cr, g), d[g][st], part);
 #pragma unroll
-                    for (int i = 1; i < K; ++i)
-                        t = fmaf(coef<K>(cr, g, i), d[g][st][i], t);
-                    part[g] = t;
+                    for (int p = 0; p < NP; ++p)
+                        acc[p] += part[p];
                 }
-                float v = ((part[0] + part[1]) + (part[2] + part[3])) * oscale[st];
-                v += dpp_f32<DPP_QUAD_XOR1>(v);
-                v += dpp_f32<DPP_QUAD_XOR2>(v);
+#pragma unroll
+                for (int p = 0; p < NP; ++p) {
+                    float v = acc[p] * oscale[st];
+                    v += dpp_f32<DPP_QUAD_XOR1>(v);
+                    v += dpp_f32<DPP_QUAD_XOR2>(v);
+                    acc[p] = v;
+                }
                 if (valid && limb == 0) {
-                    float *r = red_w + cur_i * red_tile + st * TILE_ROWS * SBS_VPS;
-                    if (!MULTI || cur_gb == wv)
-                        *r = v;
-                    else
-                        *r += v;
+                    float *r = red_w + cur_i * red_tile + st * TR * SBS_VPS;
+#pragma unroll
+                    for (int p = 0; p < NP; ++p) {
+                        if (!MULTI || cur_gb == wv)
+                            r[p * SBS_VPS] = acc[p];
+                        else
+                            r[p * SBS_VPS] += acc[p];
+                    }
                 }
             }
             if (valid) {
@@ -273,17 +284,17 @@ __global__ void __launch_bounds__(512) gemm_sbs_kernel(GemvArgs a)
     }
 
     __syncthreads();
-    const int row_base = tile0 * TILE_ROWS;
-    const int rows = ntl * TILE_ROWS;
+    const int row_base = tile0 * TR;
+    const int rows = ntl * TR;
     for (int idx = threadIdx.x; idx < rows * B; idx += blockDim.x) {
         const int b = idx / rows, lr = idx % rows;
         const int o = row_base + lr;
         if (o < a.O) {
             const int st = b / SBS_VPS, v = b % SBS_VPS;
-            const float *r = red + (lr / TILE_ROWS) * red_tile + (st * TILE_ROWS + lr % TILE_ROWS) * SBS_VPS + v;
+            const float *r = red + (lr / TR) * red_tile + (st * TR + lr % TR) * SBS_VPS + v;
             float s = 0.f;
             for (int w = 0; w < nw; ++w)
-                s += r[w * NS * TILE_ROWS * SBS_VPS];
+                s += r[w * NS * TR * SBS_VPS];
             a.y[(size_t)b * a.O + o] = __half_as_ushort(__float2half_rn(s));
         }
     }
@@ -312,7 +323,7 @@ int launch_gemm_sbs(const Dims &d, const void *planes_dev, const void *coeffs_de
     const int waves = (d.n_gblocks + gpw - 1) / gpw;
     // tiles per workgroup, capped so that dynamic LDS stays within 64 KiB
     const size_t fixed = (size_t)waves * sbs_stage_bytes(nb);
-    const size_t per_tile = (size_t)waves * sbs_sets(nb) * TILE_ROWS * SBS_VPS * 4;
+    const size_t per_tile = (size_t)waves * sbs_sets(nb) * d.tr * SBS_VPS * 4;
     const int max_tpw = (int)((SBVR_MAX_DYN_LDS - fixed) / per_tile);
     const int tpw = min((d.n_tiles + SBVR_SBS_GROUPS - 1) / SBVR_SBS_GROUPS, max_tpw);
     const int grid = (d.n_tiles + tpw - 1) / tpw;

@@ -1,7 +1,8 @@
 // Batch-1 SBVR GEMV (Sec. 4.4): y[o] = sum_g sum_i c[o][g][i] * S[o][g][i].
 //
 // One-shot kernel, for matrices whose loads can all be in flight at once.
-// A workgroup owns T tiles (4T consecutive rows); its wavefront w owns gblock
+// A workgroup owns T tiles (T * TR consecutive rows, TR = 16 / row slots: 4
+// rows at k = 3, 4, 8 at k = 2, 16 at k = 1); its wavefront w owns gblock
 // w (512 inner elements; at most 16 per row: split-K inside the workgroup).
 // Partial row sums are reduced across wavefronts in LDS in a fixed order:
 // results are deterministic and there is no global workspace.  Larger
@@ -14,7 +15,8 @@
 // Four chained instructions (q = 0..3) therefore leave in D[row][4s+l] the
 // complete per-plane sum of group s for limb l, and the coefficients are
 // applied once per four instructions: D rows are (tile row, plane), so a lane
-// multiplies its four D values by the four coefficients of one (row, group).
+// multiplies its four D values by their coefficients, which belong to one
+// group and to 1, 2 or 4 tile rows (k = 3..4, 2, 1).
 //
 // Latency hiding.  Every load a wavefront needs -- its 1 KiB of activations,
 // then the T tiles' plane and coefficient blocks -- is issued before any
@@ -31,7 +33,7 @@ constexpr int B1_WAVE_LDS = 2048;  // per wavefront: [q][s][l][32 B]
 template <int K, int T>
 struct B1Regs {
     uint4 p[T];  // plane words of each tile (this lane's 16 bytes)
-    uint2 c[T];  // this lane's coefficients of each tile
+    uint2 c[T];  // the coefficients of this lane's four D rows, each tile
     uint4 x;     // this lane's 8 activations
 };
 
@@ -48,15 +50,15 @@ __global__ void __launch_bounds__(1024) gemv_b1_kernel(GemvArgs a)
     const int tile0 = blockIdx.x * T;
     const int gb = wv;
 
-    // A operand: row m = lane%16 = (tile row r, plane i), k-block = group slot.
-    // Lanes of planes >= K read a valid slot and zero it.
-    const int a_r = (lane & 15) >> 2, a_i = lane & 3, a_b = lane >> 4;
-    const bool a_ok = a_i < K;
-    const unsigned a_off = (unsigned)((a_b * TILE_ROWS + a_r) * K + (a_ok ? a_i : 0));
-    // coefficients: D rows of this lane are tile row lane/16, planes 0..3
-    const unsigned c_off = (unsigned)(((lane >> 4) * GB + ((lane & 15) >> 2)) * K);
-    constexpr int PBLK = GB * TILE_ROWS * K;  // uint4 per plane block
-    constexpr int CBLK = TILE_ROWS * GB * K;  // coefficients per block
+    constexpr int TR = tile_rows(K), NP = partials_per_lane<K>();
+    // A operand: row m = lane%16 = (tile row, plane), k-block = group slot;
+    // lanes of empty plane slots (K = 3) read a valid slot and zero it.
+    bool a_ok;
+    const unsigned a_off = a_slot_bytes<K>(lane, a_ok) / 16;
+    // coefficients of the lane's D rows (group slot (lane%16)/4)
+    const unsigned c_off = (unsigned)(((lane >> 4) * GB + ((lane & 15) >> 2)) * coefs_per_lane<K>());
+    constexpr int PBLK = GB * TR * K;  // uint4 per plane block
+    constexpr int CBLK = GB * TR * K;  // coefficients per block
     // Tiles past the end (last workgroup) re-read the last tile; their rows
     // are >= O and never stored.  Block indices are wavefront-uniform, so each
     // load is a scalar base plus the lane's 32-bit offset.
@@ -74,7 +76,7 @@ __global__ void __launch_bounds__(1024) gemv_b1_kernel(GemvArgs a)
             const size_t blk = (size_t)(tblk[t] + gb);
             const uint4 v = load_nt16(a.planes + blk * PBLK + a_off);
             R.p[t] = a_ok ? v : make_uint4(0u, 0u, 0u, 0u);
-            R.c[t] = load_coeffs<K>(a.coeffs + blk * CBLK + c_off);
+            R.c[t] = load_coefs4<K>(a.coeffs + blk * CBLK + c_off);
         }
     };
 
@@ -93,10 +95,12 @@ __global__ void __launch_bounds__(1024) gemv_b1_kernel(GemvArgs a)
     const int hi_off = (act && s >= 2) ? data_off : zero_off;
     const int inv_alpha = inv_alpha_exp(lane & 3);
 
-    float acc[T];
+    float acc[T][NP];
 #pragma unroll
     for (int t = 0; t < T; ++t)
-        acc[t] = 0.f;
+#pragma unroll
+        for (int p = 0; p < NP; ++p)
+            acc[t][p] = 0.f;
 
     // Activation limbs of the gblock in R -> LDS -> the four B operands;
     // returns 2^-sigma, the factor that undoes the activation scaling.
@@ -122,7 +126,11 @@ __global__ void __launch_bounds__(1024) gemv_b1_kernel(GemvArgs a)
             d = mfma_fp4_fp8(fp4_operand(R.p[t].y), Bq[1], d);
             d = mfma_fp4_fp8(fp4_operand(R.p[t].z), Bq[2], d);
             d = mfma_fp4_fp8(fp4_operand(R.p[t].w), Bq[3], d);
-            acc[t] = fmaf(apply_coeffs(R.c[t], d), inv_scale, acc[t]);
+            float part[NP];
+            apply_coefs<K>(R.c[t], d, part);
+#pragma unroll
+            for (int p = 0; p < NP; ++p)
+                acc[t][p] = fmaf(part[p], inv_scale, acc[t][p]);
         }
     };
 
@@ -142,16 +150,22 @@ __global__ void __launch_bounds__(1024) gemv_b1_kernel(GemvArgs a)
     // sum the 16 columns (group slot x limb) of each row ...
 #pragma unroll
     for (int t = 0; t < T; ++t)
-        acc[t] = row16_sum(acc[t]);
-    const int row_base = tile0 * TILE_ROWS;
+#pragma unroll
+        for (int p = 0; p < NP; ++p)
+            acc[t][p] = row16_sum(acc[t][p]);
+    const int row_base = tile0 * TR;
+    // lane rows: (lane / 16) * NP + p within the tile
+    const int lrow = (lane >> 4) * NP;
     if (nw == 1) {  // inner dimension not split: store directly
         if ((lane & 15) == 0) {
 #pragma unroll
-            for (int t = 0; t < T; ++t) {
-                const int o = row_base + t * TILE_ROWS + (lane >> 4);
-                if (o < a.O)
-                    a.y[o] = __half_as_ushort(__float2half_rn(acc[t]));
-            }
+            for (int t = 0; t < T; ++t)
+#pragma unroll
+                for (int p = 0; p < NP; ++p) {
+                    const int o = row_base + t * TR + lrow + p;
+                    if (o < a.O)
+                        a.y[o] = __half_as_ushort(__float2half_rn(acc[t][p]));
+                }
         }
         return;
     }
@@ -159,21 +173,23 @@ __global__ void __launch_bounds__(1024) gemv_b1_kernel(GemvArgs a)
     if ((lane & 15) == 0) {
 #pragma unroll
         for (int t = 0; t < T; ++t)
-            red[(wv * T + t) * TILE_ROWS + (lane >> 4)] = acc[t];
+#pragma unroll
+            for (int p = 0; p < NP; ++p)
+                red[(wv * T + t) * TR + lrow + p] = acc[t][p];
     }
     __syncthreads();
-    for (int idx = threadIdx.x; idx < T * TILE_ROWS; idx += blockDim.x) {
+    for (int idx = threadIdx.x; idx < T * TR; idx += blockDim.x) {
         const int o = row_base + idx;
         if (o < a.O) {
             float v = 0.f;
             for (int w = 0; w < nw; ++w)
-                v += red[w * T * TILE_ROWS + idx];
+                v += red[w * T * TR + idx];
             a.y[o] = __half_as_ushort(__float2half_rn(v));
         }
     }
 }
 
-// Launch shape.  T tiles (4T rows) per workgroup: the most (<= 8) that still
+// Launch shape.  T tiles (T * TR rows) per workgroup: the most (<= 8) that still
 // leaves >= 256 workgroups for 256 CUs; one wavefront per gblock.
 constexpr int B1_MAX_WAVES = 16;
 
@@ -216,7 +232,7 @@ int launch_gemv_b1(const Dims &d, const void *planes_dev, const void *coeffs_dev
     GemvArgs a = {(const uint4 *)planes_dev, (const uint16_t *)coeffs_dev, x, y, d.O, d.I, d.k,
                   d.n_tiles, d.n_gblocks, 1, 1, 0};
     const int grid = (d.n_tiles + T - 1) / T;
-    const size_t lds = (size_t)waves * B1_WAVE_LDS + (size_t)waves * T * TILE_ROWS * 4;
+    const size_t lds = (size_t)waves * B1_WAVE_LDS + (size_t)waves * T * d.tr * 4;
     const void *fn = d.k == 4   ? b1_kernel_for<4>(T)
                      : d.k == 3 ? b1_kernel_for<3>(T)
                      : d.k == 2 ? b1_kernel_for<2>(T)

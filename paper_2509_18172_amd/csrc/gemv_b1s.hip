@@ -1,7 +1,7 @@
 // Streaming batch-1 SBVR GEMV (Sec. 4.4) for matrices too large to hold in
 // flight at once.
 //
-// A workgroup owns tpw consecutive tiles (4 rows each) and every gblock
+// A workgroup owns tpw consecutive tiles (TR rows each) and every gblock
 // (512 inner elements) of them; its W wavefronts split the gblocks, wavefront
 // w taking w, w+W, w+2W, ...  A wavefront's work is the sequence of items
 // (gblock, tile): for each of its gblocks, the workgroup's tiles in order.
@@ -16,7 +16,7 @@
 // compiler keeps each slot in fixed registers with counted waits.
 //
 // Row sums of each (tile, gblock) item are added into an LDS array
-// [tile][wavefront][row] in gblock order; at the end the workgroup sums the
+// [tile][wavefront][TR rows] in gblock order; at the end the workgroup sums the
 // wavefronts in order, so the result is deterministic and no global
 // workspace is used.
 //
@@ -60,28 +60,27 @@ __global__ void __launch_bounds__(1024) gemv_b1s_kernel(GemvArgs a)
     const int wv = wave_id();
     const int nw = blockDim.x >> 6;
     unsigned char *lds = smem + wv * B1S_WAVE_LDS;
-    float *red = (float *)(smem + nw * B1S_WAVE_LDS);  // [tpw][nw][TILE_ROWS]
+    constexpr int TR = tile_rows(K), NP = partials_per_lane<K>();
+    float *red = (float *)(smem + nw * B1S_WAVE_LDS);  // [tpw][nw][TR]
 
     const int tile0 = blockIdx.x * a.tpw;
     const int ntl = min(a.tpw, a.n_tiles - tile0);
     // MULTI: several gblocks per wavefront; otherwise exactly one (wv)
     const int n_items = MULTI ? ((a.n_gblocks - wv + nw - 1) / nw) * ntl : ntl;
 
-    // A operand lane mapping: row m = lane%16 = (tile row r, plane i),
-    // k-block = group slot; planes >= K read a valid slot and are zeroed.
-    const int a_r = (lane & 15) >> 2, a_i = lane & 3, a_b = lane >> 4;
-    const bool a_ok = a_i < K;
-    const unsigned a_off = (unsigned)((a_b * TILE_ROWS + a_r) * K + (a_ok ? a_i : 0));
-    // coefficients of the lane's D rows: tile row lane/16, planes 0..3
-    const unsigned c_off = (unsigned)(((lane >> 4) * GB + ((lane & 15) >> 2)) * K);
-    constexpr unsigned PBLK_B = GB * TILE_ROWS * K * 16;  // bytes per plane block
-    constexpr unsigned CBLK_B = TILE_ROWS * GB * K * 2;   // bytes per coefficient block
+    // A operand lane mapping: row m = lane%16 = (tile row, plane), k-block =
+    // group slot; empty plane slots (K = 3) read a valid slot and are zeroed.
+    bool a_ok;
+    const unsigned p_lane = a_slot_bytes<K>(lane, a_ok);
+    // coefficients of the lane's D rows (group slot (lane%16)/4)
+    const unsigned c_lane = (unsigned)(((lane >> 4) * GB + ((lane & 15) >> 2)) * coefs_per_lane<K>()) * 2u;
+    constexpr unsigned PBLK_B = GB * TR * K * 16;  // bytes per plane block
+    constexpr unsigned CBLK_B = GB * TR * K * 2;   // bytes per coefficient block
     const unsigned pstep = (unsigned)a.n_gblocks * PBLK_B;  // next tile, same gblock
     const unsigned cstep = (unsigned)a.n_gblocks * CBLK_B;
     const size_t blk0 = (size_t)tile0 * a.n_gblocks;
     const buf_rsrc prs = make_rsrc((const unsigned char *)a.planes + blk0 * PBLK_B, (unsigned)ntl * pstep);
     const buf_rsrc crs = make_rsrc((const unsigned char *)a.coeffs + blk0 * CBLK_B, (unsigned)ntl * cstep);
-    const unsigned p_lane = a_off * 16, c_lane = c_off * 2;
 
     // Prefetch cursor (wavefront-uniform): next item whose loads are issued.
     int pf_i = 0, pf_gb = wv;
@@ -106,7 +105,7 @@ __global__ void __launch_bounds__(1024) gemv_b1s_kernel(GemvArgs a)
             ++pf_i;
         }
         P[j] = buf_load16(prs, p_lane + po);
-        C[j] = buf_coeffs<K>(crs, c_lane + co);
+        C[j] = buf_coefs4<K>(crs, c_lane + co);
     };
     // Activations of a gblock; lanes past I (ragged end) read a valid address
     // and are zeroed when the operand is built.
@@ -157,7 +156,7 @@ __global__ void __launch_bounds__(1024) gemv_b1s_kernel(GemvArgs a)
     build(x_cur, wv);
     __builtin_amdgcn_sched_barrier(0);
 
-    float *red_w = red + wv * TILE_ROWS + (lane >> 4);
+    float *red_w = red + wv * TR + (lane >> 4) * NP;
     int cur_i = 0, cur_gb = wv;
     for (int m0 = 0; m0 < n_items; m0 += D) {
 #pragma unroll
@@ -176,13 +175,20 @@ __global__ void __launch_bounds__(1024) gemv_b1s_kernel(GemvArgs a)
                 d = mfma_fp4_fp8(fp4_operand(pw.y), Bq[1], d);
                 d = mfma_fp4_fp8(fp4_operand(pw.z), Bq[2], d);
                 d = mfma_fp4_fp8(fp4_operand(pw.w), Bq[3], d);
-                const float v = row16_sum(apply_coeffs(C[j], d) * inv_scale);
+                float part[NP];
+                apply_coefs<K>(C[j], d, part);
+#pragma unroll
+                for (int p = 0; p < NP; ++p)
+                    part[p] = row16_sum(part[p] * inv_scale);
                 if ((lane & 15) == 0) {
-                    float *r = red_w + cur_i * nw * TILE_ROWS;
-                    if (!MULTI || cur_gb == wv)
-                        *r = v;
-                    else
-                        *r += v;
+                    float *r = red_w + cur_i * nw * TR;
+#pragma unroll
+                    for (int p = 0; p < NP; ++p) {
+                        if (!MULTI || cur_gb == wv)
+                            r[p] = part[p];
+                        else
+                            r[p] += part[p];
+                    }
                 }
                 if (++cur_i == ntl && MULTI) {
                     cur_i = 0;
@@ -194,14 +200,14 @@ __global__ void __launch_bounds__(1024) gemv_b1s_kernel(GemvArgs a)
     }
 
     __syncthreads();
-    const int row_base = tile0 * TILE_ROWS;
-    for (int idx = threadIdx.x; idx < ntl * TILE_ROWS; idx += blockDim.x) {
+    const int row_base = tile0 * TR;
+    for (int idx = threadIdx.x; idx < ntl * TR; idx += blockDim.x) {
         const int o = row_base + idx;
         if (o < a.O) {
-            const float *r = red + (idx / TILE_ROWS) * nw * TILE_ROWS + (idx % TILE_ROWS);
+            const float *r = red + (idx / TR) * nw * TR + (idx % TR);
             float v = 0.f;
             for (int w = 0; w < nw; ++w)
-                v += r[w * TILE_ROWS];
+                v += r[w * TR];
             a.y[o] = __half_as_ushort(__float2half_rn(v));
         }
     }
@@ -224,7 +230,7 @@ int launch_gemv_b1s(const Dims &d, const void *planes_dev, const void *coeffs_de
     const int grid = (d.n_tiles + tpw - 1) / tpw;
     GemvArgs a = {(const uint4 *)planes_dev, (const uint16_t *)coeffs_dev, x, y, d.O, d.I, d.k,
                   d.n_tiles, d.n_gblocks, gpw, 1, tpw};
-    const size_t lds = (size_t)waves * B1S_WAVE_LDS + (size_t)tpw * waves * TILE_ROWS * 4;
+    const size_t lds = (size_t)waves * B1S_WAVE_LDS + (size_t)tpw * waves * d.tr * 4;
     const bool multi = gpw > 1;
     const void *fn = d.k == 4   ? b1s_kernel_for<4>(multi)
                      : d.k == 3 ? b1s_kernel_for<3>(multi)

@@ -4,16 +4,29 @@
 // 128 plane bits in four 32-bit words plus one binary16 coefficient
 // (Sec. 4.1, Sec. 4.4).  The device format regroups those words so that a
 // wavefront's 128-bit loads are contiguous and so that each loaded word can be
-// turned into matrix-core operands with a handful of bit masks:
+// turned into matrix-core operands with a handful of bit masks.
 //
-//   tile      TILE_ROWS = 4 consecutive rows
+// A matrix-core instruction has 16 A rows; they hold (tile row r, plane i)
+// pairs, m = r * RS + i, with RS = 16 / TR "row slots" per tile row:
+//
+//   k     tile rows TR   row slots RS   rows used
+//   1          16             1            16
+//   2           8             2            16
+//   3           4             4            12 (plane slot 3 stays empty)
+//   4           4             4            16
+//
 //   gblock    GB = 4 consecutive groups (512 inner-dimension elements)
 //   block     one (tile, gblock) pair; blocks are stored tile-major:
 //             block index = tile * n_gblocks + gblock
 //
-//   plane block (256 * k bytes): slot s = (b * TILE_ROWS + r) * k + i holds the
-//     four words (16 bytes) of plane i of row 4*tile + r for group 4*gblock + b.
-//   coeff block (32 * k bytes):  entry (r * GB + b) * k + i holds c[o][g][i].
+//   plane block (GB * TR * k * 16 bytes): slot (b * TR + r) * k + i holds the
+//     four words (16 bytes) of plane i of row TR*tile + r for group
+//     4*gblock + b -- 1 KiB for k = 1, 2, 4.
+//   coeff block (GB * TR * k * 2 bytes): the coefficient of A row m = 4q + j
+//     (= tile row r, plane i) of group slot b is entry (q * GB + b) * CPL + j,
+//     CPL = 4 (3 for k = 3, whose rows m = 4r + i have i < 3).  A lane of a
+//     16x16 result holds rows 4q .. 4q+3: their coefficients are contiguous
+//     for one group slot (CPL entries) and for all four (4 * CPL entries).
 //
 // Within each device word the bits are transposed as a 4 x 8 bit matrix:
 // element e = 8 v + p (0 <= v < 4, 0 <= p < 8) of the word sits at bit 4 p + v.
@@ -32,12 +45,15 @@
 namespace sbvr {
 
 constexpr int GROUP = 128;     // weights per SBVR group (Sec. 4.1)
-constexpr int TILE_ROWS = 4;   // rows per tile
 constexpr int GB = 4;          // groups per gblock
 constexpr int MAX_K = 4;       // planes supported by this build
 
+// rows per tile and A-row slots per tile row for k planes
+SBVR_HD constexpr int tile_rows(int k) { return k == 1 ? 16 : (k == 2 ? 8 : 4); }
+SBVR_HD constexpr int row_slots(int k) { return 16 / tile_rows(k); }
+
 struct Dims {
-    int O, I, k, G, n_tiles, n_gblocks;
+    int O, I, k, G, tr, n_tiles, n_gblocks;
 };
 
 SBVR_HD Dims make_dims(int O, int I, int k)
@@ -47,13 +63,23 @@ SBVR_HD Dims make_dims(int O, int I, int k)
     d.I = I;
     d.k = k;
     d.G = I / GROUP;
-    d.n_tiles = (O + TILE_ROWS - 1) / TILE_ROWS;
+    d.tr = tile_rows(k);
+    d.n_tiles = (O + d.tr - 1) / d.tr;
     d.n_gblocks = (d.G + GB - 1) / GB;
     return d;
 }
 
-SBVR_HD size_t plane_block_words(int k) { return (size_t)GB * TILE_ROWS * k * 4; }
-SBVR_HD size_t coeff_block_entries(int k) { return (size_t)TILE_ROWS * GB * k; }
+SBVR_HD constexpr int coefs_per_quad(int k) { return k == 3 ? 3 : 4; }
+
+// coefficient entry of (tile row r, group slot b, plane i) within a block
+SBVR_HD int coeff_entry(int k, int r, int b, int i)
+{
+    const int m = r * row_slots(k) + i;
+    return ((m / 4) * GB + b) * coefs_per_quad(k) + m % 4;
+}
+
+SBVR_HD size_t plane_block_words(int k) { return (size_t)GB * tile_rows(k) * k * 4; }
+SBVR_HD size_t coeff_block_entries(int k) { return (size_t)GB * tile_rows(k) * k; }
 
 SBVR_HD size_t plane_bytes(const Dims &d)
 {

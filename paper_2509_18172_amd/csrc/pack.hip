@@ -17,8 +17,8 @@ __global__ void pack_planes_kernel(Dims d, const uint32_t *__restrict__ canon,
     const int within = (int)(idx % bw);
     const int slot = within / 4, w = within % 4;
     const int i = slot % d.k, br = slot / d.k;
-    const int r = br % TILE_ROWS, b = br / TILE_ROWS;
-    const int o = (int)(blk / d.n_gblocks) * TILE_ROWS + r;
+    const int r = br % d.tr, b = br / d.tr;
+    const int o = (int)(blk / d.n_gblocks) * d.tr + r;
     const int g = (int)(blk % d.n_gblocks) * GB + b;
     uint32_t v = 0;
     if (o < d.O && g < d.G)
@@ -37,8 +37,8 @@ __global__ void unpack_planes_kernel(Dims d, const uint32_t *__restrict__ dev,
     const int i = (int)(rest % d.k);
     const size_t og = rest / d.k;
     const int g = (int)(og % d.G), o = (int)(og / d.G);
-    const size_t blk = (size_t)(o / TILE_ROWS) * d.n_gblocks + g / GB;
-    const int slot = ((g % GB) * TILE_ROWS + o % TILE_ROWS) * d.k + i;
+    const size_t blk = (size_t)(o / d.tr) * d.n_gblocks + g / GB;
+    const int slot = ((g % GB) * d.tr + o % d.tr) * d.k + i;
     canon[idx] = to_canonical_word(dev[blk * plane_block_words(d.k) + slot * 4 + w]);
 }
 
@@ -51,9 +51,12 @@ __global__ void pack_coeffs_kernel(Dims d, const uint16_t *__restrict__ canon,
     const size_t be = coeff_block_entries(d.k);
     const size_t blk = idx / be;
     const int within = (int)(idx % be);
-    const int i = within % d.k, rb = within / d.k;
-    const int b = rb % GB, r = rb / GB;
-    const int o = (int)(blk / d.n_gblocks) * TILE_ROWS + r;
+    // entry (q * GB + b) * CPL + j holds A row m = 4q + j = (r, i) of slot b
+    const int cpl = coefs_per_quad(d.k), rs = row_slots(d.k);
+    const int j = within % cpl, b = (within / cpl) % GB, q = within / (cpl * GB);
+    const int m = 4 * q + j;
+    const int r = m / rs, i = m % rs;
+    const int o = (int)(blk / d.n_gblocks) * d.tr + r;
     const int g = (int)(blk % d.n_gblocks) * GB + b;
     uint16_t v = 0;
     if (o < d.O && g < d.G)
@@ -70,8 +73,8 @@ __global__ void unpack_coeffs_kernel(Dims d, const uint16_t *__restrict__ dev,
     const int i = (int)(idx % d.k);
     const size_t og = idx / d.k;
     const int g = (int)(og % d.G), o = (int)(og / d.G);
-    const size_t blk = (size_t)(o / TILE_ROWS) * d.n_gblocks + g / GB;
-    canon[idx] = dev[blk * coeff_block_entries(d.k) + ((o % TILE_ROWS) * GB + g % GB) * d.k + i];
+    const size_t blk = (size_t)(o / d.tr) * d.n_gblocks + g / GB;
+    canon[idx] = dev[blk * coeff_block_entries(d.k) + coeff_entry(d.k, o % d.tr, g % GB, i)];
 }
 
 static unsigned grid_for(size_t total) { return (unsigned)((total + 255) / 256); }

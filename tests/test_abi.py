@@ -39,9 +39,10 @@ def test_status_strings_and_version():
 @pytest.mark.parametrize("O,I,k", [(4096, 4096, 4), (1, 128, 1), (1001, 640, 3), (14336, 4096, 2)])
 def test_size_queries(O, I, k):
     G = I // 128
-    tiles, gblocks = -(-O // 4), -(-G // 4)
-    assert sb.sbvr_packed_plane_bytes(O, I, k) == tiles * gblocks * 4 * 4 * k * 16
-    assert sb.sbvr_packed_coeff_bytes(O, I, k) == tiles * gblocks * 4 * 4 * k * 2
+    tr = {1: 16, 2: 8, 3: 4, 4: 4}[k]  # rows per tile: 16 matrix-core rows of (row, plane)
+    tiles, gblocks = -(-O // tr), -(-G // 4)
+    assert sb.sbvr_packed_plane_bytes(O, I, k) == tiles * gblocks * 4 * tr * k * 16
+    assert sb.sbvr_packed_coeff_bytes(O, I, k) == tiles * gblocks * 4 * tr * k * 2
     # never smaller than the canonical tensors
     assert sb.sbvr_packed_plane_bytes(O, I, k) >= O * G * k * 16
     assert sb.sbvr_packed_coeff_bytes(O, I, k) >= O * G * k * 2
