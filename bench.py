@@ -28,6 +28,9 @@ One JSON line is printed:
   small_batch   per projection at B = 2, 4, 8 activation vectors
                 (sbvr_gemm_small_batch), same timing
   low_bit       per projection at k = 2 and 3 planes, same timing
+  prefill       per projection: sbvr_decompress to binary16 (us, GB/s of the
+                SBVR bytes read plus the 2 bytes per weight written) and, for
+                context, a 512-token library GEMM (torch.matmul) on the result
   llama3_70b    per projection of the Llama-3-70B shapes, same timing
   cpu_baseline  the CPU oracle (binary64 decompress + GEMV) on layer 0's seven
                 GEMVs, bounded to ~10 s of work, in the same unit
@@ -43,7 +46,6 @@ from __future__ import annotations
 
 import argparse
 import csv
-import glob
 import hashlib
 import json
 import os
@@ -80,14 +82,18 @@ def parse():
     return ap.parse_args()
 
 
+# The sources the batch-1 kernels (code and launch shapes) are compiled from.
+B1_KERNEL_SOURCES = ("device_ops.h", "gemv_b1.hip", "gemv_b1s.hip", "layout.h")
+
+
 def kernel_source_digest() -> str:
-    """sha256 over the HIP sources of the library: identifies the kernels a
+    """sha256 over the sources of the batch-1 kernels: identifies the kernels a
     counter record was taken on."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2509_18172_amd", "csrc")
-    for f in sorted(glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.h"))):
-        h.update(os.path.basename(f).encode())
-        with open(f, "rb") as fh:
+    for name in B1_KERNEL_SOURCES:
+        h.update(name.encode())
+        with open(os.path.join(csrc, name), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
 
@@ -358,6 +364,33 @@ def main():
                 res[name] = {"us": round(us, 3), "gbps": round(bb / (us * 1e3), 1)}
             small_batch[str(B)] = res
 
+    # ---- prefill path: decompression to binary16 (HBM-bound: reads the SBVR
+    # bytes, writes 2 bytes per weight), then a library GEMM over T tokens ----
+    prefill = {}
+    if not args.quick:
+        T = 512
+        for name in PROJ_ORDER:
+            O, I = shapes[name]
+            if any(shapes[m] == (O, I) for m in prefill):
+                prefill[name] = prefill[next(m for m in prefill if shapes[m] == (O, I))]
+                continue
+            ws = weights[name][:32]
+            n_out = max(2, int(np.ceil(ROTATE_BYTES / (2 * O * I))))
+            outs = [torch.empty((O, I), dtype=torch.float16, device=dev) for _ in range(n_out)]
+            dec = (lambda W, M, stream: sb.decompress(W, out=M, stream=stream))
+            us = launch_us([(dec, (w, outs[i % n_out])) for i, w in enumerate(ws)], n_launch=32)
+            bb = sb.algorithmic_bytes(O, I, k, 0) + 2 * O * I
+            Xt = torch.from_numpy(synth.activations(I, seed=31, batch=T)).to(dev).t().contiguous()
+            M = outs[0]
+            with torch.cuda.stream(stream):
+                for _ in range(3):
+                    torch.matmul(M, Xt)
+            gemm = [timed(lambda: torch.matmul(M, Xt)) * 1e3 for _ in range(5)]
+            prefill[name] = {"decompress_us": round(us, 3), "decompress_gbps": round(bb / (us * 1e3), 1),
+                             "decompress_bytes": bb, "gemm_us_512_tokens": round(float(np.median(gemm)), 2)}
+            del outs
+            torch.cuda.empty_cache()
+
     # ---- fewer planes (k = 2, 3) and the other model's shapes ----
     def shape_table(shp, kk, seed_cfg):
         res = {}
@@ -434,6 +467,7 @@ def main():
         "decode_step": decode_step,
         "small_batch": small_batch or None,
         "low_bit": low_bit or None,
+        "prefill": prefill or None,
         ("llama3_70b" if args.model == "llama3-8b" else "llama3_8b"): other_model,
         "cpu_baseline": cpu,
     }

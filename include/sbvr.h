@@ -70,7 +70,7 @@ enum sbvr_status {
 /* Human-readable name of a status code; never NULL, static storage. */
 const char *sbvr_status_string(int status);
 
-/* Library ABI version (major * 100 + minor). */
+/* Library ABI version (major * 100 + minor); 1.01 adds sbvr_decompress. */
 int sbvr_version(void);
 
 /*
@@ -129,6 +129,18 @@ int sbvr_gemv(int O, int I, int k, const void *planes_dev, const void *coeffs_de
 int sbvr_gemm_small_batch(int O, int I, int k, const void *planes_dev, const void *coeffs_dev,
                           const uint16_t *X, uint16_t *Y, int B, void *workspace,
                           size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Decompression for the prefill path: the decoded matrix as binary16,
+ *     W[o][128 g + j] = fp16_rne( sum_i c[o][g][i] * b[o][g][i][j] )
+ * (the subset-sum decoding of Sec. 4.1, computed exactly and rounded once),
+ * for a dense matrix-core GEMM over many tokens.
+ *   planes_dev, coeffs_dev  device-format weights from sbvr_pack.
+ *   W  binary16 [O][I] row-major (output, every element written), 16-byte
+ *      aligned; must not overlap the inputs.
+ */
+int sbvr_decompress(int O, int I, int k, const void *planes_dev, const void *coeffs_dev, uint16_t *W,
+                    hipStream_t stream);
 
 #ifdef __cplusplus
 }

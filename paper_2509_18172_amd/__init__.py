@@ -29,6 +29,7 @@ SBVR_E_HIP = -5
 EXPORTED = (
     "sbvr_status_string", "sbvr_version", "sbvr_packed_plane_bytes", "sbvr_packed_coeff_bytes",
     "sbvr_workspace_bytes", "sbvr_pack", "sbvr_unpack", "sbvr_gemv", "sbvr_gemm_small_batch",
+    "sbvr_decompress",
 )
 
 
@@ -63,6 +64,7 @@ def _load():
         "sbvr_unpack": (i32, [i32, i32, i32, vp, vp, vp, vp, vp]),
         "sbvr_gemv": (i32, [i32, i32, i32, vp, vp, vp, vp, vp, sz, vp]),
         "sbvr_gemm_small_batch": (i32, [i32, i32, i32, vp, vp, vp, vp, i32, vp, sz, vp]),
+        "sbvr_decompress": (i32, [i32, i32, i32, vp, vp, vp, vp]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -114,6 +116,10 @@ def sbvr_gemm_small_batch(O, I, k, planes_dev, coeffs_dev, X, Y, B, workspace=No
                           stream=0) -> int:
     return _lib.sbvr_gemm_small_batch(O, I, k, planes_dev, coeffs_dev, X, Y, B, workspace, ws_bytes,
                                       stream)
+
+
+def sbvr_decompress(O, I, k, planes_dev, coeffs_dev, W, stream=0) -> int:
+    return _lib.sbvr_decompress(O, I, k, planes_dev, coeffs_dev, W, stream)
 
 
 # --------------------------------------------------------------------------
@@ -203,6 +209,16 @@ def gemm_small_batch(W: PackedWeight, X, out=None, stream=None):
                                  X.data_ptr(), Y.data_ptr(), B, None, 0, _stream(stream)),
            "sbvr_gemm_small_batch")
     return Y
+
+
+def decompress(W: PackedWeight, out=None, stream=None):
+    """The decoded matrix as fp16 [O][I] (prefill path)."""
+    torch = _torch()
+    M = torch.empty((W.O, W.I), dtype=torch.float16, device=W.planes.device) if out is None else out
+    assert M.dtype == torch.float16 and M.is_contiguous() and tuple(M.shape) == (W.O, W.I)
+    _check(sbvr_decompress(W.O, W.I, W.k, W.planes.data_ptr(), W.coeffs.data_ptr(), M.data_ptr(),
+                           _stream(stream)), "sbvr_decompress")
+    return M
 
 
 def algorithmic_bytes(O: int, I: int, k: int, B: int = 1) -> int:

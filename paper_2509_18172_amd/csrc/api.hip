@@ -72,7 +72,7 @@ const char *sbvr_status_string(int status)
     }
 }
 
-int sbvr_version(void) { return 100; }
+int sbvr_version(void) { return 101; }
 
 size_t sbvr_packed_plane_bytes(int O, int I, int k)
 {
@@ -133,6 +133,19 @@ int sbvr_gemm_small_batch(int O, int I, int k, const void *planes_dev, const voi
     if (B == 1)
         return launch_gemv_b1(d, planes_dev, coeffs_dev, X, Y, stream);
     return launch_gemm_sbs(d, planes_dev, coeffs_dev, X, Y, B, stream);
+}
+
+int sbvr_decompress(int O, int I, int k, const void *planes_dev, const void *coeffs_dev, uint16_t *W,
+                    hipStream_t stream)
+{
+    int st = check_shape(O, I, k);
+    if (st != SBVR_OK)
+        return st;
+    if (!planes_dev || !coeffs_dev || !W)
+        return SBVR_E_INVALID_ARG;
+    if (!aligned(planes_dev, 16) || !aligned(coeffs_dev, 16) || !aligned(W, 16))
+        return SBVR_E_ALIGNMENT;
+    return launch_decompress(make_dims(O, I, k), planes_dev, coeffs_dev, W, stream);
 }
 
 }  // extern "C"

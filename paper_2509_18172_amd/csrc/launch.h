@@ -28,6 +28,8 @@ int launch_gemv_b1(const Dims &d, const void *planes_dev, const void *coeffs_dev
                    const uint16_t *x, uint16_t *y, hipStream_t stream);
 int launch_gemv_b1s(const Dims &d, const void *planes_dev, const void *coeffs_dev,
                     const uint16_t *x, uint16_t *y, hipStream_t stream);
+int launch_decompress(const Dims &d, const void *planes_dev, const void *coeffs_dev, uint16_t *W,
+                      hipStream_t stream);
 int launch_gemm_sbs(const Dims &d, const void *planes_dev, const void *coeffs_dev,
                     const uint16_t *X, uint16_t *Y, int B, hipStream_t stream);
 

@@ -388,3 +388,79 @@ def test_graph_capture_replays_match_eager(sb):
         assert torch.equal(y, y_eager), rep
         assert torch.equal(Y, Y_eager), rep
         _ = (x.float() * 2).sum().item()  # eager work between replays
+
+
+# --------------------------------------------------------------------------
+# Prefill path: decompression to binary16 (bit-exact) and a library GEMM
+# --------------------------------------------------------------------------
+
+def oracle_fp16(planes, coeffs):
+    """binary16 bits of the exact decoded weights (numpy rounds binary64 to
+    binary16 to nearest, ties to even; overflow gives infinity)."""
+    with np.errstate(over="ignore"):
+        return oracle.decompress(planes, coeffs).astype(np.float16).view(np.uint16)
+
+
+def run_decompress(sb, planes, coeffs):
+    M = sb.decompress(packed(sb, planes, coeffs))
+    torch.cuda.synchronize()
+    return M.cpu().numpy().view(np.uint16)
+
+
+@pytest.mark.parametrize("O,I,k", [(1, 128, 4), (3, 128, 1), (1001, 640, 3), (7, 896, 4), (4097, 1152, 2),
+                                   (130, 4224, 4), (16, 512, 1), (4096, 4096, 4), (1024, 14336, 2)])
+def test_decompress_bit_exact(sb, O, I, k):
+    planes, coeffs = synth.random_sbvr(O, I, k, seed=O * 7 + I + k)
+    got = run_decompress(sb, planes, coeffs)
+    want = oracle_fp16(planes, coeffs)
+    assert got.shape == (O, I)
+    assert np.array_equal(got, want), int((got != want).sum())
+
+
+def test_decompress_rounding_edges(sb):
+    """Coefficient sets whose subset sums are ties, subnormals, exact
+    cancellations and overflows of binary16."""
+    h = lambda v: np.float16(v).view(np.uint16)  # noqa: E731
+    quads = [
+        (1.0, 2.0 ** -11, 0.0, 0.0),              # 1 + half ulp: tie -> 1.0
+        (1.0 + 2.0 ** -10, 2.0 ** -11, 0.0, 0.0),  # tie -> even neighbour above
+        (2048.0, 1.0, 0.0, 0.0),                  # 2049: tie -> 2048
+        (2050.0, 1.0, 0.0, 0.0),                  # 2051: tie -> 2052
+        (2.0 ** -14, -(2.0 ** -24), 0.0, 0.0),     # largest subnormal
+        (3 * 2.0 ** -24, 2.0 ** -24, -(2.0 ** -24), 0.0),  # subnormal sums
+        (65504.0, 65504.0, 0.0, 0.0),             # overflow -> inf
+        (65504.0, 16.0, 0.0, 0.0),                # 65520: tie at the top -> inf
+        (65504.0, 8.0, -65504.0, 0.0),            # 65512 -> 65504; exact cancellations
+        (-1.0, -(2.0 ** -11), 1.0, 2.0 ** -24),   # negative tie, mixed signs
+        (0.1, 0.2, 0.3, -0.6),                    # inexact decimals
+        (-0.0, 0.0, -0.0, 1e-4),
+    ]
+    O, I, k = len(quads) * 3, 512, 4
+    coeffs = np.zeros((O, I // 128, k), dtype=np.uint16)
+    for r in range(O):
+        coeffs[r, :, :] = [h(v) for v in quads[r % len(quads)]]
+    rng = np.random.default_rng(1)
+    planes = rng.integers(0, 2 ** 32, size=(O, I // 128, k, 4), dtype=np.uint64).astype(np.uint32)
+    planes[: len(quads)] = 0xFFFFFFFF  # every subset sum present: all bits set, then random
+    planes[len(quads): 2 * len(quads), :, :, 0] = 0xFFFFFFFF
+    got = run_decompress(sb, planes, coeffs)
+    want = oracle_fp16(planes, coeffs)
+    assert np.array_equal(got, want), np.argwhere(got != want)[:5]
+
+
+def test_prefill_gemm_with_library_matmul(sb):
+    """Prefill: Y^T = W x^T over T tokens with the decompressed W and a
+    library GEMM (fp32 accumulation), against the oracle per token."""
+    O, I, T = 1024, 4096, 64
+    W = synth.weights(O, I, 0.02, seed=synth.seed_for(2, 0, 1), outlier_frac=0.001)
+    planes, coeffs = oracle.encode_matrix(W, 4)
+    X = synth.activations(I, seed=99, batch=T)
+    M = sb.decompress(packed(sb, planes, coeffs))
+    Xt = dev(X).t().contiguous()                      # [I][T]
+    Yt = torch.matmul(M, Xt)                          # [O][T], fp16 in, fp32 accumulate
+    torch.cuda.synchronize()
+    Y = Yt.t().cpu().numpy().astype(np.float64)
+    Y_ref = oracle.sbvr_gemv(planes, coeffs, X)
+    errs = [rel_err(Y[t], Y_ref[t]) for t in range(T)]
+    log(f"prefill {O}x{I} T={T} worst err={max(errs):.3e}")
+    assert max(errs) <= TOL
