@@ -93,6 +93,11 @@ def _lib():
             "oracle_gemv_dense": (None, [C.c_int, C.c_int, dp, dp, dp]),
             "oracle_sbvr_gemv": (C.c_int, [C.c_int, C.c_int, C.c_int, u32p, u16p, u16p, C.c_int,
                                            ip, C.c_int, C.c_int, dp]),
+            "oracle_sbvr_gemv_f64": (C.c_int, [C.c_int, C.c_int, C.c_int, u32p, u16p, dp, C.c_int,
+                                               ip, C.c_int, C.c_int, dp]),
+            "oracle_act_quantize": (C.c_int, [C.c_int, C.c_int, u16p, P(C.c_int32), fp]),
+            "oracle_act_planes": (None, [C.c_int, C.c_int, P(C.c_int32), u8p]),
+            "oracle_act_decode": (None, [C.c_int, C.c_int, u8p, fp, dp]),
             "oracle_rtn_sym_mse": (C.c_double, [dp, C.c_int, C.c_int]),
             "oracle_rtn_asym_mse": (C.c_double, [dp, C.c_int, C.c_int]),
         }
@@ -272,6 +277,68 @@ def sbvr_gemv(planes: np.ndarray, coeffs: np.ndarray, x_fp16: np.ndarray, rows=N
         raise ValueError("oracle_sbvr_gemv rejected its arguments")
     y = y[0] if squeeze else y
     return (y, nt) if return_threads else y
+
+
+# --------------------------------------------------------------------------
+# Online activation conversion (Sec. 4.3, Eq. 12) and the W4A8 GEMV reference
+# --------------------------------------------------------------------------
+
+ACT_BITS = 8  # l: SBVR-8 activations (Sec. 4.3)
+
+
+def act_quantize(x_fp16, l: int = ACT_BITS):
+    """Codes q (int32 [I]) and per-group scales s (float32 [I/128]) of the
+    online conversion (readings R11-R13 in the C source)."""
+    x = np.ascontiguousarray(np.asarray(x_fp16, dtype=np.float16).view(np.uint16))
+    I = x.size
+    q = np.zeros(I, dtype=np.int32)
+    s = np.zeros(I // GROUP, dtype=np.float32)
+    if _lib().oracle_act_quantize(I, l, _ptr(x, C.c_uint16), _ptr(q, C.c_int32), _ptr(s, C.c_float)) != 0:
+        raise ValueError("oracle_act_quantize rejected its arguments")
+    return q, s
+
+
+def act_planes(q, l: int = ACT_BITS) -> np.ndarray:
+    """SBVR-l bitvectors [I][l] of codes q in Eq. 12's coefficient order."""
+    q = np.ascontiguousarray(q, dtype=np.int32)
+    planes = np.zeros((q.size, l), dtype=np.uint8)
+    _lib().oracle_act_planes(q.size, l, _ptr(q, C.c_int32), _ptr(planes, C.c_uint8))
+    return planes
+
+
+def act_decode(planes, s, l: int = ACT_BITS) -> np.ndarray:
+    """Decoded activations (binary64) from SBVR-l bitvectors and group scales."""
+    planes = np.ascontiguousarray(planes, dtype=np.uint8)
+    s = np.ascontiguousarray(s, dtype=np.float32)
+    out = np.zeros(planes.shape[0])
+    _lib().oracle_act_decode(planes.shape[0], l, _ptr(planes, C.c_uint8), _ptr(s, C.c_float),
+                             _ptr(out, C.c_double))
+    return out
+
+
+def sbvr_gemv_w4a8(planes: np.ndarray, coeffs: np.ndarray, x_fp16: np.ndarray, rows=None,
+                   nthreads: int = 0) -> np.ndarray:
+    """The W4A8 decode GEMV reference: y = W_hat x_hat in binary64, with x_hat
+    the SBVR-8 decoded activations of x (conversion, bitvectors, decoding)."""
+    planes = np.ascontiguousarray(planes, dtype=np.uint32)
+    coeffs = np.ascontiguousarray(coeffs, dtype=np.uint16)
+    O, G, K, _ = planes.shape
+    I = G * GROUP
+    q, s = act_quantize(x_fp16)
+    x_hat = np.ascontiguousarray(act_decode(act_planes(q), s))
+    if rows is None:
+        rows_arr, n_rows = None, O
+    else:
+        rows_arr = np.ascontiguousarray(rows, dtype=np.int32)
+        n_rows = rows_arr.size
+    y = np.zeros(n_rows)
+    nt = _lib().oracle_sbvr_gemv_f64(O, I, K, _ptr(planes, C.c_uint32), _ptr(coeffs, C.c_uint16),
+                                     _ptr(x_hat, C.c_double), 1,
+                                     _ptr(rows_arr, C.c_int) if rows_arr is not None else None,
+                                     n_rows, int(nthreads), _ptr(y, C.c_double))
+    if nt < 0:
+        raise ValueError("oracle_sbvr_gemv_f64 rejected its arguments")
+    return y
 
 
 def rtn_sym_mse(D, bits: int) -> float:

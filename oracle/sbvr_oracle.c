@@ -34,6 +34,17 @@
  *   R6  Candidates with s <= 0 or a non-finite coefficient are skipped; if
  *       none is left the coefficients are (fp16(mean), 0, ..., 0).
  *   R7  Entries are visited r-outer, then s, then b (index order of Eq. 4).
+ *   R11 Online activation conversion (Sec. 4.3, Eq. 12): the coefficients
+ *       {-2^(l-1) s, s, 2s, ..., 2^(l-2) s} are the two's-complement weights
+ *       of an l-bit integer code q; the per-vector scale "absmax / 2^l" as
+ *       printed would leave half of [-absmax, absmax] outside that grid, so
+ *       s = absmax / (2^(l-1) - 1).
+ *   R12 Activation vectors are the 128-element groups of the inner dimension,
+ *       the ones that meet a weight group in the inner product (Sec. 4.4).
+ *   R13 The grid point is the conventional integer-grid rounding the section
+ *       adopts: t = x / s in binary32, q = t rounded to nearest even, within
+ *       +-(2^(l-1) - 1); s and t are binary32 (the precision the GPU kernel
+ *       takes this decision in); an all-zero vector has s = 0 and q = 0.
  */
 #include <math.h>
 #include <pthread.h>
@@ -483,6 +494,97 @@ int oracle_sbvr_gemv(int O, int I, int K, const uint32_t *planes, const uint16_t
     free(jobs);
     free(x);
     return nt;
+}
+
+/* Same as oracle_sbvr_gemv with activations given as binary64 values. */
+int oracle_sbvr_gemv_f64(int O, int I, int K, const uint32_t *planes, const uint16_t *coeffs,
+                         const double *x, int B, const int *rows, int n_rows, int nthreads,
+                         double *y)
+{
+    if (O < 1 || I < GROUP || I % GROUP || K < 1 || K > KMAX || B < 1)
+        return -1;
+    if (!rows)
+        n_rows = O;
+    int nt = resolve_threads(nthreads);
+    if (nt > n_rows)
+        nt = n_rows;
+    pthread_t *th = (pthread_t *)malloc(sizeof(pthread_t) * (size_t)nt);
+    gemv_job *jobs = (gemv_job *)malloc(sizeof(gemv_job) * (size_t)nt);
+    for (int i = 0; i < nt; ++i) {
+        gemv_job j = {O, I, K, B, planes, coeffs, x, rows, y, n_rows,
+                      (int)((long)n_rows * i / nt), (int)((long)n_rows * (i + 1) / nt)};
+        jobs[i] = j;
+        pthread_create(&th[i], NULL, gemv_worker, &jobs[i]);
+    }
+    for (int i = 0; i < nt; ++i)
+        pthread_join(th[i], NULL);
+    free(th);
+    free(jobs);
+    return nt;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Online activation conversion to SBVR-l (Sec. 4.3, Eq. 12; readings       */
+/* R11-R13).                                                                 */
+/* ------------------------------------------------------------------------ */
+
+/* x: binary16 [I] (I a multiple of 128); q: codes [I]; s: scales [I / 128]. */
+int oracle_act_quantize(int I, int l, const uint16_t *x, int32_t *q, float *s)
+{
+    if (I < GROUP || I % GROUP || l < 2 || l > 16)
+        return -1;
+    const int qmax = (1 << (l - 1)) - 1;
+    for (int g = 0; g < I / GROUP; ++g) {
+        float amax = 0.0f;
+        for (int j = 0; j < GROUP; ++j) {
+            const float v = (float)oracle_fp16_to_double(x[g * GROUP + j]);
+            const float a = v < 0.0f ? -v : v;
+            if (a > amax)
+                amax = a;
+        }
+        const float sc = amax / (float)qmax;
+        s[g] = sc;
+        for (int j = 0; j < GROUP; ++j) {
+            int code = 0;
+            if (sc > 0.0f) {
+                const float t = (float)oracle_fp16_to_double(x[g * GROUP + j]) / sc;
+                code = (int)nearbyintf(t);
+                if (code > qmax)
+                    code = qmax;
+                if (code < -qmax)
+                    code = -qmax;
+            }
+            q[g * GROUP + j] = code;
+        }
+    }
+    return 0;
+}
+
+/* Bitvectors of l-bit codes in Eq. 12's coefficient order: plane 0 carries
+ * -2^(l-1) s, plane i >= 1 carries 2^(i-1) s.  planes: [n][l] of 0/1. */
+void oracle_act_planes(int n, int l, const int32_t *q, uint8_t *planes)
+{
+    for (int e = 0; e < n; ++e) {
+        const int neg = q[e] < 0;
+        const int rest = q[e] + (neg ? (1 << (l - 1)) : 0);  /* in [0, 2^(l-1)) */
+        planes[(long)e * l] = (uint8_t)neg;
+        for (int i = 1; i < l; ++i)
+            planes[(long)e * l + i] = (uint8_t)((rest >> (i - 1)) & 1);
+    }
+}
+
+/* Decoded activations: x_hat = sum_i coefficient_i * bit_i with Eq. 12's
+ * coefficients for the group's scale (binary64, exact). */
+void oracle_act_decode(int I, int l, const uint8_t *planes, const float *s, double *x_hat)
+{
+    for (int e = 0; e < I; ++e) {
+        const double sc = (double)s[e / GROUP];
+        double v = planes[(long)e * l] ? -ldexp(sc, l - 1) : 0.0;
+        for (int i = 1; i < l; ++i)
+            if (planes[(long)e * l + i])
+                v += ldexp(sc, i - 1);
+        x_hat[e] = v;
+    }
 }
 
 /* ------------------------------------------------------------------------ */

@@ -388,3 +388,87 @@ def test_synth_is_deterministic_and_sane():
     assert abs(g.std() / 0.02 - 1) < 5 / np.sqrt(2 * g.size)
     x = synth.activations(4096, seed=synth.X_SEED_OFFSET)
     assert x.dtype == np.float16 and abs(float(x.astype(np.float64).std()) - 1) < 0.05
+
+
+# --------------------------------------------------------------------------
+# Online activation conversion to SBVR-8 (Sec. 4.3, Eq. 12) and the W4A8
+# reference (readings R11-R13 of the oracle)
+# --------------------------------------------------------------------------
+
+def test_eq12_eight_bit_coefficients_are_twos_complement():
+    """l = 8: {-128, 1, 2, ..., 64} (s = 1) has every integer -128..127 as
+    exactly one subset sum -- two's complement."""
+    coeffs = np.array([oracle.fp16_from_double(v) for v in (-128, 1, 2, 4, 8, 16, 32, 64)], dtype=np.uint16)
+    sums = oracle.subset_sums(coeffs)
+    assert sorted(sums.tolist()) == list(range(-128, 128))
+
+
+def test_act_bitvectors_decode_every_code():
+    q = np.arange(-127, 128, dtype=np.int32)
+    q = np.concatenate([q, np.zeros(128 * 2 - q.size, dtype=np.int32)])   # two groups
+    planes = oracle.act_planes(q)
+    assert planes.shape == (256, 8) and set(np.unique(planes)) <= {0, 1}
+    s = np.array([1.0, 0.375], dtype=np.float32)
+    x_hat = oracle.act_decode(planes, s)
+    np.testing.assert_array_equal(x_hat, q.astype(np.float64) * np.repeat(s.astype(np.float64), 128))
+    # the bit patterns are the two's-complement bytes of q
+    byte = (planes[:, 0].astype(int) << 7) | sum(planes[:, i].astype(int) << (i - 1) for i in range(1, 8))
+    np.testing.assert_array_equal(byte.astype(np.uint8), q.astype(np.int8).view(np.uint8))
+
+
+def test_act_quantize_nearest_grid_point():
+    """Each element maps to the nearest point of {k s : |k| <= 127} (fp64
+    check; the binary32 decision may differ only within rounding of a tie),
+    the error is at most s/2, and the group's absmax element maps to +-127."""
+    rng = np.random.default_rng(5)
+    for trial in range(20):
+        x = (rng.standard_normal(512) * 10 ** rng.uniform(-4, 3)).astype(np.float16)
+        if trial == 0:
+            x[:128] = 0           # a zero group
+        q, s = oracle.act_quantize(x)
+        xd = x.astype(np.float64)
+        for g in range(4):
+            sl = slice(128 * g, 128 * g + 128)
+            sg = float(s[g])
+            if np.abs(xd[sl]).max() == 0:
+                assert sg == 0 and np.all(q[sl] == 0)
+                continue
+            assert np.abs(q[sl]).max() == 127
+            err = np.abs(xd[sl] - q[sl] * sg)
+            assert err.max() <= sg / 2 * (1 + 2 ** -20)
+            t = xd[sl] / sg
+            clear = np.abs(np.abs(t - np.floor(t)) - 0.5) > 1e-4   # not near a tie
+            assert np.array_equal(q[sl][clear], np.clip(np.round(t[clear]), -127, 127).astype(np.int32))
+
+
+def test_act_quantize_power_of_two_scaling():
+    x = synth.activations(384, seed=8)
+    q1, s1 = oracle.act_quantize(x)
+    q2, s2 = oracle.act_quantize((x.astype(np.float32) * 4).astype(np.float16))
+    np.testing.assert_array_equal(q1, q2)
+    np.testing.assert_array_equal(s2, s1 * 4)
+
+
+def test_w4a8_reference_equals_fp16_reference_on_grid_activations():
+    """Activations that already lie on the grid (integers with absmax 127, so
+    s = 1) convert exactly: the W4A8 reference equals the fp16 one."""
+    O, I, K = 24, 512, 4
+    planes, coeffs = synth.random_sbvr(O, I, K, seed=4)
+    rng = np.random.default_rng(2)
+    x = rng.integers(-127, 128, size=I).astype(np.float16)
+    x[::128] = 127.0
+    q, s = oracle.act_quantize(x)
+    assert np.all(s == 1.0) and np.array_equal(q, x.astype(np.int32))
+    np.testing.assert_array_equal(oracle.sbvr_gemv_w4a8(planes, coeffs, x), oracle.sbvr_gemv(planes, coeffs, x))
+
+
+def test_w4a8_reference_is_dense_gemv_of_decoded_operands():
+    O, I, K = 16, 640, 3
+    planes, coeffs = synth.random_sbvr(O, I, K, seed=9)
+    x = synth.activations(I, seed=10)
+    q, s = oracle.act_quantize(x)
+    x_hat = oracle.act_decode(oracle.act_planes(q), s)
+    y = oracle.sbvr_gemv_w4a8(planes, coeffs, x)
+    np.testing.assert_allclose(y, oracle.decompress(planes, coeffs) @ x_hat, rtol=1e-12, atol=1e-15)
+    rows = [3, 0, 15]
+    np.testing.assert_array_equal(oracle.sbvr_gemv_w4a8(planes, coeffs, x, rows=rows), y[rows])
