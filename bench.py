@@ -27,6 +27,8 @@ One JSON line is printed:
                 taken on the current kernel sources (else null)
   small_batch   per projection at B = 2, 4, 8 activation vectors
                 (sbvr_gemm_small_batch), same timing
+  w4a8          per projection, batch 1 with the activations converted online
+                to 8-bit SBVR codes (sbvr_gemv_a8), same timing
   low_bit       per projection at k = 2 and 3 planes, same timing
   prefill       per projection: sbvr_decompress to binary16 (us, GB/s of the
                 SBVR bytes read plus the 2 bytes per weight written) and, for
@@ -35,9 +37,9 @@ One JSON line is printed:
   cpu_baseline  the CPU oracle (binary64 decompress + GEMV) on layer 0's seven
                 GEMVs, bounded to ~10 s of work, in the same unit
 
---traffic-probe runs, eagerly, four launches of every projection shape and an
-elementwise negation over 256 MiB of float32 (reads and writes 256 MiB: the
-counter calibration), for
+--traffic-probe runs, eagerly, four launches of every projection shape (fp16
+and W4A8 activations) and an elementwise negation over 256 MiB of float32
+(reads and writes 256 MiB: the counter calibration), for
   rocprofv3 --pmc FETCH_SIZE -- python3 bench.py --traffic-probe   (and WRITE_SIZE);
 --traffic-summary FETCH_CSV WRITE_CSV turns the two counter files into the
 record kept under profiles/.
@@ -153,21 +155,23 @@ def load_traffic(kernel: str):
     return None if k is None else k["bytes_per_launch"]
 
 
-def b1_kernel_instance(O: int, I: int, k: int) -> str:
+def b1_kernel_instance(O: int, I: int, k: int, a8: bool = False) -> str:
     """Name of the batch-1 kernel instance the library launches for an O x I
     matrix: the streaming kernel (ring depth D, several gblocks per wavefront
     or one) when a row has more than 16 gblocks of 512 elements or the matrix
     has at least 24576 (tile, gblock) blocks (tiles of 16/k rows, 4 at k = 3);
     otherwise the one-shot
     kernel with T tiles per workgroup, the most of 8/4/2/1 that still leaves
-    >= 256 workgroups."""
+    >= 256 workgroups.  The last template argument selects the W4A8 build
+    (activations converted online to SBVR-8)."""
+    a8 = "true" if a8 else "false"
     tr = {1: 16, 2: 8}.get(k, 4)  # rows per tile: 16 matrix-core rows of (row, plane)
     n_tiles, n_gblocks = (O + tr - 1) // tr, (I + 511) // 512
     if n_gblocks > 16 or n_tiles * n_gblocks >= 24576:
         multi = n_gblocks > 16
-        return f"gemv_b1s_kernel<{k}, {3 if multi else 2}, {'true' if multi else 'false'}>"
+        return f"gemv_b1s_kernel<{k}, {3 if multi else 2}, {'true' if multi else 'false'}, {a8}>"
     T = next((t for t in (8, 4, 2) if n_tiles // t >= 256), 1)
-    return f"gemv_b1_kernel<{k}, {T}>"
+    return f"gemv_b1_kernel<{k}, {T}, {a8}>"
 
 
 ROTATE_BYTES = 320e6  # > 256 MB MALL + 8 x 4 MB L2
@@ -234,6 +238,10 @@ def main():
                 for li in range(L):
                     W, x, y = layers[li][name]
                     sb.gemv(W, x, out=y, stream=stream)
+            for name in PROJ_ORDER:  # the W4A8 build of the same kernels
+                for li in range(L):
+                    W, x, y = layers[li][name]
+                    sb.gemv_a8(W, x, out=y, stream=stream)
             # calibration: an elementwise kernel that reads and writes CALIB_BYTES
             src = torch.ones(CALIB_BYTES // 4, dtype=torch.float32, device=dev)
             dst = torch.empty_like(src)
@@ -364,6 +372,20 @@ def main():
                 res[name] = {"us": round(us, 3), "gbps": round(bb / (us * 1e3), 1)}
             small_batch[str(B)] = res
 
+    # ---- W4A8 decode (sbvr_gemv_a8: activations converted online to SBVR-8)
+    # on the same weight copies ----
+    w4a8 = {}
+    if not args.quick:
+        def a8_call(W, x, y):
+            return (lambda W, x, y, stream: sb.gemv_a8(W, x, out=y, stream=stream)), (W, x, y)
+        for name in PROJ_ORDER:
+            O, I = shapes[name]
+            ws = weights[name]
+            xs = [torch.from_numpy(synth.activations(I, seed=800 + i)).to(dev) for i in range(8)]
+            ys = [torch.empty(O, dtype=torch.float16, device=dev) for _ in range(8)]
+            us = launch_us([a8_call(w, xs[i % 8], ys[i % 8]) for i, w in enumerate(ws)])
+            w4a8[name] = {"us": round(us, 3), "gbps": round(nbytes[name] / (us * 1e3), 1)}
+
     # ---- prefill path: decompression to binary16 (HBM-bound: reads the SBVR
     # bytes, writes 2 bytes per weight), then a library GEMM over T tokens ----
     prefill = {}
@@ -466,6 +488,7 @@ def main():
         "roofline": roofline,
         "decode_step": decode_step,
         "small_batch": small_batch or None,
+        "w4a8": w4a8 or None,
         "low_bit": low_bit or None,
         "prefill": prefill or None,
         ("llama3_70b" if args.model == "llama3-8b" else "llama3_8b"): other_model,

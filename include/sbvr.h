@@ -70,7 +70,8 @@ enum sbvr_status {
 /* Human-readable name of a status code; never NULL, static storage. */
 const char *sbvr_status_string(int status);
 
-/* Library ABI version (major * 100 + minor); 1.01 adds sbvr_decompress. */
+/* Library ABI version (major * 100 + minor); 1.01 adds sbvr_decompress,
+ * 1.02 sbvr_gemv_a8. */
 int sbvr_version(void);
 
 /*
@@ -129,6 +130,20 @@ int sbvr_gemv(int O, int I, int k, const void *planes_dev, const void *coeffs_de
 int sbvr_gemm_small_batch(int O, int I, int k, const void *planes_dev, const void *coeffs_dev,
                           const uint16_t *X, uint16_t *Y, int B, void *workspace,
                           size_t ws_bytes, hipStream_t stream);
+
+/*
+ * The W4A8 decode GEMV (Sec. 4.3 and 4.4 with 8-bit SBVR activations): x is
+ * converted online, per 128-element group g, to an 8-bit code with Eq. 12's
+ * two's-complement coefficients {-128 s_g, s_g, 2 s_g, ..., 64 s_g}:
+ *     s_g = max_j abs(x[128 g + j]) / 127,  q_j = rne(x_j / s_g) in [-127, 127]
+ * (binary32, correctly rounded division; a zero group has s_g = 0, q = 0),
+ * and
+ *     y[o] = fp16_rne( sum_g s_g sum_i c[o][g][i] * sum_j b[o][g][i][j] q_j ).
+ * Arguments as sbvr_gemv (x binary16 [I], y binary16 [O]).
+ */
+int sbvr_gemv_a8(int O, int I, int k, const void *planes_dev, const void *coeffs_dev,
+                 const uint16_t *x, uint16_t *y, void *workspace, size_t ws_bytes,
+                 hipStream_t stream);
 
 /*
  * Decompression for the prefill path: the decoded matrix as binary16,

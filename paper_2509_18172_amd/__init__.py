@@ -29,7 +29,7 @@ SBVR_E_HIP = -5
 EXPORTED = (
     "sbvr_status_string", "sbvr_version", "sbvr_packed_plane_bytes", "sbvr_packed_coeff_bytes",
     "sbvr_workspace_bytes", "sbvr_pack", "sbvr_unpack", "sbvr_gemv", "sbvr_gemm_small_batch",
-    "sbvr_decompress",
+    "sbvr_decompress", "sbvr_gemv_a8",
 )
 
 
@@ -65,6 +65,7 @@ def _load():
         "sbvr_gemv": (i32, [i32, i32, i32, vp, vp, vp, vp, vp, sz, vp]),
         "sbvr_gemm_small_batch": (i32, [i32, i32, i32, vp, vp, vp, vp, i32, vp, sz, vp]),
         "sbvr_decompress": (i32, [i32, i32, i32, vp, vp, vp, vp]),
+        "sbvr_gemv_a8": (i32, [i32, i32, i32, vp, vp, vp, vp, vp, sz, vp]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -116,6 +117,10 @@ def sbvr_gemm_small_batch(O, I, k, planes_dev, coeffs_dev, X, Y, B, workspace=No
                           stream=0) -> int:
     return _lib.sbvr_gemm_small_batch(O, I, k, planes_dev, coeffs_dev, X, Y, B, workspace, ws_bytes,
                                       stream)
+
+
+def sbvr_gemv_a8(O, I, k, planes_dev, coeffs_dev, x, y, workspace=None, ws_bytes=0, stream=0) -> int:
+    return _lib.sbvr_gemv_a8(O, I, k, planes_dev, coeffs_dev, x, y, workspace, ws_bytes, stream)
 
 
 def sbvr_decompress(O, I, k, planes_dev, coeffs_dev, W, stream=0) -> int:
@@ -209,6 +214,17 @@ def gemm_small_batch(W: PackedWeight, X, out=None, stream=None):
                                  X.data_ptr(), Y.data_ptr(), B, None, 0, _stream(stream)),
            "sbvr_gemm_small_batch")
     return Y
+
+
+def gemv_a8(W: PackedWeight, x, out=None, stream=None):
+    """The W4A8 decode GEMV: x fp16 [I] converted online to SBVR-8 activations
+    (per-128-group scale, 8-bit two's-complement codes); returns fp16 [O]."""
+    torch = _torch()
+    assert x.dtype == torch.float16 and x.is_contiguous() and x.shape == (W.I,)
+    y = torch.empty(W.O, dtype=torch.float16, device=x.device) if out is None else out
+    _check(sbvr_gemv_a8(W.O, W.I, W.k, W.planes.data_ptr(), W.coeffs.data_ptr(), x.data_ptr(),
+                        y.data_ptr(), None, 0, _stream(stream)), "sbvr_gemv_a8")
+    return y
 
 
 def decompress(W: PackedWeight, out=None, stream=None):

@@ -72,7 +72,7 @@ const char *sbvr_status_string(int status)
     }
 }
 
-int sbvr_version(void) { return 101; }
+int sbvr_version(void) { return 102; }
 
 size_t sbvr_packed_plane_bytes(int O, int I, int k)
 {
@@ -118,7 +118,7 @@ int sbvr_gemv(int O, int I, int k, const void *planes_dev, const void *coeffs_de
     int st = check_gemv(O, I, k, planes_dev, coeffs_dev, x, y, 1, ws_bytes);
     if (st != SBVR_OK)
         return st;
-    return launch_gemv_b1(make_dims(O, I, k), planes_dev, coeffs_dev, x, y, stream);
+    return launch_gemv_b1(make_dims(O, I, k), planes_dev, coeffs_dev, x, y, false, stream);
 }
 
 int sbvr_gemm_small_batch(int O, int I, int k, const void *planes_dev, const void *coeffs_dev,
@@ -131,8 +131,18 @@ int sbvr_gemm_small_batch(int O, int I, int k, const void *planes_dev, const voi
         return st;
     const Dims d = make_dims(O, I, k);
     if (B == 1)
-        return launch_gemv_b1(d, planes_dev, coeffs_dev, X, Y, stream);
+        return launch_gemv_b1(d, planes_dev, coeffs_dev, X, Y, false, stream);
     return launch_gemm_sbs(d, planes_dev, coeffs_dev, X, Y, B, stream);
+}
+
+int sbvr_gemv_a8(int O, int I, int k, const void *planes_dev, const void *coeffs_dev,
+                 const uint16_t *x, uint16_t *y, void *workspace, size_t ws_bytes, hipStream_t stream)
+{
+    (void)workspace;
+    int st = check_gemv(O, I, k, planes_dev, coeffs_dev, x, y, 1, ws_bytes);
+    if (st != SBVR_OK)
+        return st;
+    return launch_gemv_b1(make_dims(O, I, k), planes_dev, coeffs_dev, x, y, true, stream);
 }
 
 int sbvr_decompress(int O, int I, int k, const void *planes_dev, const void *coeffs_dev, uint16_t *W,

@@ -217,6 +217,80 @@ __device__ __forceinline__ Limbs split_limbs(uint4 xv, int sigma, int inv_alpha)
     return L;
 }
 
+// Online conversion to SBVR-8 activations (Sec. 4.3, Eq. 12) for the W4A8
+// decode path.  The lanes 16r .. 16r+15 of a wavefront hold the 128 elements
+// of group r of the gblock (eight each).  Per group: s = absmax / 127 and the
+// 8-bit code q = rne(fl(x / s)) within +-127 (binary32, correctly rounded
+// division; a zero group has s = 0, q = 0).  Eq. 12's coefficients are the
+// two's-complement weights of q, so the matrix-core operand carries q itself,
+// split exactly into two E4M3 limbs: 16 * floor(q / 16) and q mod 16 (each
+// divided by alpha_v, still exact), in the hi and mid limb slots (lo = 0).
+// Returns the limbs; `out_scale` receives the scale of the group of the
+// lane's result column (slot (lane % 16) / 4), which multiplies its sums.
+//
+// The code is taken from t = x * rcp(s) when t is clearly away from a
+// half-integer: rcp is within 1 ulp and the product adds half an ulp, so
+// |t - fl(x / s)| <= 2^-22 |x / s| <= 2^-15 (|x / s| <= 128); a distance of
+// at least 2^-14 from the nearest half-integer then gives the same rounded
+// integer as fl(x / s).  Elements closer than that (rare) use the correctly
+// rounded division.
+__device__ __forceinline__ float row16_max(float v)
+{
+    v = fmaxf(v, dpp_f32<DPP_QUAD_XOR1>(v));
+    v = fmaxf(v, dpp_f32<DPP_QUAD_XOR2>(v));
+    v = fmaxf(v, dpp_f32<DPP_ROW_HALF_MIRROR>(v));
+    v = fmaxf(v, dpp_f32<DPP_ROW_MIRROR>(v));
+    return v;
+}
+
+__device__ __forceinline__ Limbs a8_limbs(uint4 xv, int lane, int inv_alpha, float &out_scale)
+{
+    const uint32_t w[4] = {xv.x, xv.y, xv.z, xv.w};
+    float xf[8];
+    float amax = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        xf[2 * i] = half_bits_to_float(w[i] & 0xffffu);
+        xf[2 * i + 1] = half_bits_to_float(w[i] >> 16);
+        amax = fmaxf(amax, fmaxf(fabsf(xf[2 * i]), fabsf(xf[2 * i + 1])));
+    }
+    const float sg = __fdiv_rn(row16_max(amax), 127.0f);  // this lane's group
+    const float r = sg > 0.f ? __builtin_amdgcn_rcpf(sg) : 0.f;
+    float qf[8];
+    float dmax = 0.f;  // largest |t - rint(t)| (exact differences)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        const float t = xf[e] * r;
+        qf[e] = rintf(t);
+        dmax = fmaxf(dmax, fabsf(t - qf[e]));
+    }
+    if (dmax >= 0.5f - 0x1p-14f) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+            qf[e] = rintf(__fdiv_rn(xf[e], sg));  // sg > 0 here: t = 0 otherwise
+    }
+    const float f = ldexpf(1.0f, inv_alpha), f16 = 16.0f * f;
+    float hi[8], lo[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        const float q = fminf(127.f, fmaxf(-127.f, qf[e]));
+        const float fl = floorf(q * 0.0625f);  // floor(q / 16), exact
+        hi[e] = fl * f16;
+        lo[e] = fmaf(fl, -16.0f, q) * f;  // q mod 16, exact
+    }
+    Limbs L;
+    pack8_fp8(hi, L.hi);
+    pack8_fp8(lo, L.mid);
+    L.lo[0] = L.lo[1] = 0u;
+    const int slot = (lane & 15) >> 2;
+    const float s0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sg), 0));
+    const float s1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sg), 16));
+    const float s2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sg), 32));
+    const float s3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sg), 48));
+    out_scale = slot == 0 ? s0 : (slot == 1 ? s1 : (slot == 2 ? s2 : s3));
+    return L;
+}
+
 // max |x| over the wavefront's binary16 activations (eight per lane), as a
 // float: the magnitudes' bit patterns order like unsigned integers.
 __device__ __forceinline__ float wave_absmax_h(uint4 v)

@@ -37,7 +37,7 @@ struct B1Regs {
     uint4 x;     // this lane's 8 activations
 };
 
-template <int K, int T>
+template <int K, int T, bool A8>
 __global__ void __launch_bounds__(1024) gemv_b1_kernel(GemvArgs a)
 {
     extern __shared__ __align__(16) unsigned char smem[];
@@ -71,6 +71,7 @@ __global__ void __launch_bounds__(1024) gemv_b1_kernel(GemvArgs a)
         // activations first; lanes past I (ragged end) read a valid address
         // and are zeroed before use
         R.x = *(const uint4 *)(a.x + min(gb * (GB * GROUP) + lane * 8, a.I - 8));
+        __builtin_amdgcn_sched_barrier(0);  // the operand build waits only for x
 #pragma unroll
         for (int t = 0; t < T; ++t) {
             const size_t blk = (size_t)(tblk[t] + gb);
@@ -103,11 +104,19 @@ __global__ void __launch_bounds__(1024) gemv_b1_kernel(GemvArgs a)
             acc[t][p] = 0.f;
 
     // Activation limbs of the gblock in R -> LDS -> the four B operands;
-    // returns 2^-sigma, the factor that undoes the activation scaling.
+    // returns the factor that undoes the activation scaling (2^-sigma; with
+    // SBVR-8 activations the lane's group scale).
     auto operands = [&](const B1Regs<K, T> &R, v8i *Bq) -> float {
         const uint4 xv = gb * (GB * GROUP) + lane * 8 < a.I ? R.x : make_uint4(0u, 0u, 0u, 0u);
-        const int sigma = scale_exponent(wave_absmax_h(xv));
-        const Limbs L = split_limbs(xv, sigma, inv_alpha);
+        float out_scale;
+        Limbs L;
+        if constexpr (A8) {
+            L = a8_limbs(xv, lane, inv_alpha, out_scale);
+        } else {
+            const int sigma = scale_exponent(wave_absmax_h(xv));
+            L = split_limbs(xv, sigma, inv_alpha);
+            out_scale = ldexpf(1.0f, -sigma);
+        }
         // same wavefront: the LDS writes complete before the reads below
         *(uint2 *)(lds + wr_off + 0 * 32) = make_uint2(L.hi[0], L.hi[1]);
         *(uint2 *)(lds + wr_off + 1 * 32) = make_uint2(L.mid[0], L.mid[1]);
@@ -115,7 +124,7 @@ __global__ void __launch_bounds__(1024) gemv_b1_kernel(GemvArgs a)
 #pragma unroll
         for (int q = 0; q < 4; ++q)
             Bq[q] = lds_operand(lds + lo_off + q * 512, lds + hi_off + q * 512);
-        return ldexpf(1.0f, -sigma);
+        return out_scale;
     };
     // The T tiles of the gblock in R.
     auto tiles = [&](const B1Regs<K, T> &R, const v8i *Bq, float inv_scale) {
@@ -205,15 +214,21 @@ static int choose_b1_tiles(const Dims &d)
 #endif
 }
 
-template <int K>
+template <int K, bool A8>
 static const void *b1_kernel_for(int T)
 {
     switch (T) {
-    case 8: return (const void *)gemv_b1_kernel<K, 8>;
-    case 4: return (const void *)gemv_b1_kernel<K, 4>;
-    case 2: return (const void *)gemv_b1_kernel<K, 2>;
-    default: return (const void *)gemv_b1_kernel<K, 1>;
+    case 8: return (const void *)gemv_b1_kernel<K, 8, A8>;
+    case 4: return (const void *)gemv_b1_kernel<K, 4, A8>;
+    case 2: return (const void *)gemv_b1_kernel<K, 2, A8>;
+    default: return (const void *)gemv_b1_kernel<K, 1, A8>;
     }
+}
+
+template <int K>
+static const void *b1_kernel_for(int T, bool a8)
+{
+    return a8 ? b1_kernel_for<K, true>(T) : b1_kernel_for<K, false>(T);
 }
 
 // Matrices with more (tile, gblock) blocks than this, or more than 16
@@ -223,20 +238,20 @@ static const void *b1_kernel_for(int T)
 #endif
 
 int launch_gemv_b1(const Dims &d, const void *planes_dev, const void *coeffs_dev,
-                   const uint16_t *x, uint16_t *y, hipStream_t stream)
+                   const uint16_t *x, uint16_t *y, bool a8, hipStream_t stream)
 {
     if (d.n_gblocks > B1_MAX_WAVES || (long)d.n_tiles * d.n_gblocks >= SBVR_B1S_MIN_BLOCKS)
-        return launch_gemv_b1s(d, planes_dev, coeffs_dev, x, y, stream);
+        return launch_gemv_b1s(d, planes_dev, coeffs_dev, x, y, a8, stream);
     const int T = choose_b1_tiles(d);
     const int waves = d.n_gblocks;
     GemvArgs a = {(const uint4 *)planes_dev, (const uint16_t *)coeffs_dev, x, y, d.O, d.I, d.k,
                   d.n_tiles, d.n_gblocks, 1, 1, 0};
     const int grid = (d.n_tiles + T - 1) / T;
     const size_t lds = (size_t)waves * B1_WAVE_LDS + (size_t)waves * T * d.tr * 4;
-    const void *fn = d.k == 4   ? b1_kernel_for<4>(T)
-                     : d.k == 3 ? b1_kernel_for<3>(T)
-                     : d.k == 2 ? b1_kernel_for<2>(T)
-                                : b1_kernel_for<1>(T);
+    const void *fn = d.k == 4   ? b1_kernel_for<4>(T, a8)
+                     : d.k == 3 ? b1_kernel_for<3>(T, a8)
+                     : d.k == 2 ? b1_kernel_for<2>(T, a8)
+                                : b1_kernel_for<1>(T, a8);
     void *args[] = {&a};
     return launch_kernel(fn, dim3(grid), dim3(64 * waves), lds, stream, args);
 }

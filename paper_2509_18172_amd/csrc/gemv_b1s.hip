@@ -52,7 +52,7 @@ constexpr int B1S_WAVE_LDS = 2048;  // per wavefront: [q][s][l][32 B]
 #define SBVR_B1S_GROUPS_MULTI 256
 #endif
 
-template <int K, int D, bool MULTI>
+template <int K, int D, bool MULTI, bool A8>
 __global__ void __launch_bounds__(1024) gemv_b1s_kernel(GemvArgs a)
 {
     extern __shared__ __align__(16) unsigned char smem[];
@@ -114,7 +114,9 @@ __global__ void __launch_bounds__(1024) gemv_b1s_kernel(GemvArgs a)
         return *(const uint4 *)(a.x + min(e, a.I - 8));
     };
 
+    // x first: the operand build waits only for it, not for the ring loads
     uint4 x_cur = load_x(wv);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int j = 0; j < D; ++j)
         issue(j);
@@ -141,9 +143,14 @@ __global__ void __launch_bounds__(1024) gemv_b1s_kernel(GemvArgs a)
     float inv_scale;
     auto build = [&](uint4 xr, int gb) {
         const uint4 xv = gb * (GB * GROUP) + lane * 8 < a.I ? xr : make_uint4(0u, 0u, 0u, 0u);
-        const int sigma = scale_exponent(wave_absmax_h(xv));
-        inv_scale = ldexpf(1.0f, -sigma);
-        const Limbs L = split_limbs(xv, sigma, inv_alpha);
+        Limbs L;
+        if constexpr (A8) {
+            L = a8_limbs(xv, lane, inv_alpha, inv_scale);  // per lane: its column's group scale
+        } else {
+            const int sigma = scale_exponent(wave_absmax_h(xv));
+            inv_scale = ldexpf(1.0f, -sigma);
+            L = split_limbs(xv, sigma, inv_alpha);
+        }
         // same wavefront: these writes land before the reads below, and after
         // the reads of the previous gblock's operand
         *(uint2 *)(lds + wr_off + 0 * 32) = make_uint2(L.hi[0], L.hi[1]);
@@ -213,15 +220,21 @@ __global__ void __launch_bounds__(1024) gemv_b1s_kernel(GemvArgs a)
     }
 }
 
-template <int K>
+template <int K, bool A8>
 static const void *b1s_kernel_for(bool multi)
 {
-    return multi ? (const void *)gemv_b1s_kernel<K, SBVR_B1S_DEPTH_MULTI, true>
-                 : (const void *)gemv_b1s_kernel<K, SBVR_B1S_DEPTH, false>;
+    return multi ? (const void *)gemv_b1s_kernel<K, SBVR_B1S_DEPTH_MULTI, true, A8>
+                 : (const void *)gemv_b1s_kernel<K, SBVR_B1S_DEPTH, false, A8>;
+}
+
+template <int K>
+static const void *b1s_kernel_for(bool multi, bool a8)
+{
+    return a8 ? b1s_kernel_for<K, true>(multi) : b1s_kernel_for<K, false>(multi);
 }
 
 int launch_gemv_b1s(const Dims &d, const void *planes_dev, const void *coeffs_dev,
-                    const uint16_t *x, uint16_t *y, hipStream_t stream)
+                    const uint16_t *x, uint16_t *y, bool a8, hipStream_t stream)
 {
     const int gpw = (d.n_gblocks + SBVR_B1S_MAX_WAVES - 1) / SBVR_B1S_MAX_WAVES;
     const int waves = (d.n_gblocks + gpw - 1) / gpw;
@@ -232,10 +245,10 @@ int launch_gemv_b1s(const Dims &d, const void *planes_dev, const void *coeffs_de
                   d.n_tiles, d.n_gblocks, gpw, 1, tpw};
     const size_t lds = (size_t)waves * B1S_WAVE_LDS + (size_t)tpw * waves * d.tr * 4;
     const bool multi = gpw > 1;
-    const void *fn = d.k == 4   ? b1s_kernel_for<4>(multi)
-                     : d.k == 3 ? b1s_kernel_for<3>(multi)
-                     : d.k == 2 ? b1s_kernel_for<2>(multi)
-                                : b1s_kernel_for<1>(multi);
+    const void *fn = d.k == 4   ? b1s_kernel_for<4>(multi, a8)
+                     : d.k == 3 ? b1s_kernel_for<3>(multi, a8)
+                     : d.k == 2 ? b1s_kernel_for<2>(multi, a8)
+                                : b1s_kernel_for<1>(multi, a8);
     void *args[] = {&a};
     return launch_kernel(fn, dim3(grid), dim3(64 * waves), lds, stream, args);
 }

@@ -24,10 +24,11 @@ int launch_pack(const Dims &d, const uint32_t *planes_canon, const uint16_t *coe
                 void *planes_dev, void *coeffs_dev, hipStream_t stream);
 int launch_unpack(const Dims &d, const void *planes_dev, const void *coeffs_dev,
                   uint32_t *planes_canon, uint16_t *coeffs_canon, hipStream_t stream);
+// a8: activations converted online to SBVR-8 (the W4A8 decode path)
 int launch_gemv_b1(const Dims &d, const void *planes_dev, const void *coeffs_dev,
-                   const uint16_t *x, uint16_t *y, hipStream_t stream);
+                   const uint16_t *x, uint16_t *y, bool a8, hipStream_t stream);
 int launch_gemv_b1s(const Dims &d, const void *planes_dev, const void *coeffs_dev,
-                    const uint16_t *x, uint16_t *y, hipStream_t stream);
+                    const uint16_t *x, uint16_t *y, bool a8, hipStream_t stream);
 int launch_decompress(const Dims &d, const void *planes_dev, const void *coeffs_dev, uint16_t *W,
                       hipStream_t stream);
 int launch_gemm_sbs(const Dims &d, const void *planes_dev, const void *coeffs_dev,

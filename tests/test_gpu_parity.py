@@ -189,8 +189,12 @@ def test_small_batch_low_bit(sb, k):
 # --------------------------------------------------------------------------
 
 def fp16_ulp(v):
+    """Spacing above |v| in binary16 (at the largest finite value, the
+    spacing below it, 32)."""
     v = np.abs(np.asarray(v, dtype=np.float16))
-    return (np.nextafter(v, np.float16(np.inf)) - v).astype(np.float64)
+    with np.errstate(over="ignore"):
+        u = (np.nextafter(v, np.float16(np.inf)) - v).astype(np.float64)
+    return np.where(np.isinf(u), 32.0, u)
 
 
 def test_unit_vector_picks_a_column(sb):
@@ -464,3 +468,192 @@ def test_prefill_gemm_with_library_matmul(sb):
     errs = [rel_err(Y[t], Y_ref[t]) for t in range(T)]
     log(f"prefill {O}x{I} T={T} worst err={max(errs):.3e}")
     assert max(errs) <= TOL
+
+
+# --------------------------------------------------------------------------
+# W4A8 decode path: online conversion of x to SBVR-8 activations (Sec. 4.3,
+# Eq. 12) inside the GEMV; reference = oracle.sbvr_gemv_w4a8
+# --------------------------------------------------------------------------
+
+def run_gemv_a8(sb, W, x16):
+    y = sb.gemv_a8(W, dev(x16))
+    torch.cuda.synchronize()
+    return y.cpu().numpy().astype(np.float64)
+
+
+def selection_sbvr(O, I, k, cols):
+    """Planes and coefficients with W_hat[o][cols[o]] = 1 and zero elsewhere:
+    plane 0 has the one bit, coefficient 1.0; the other planes are empty."""
+    G = I // 128
+    planes = np.zeros((O, G, k, 4), dtype=np.uint32)
+    coeffs = np.zeros((O, G, k), dtype=np.uint16)
+    for o, j in enumerate(cols):
+        g, t = divmod(int(j), 128)
+        planes[o, g, 0, t // 32] |= np.uint32(1) << np.uint32(t % 32)
+        coeffs[o, g, 0] = np.float16(1.0).view(np.uint16)
+    return planes, coeffs
+
+
+@pytest.mark.parametrize("O,I", SHAPES_8B + SHAPES_70B)
+def test_a8_full_size_k4(sb, O, I):
+    planes, coeffs = synth.random_sbvr(O, I, 4, seed=O + 11 * I)
+    x = synth.activations(I, seed=O + 2 * I + synth.X_SEED_OFFSET)
+    y = run_gemv_a8(sb, packed(sb, planes, coeffs), x)
+    err = rel_err(y, oracle.sbvr_gemv_w4a8(planes, coeffs, x))
+    log(f"a8 full {O}x{I} k=4 err={err:.3e}")
+    assert err <= TOL
+
+
+@pytest.mark.parametrize("k", [1, 2, 3])
+@pytest.mark.parametrize("O,I", [(4096, 4096), (4096, 14336)])
+def test_a8_full_size_low_bit(sb, O, I, k):
+    planes, coeffs = synth.random_sbvr(O, I, k, seed=O + 11 * I + k)
+    x = synth.activations(I, seed=O + 2 * I + k + synth.X_SEED_OFFSET)
+    y = run_gemv_a8(sb, packed(sb, planes, coeffs), x)
+    err = rel_err(y, oracle.sbvr_gemv_w4a8(planes, coeffs, x))
+    log(f"a8 full {O}x{I} k={k} err={err:.3e}")
+    assert err <= TOL
+
+
+@pytest.mark.parametrize("O,I,k", [(1, 128, 4), (3, 128, 1), (1001, 640, 3), (7, 896, 4),
+                                   (4097, 1152, 2), (33, 2560, 4)])
+def test_a8_ragged_shapes(sb, O, I, k):
+    """Both batch-1 kernels (one-shot for short rows, streaming for long),
+    partial tiles and partial gblocks."""
+    planes, coeffs = synth.random_sbvr(O, I, k, seed=O + I + k)
+    x = synth.activations(I, seed=O * 3 + k)
+    y = run_gemv_a8(sb, packed(sb, planes, coeffs), x)
+    err = rel_err(y, oracle.sbvr_gemv_w4a8(planes, coeffs, x))
+    assert err <= TOL, err
+
+
+@pytest.mark.parametrize("I", [640, 4096])
+def test_a8_codes_through_a_selection_matrix(sb, I):
+    """y[o] = s_g q_j for a matrix that selects column j: every output checks
+    one 8-bit code and its group scale.  A code off by one moves y by s_g,
+    at least 1/127 of |y| -- several binary16 ulps -- so agreement within one
+    ulp means every code and scale matches the oracle's.  Groups span normal,
+    subnormal, zero and single-element-dominated magnitudes."""
+    G = I // 128
+    rng = np.random.default_rng(I)
+    x = rng.standard_normal(I)
+    mags = [1.0, 3e3, 1e-6, 0.0, 6000.0, 0.5, 2.0 ** -20, 7.0]
+    for g in range(G):
+        x[g * 128:(g + 1) * 128] *= mags[g % len(mags)]
+    if G > 5:
+        x[5 * 128 + 3] = 65504.0  # one element dominates its group
+    x16 = x.astype(np.float16)
+    assert np.all(np.isfinite(x16))
+    cols = np.arange(I)
+    planes, coeffs = selection_sbvr(I, I, 4, cols)
+    assert np.array_equal(oracle.decompress(planes, coeffs), np.eye(I))
+    y = run_gemv_a8(sb, packed(sb, planes, coeffs), x16)
+    q, s = oracle.act_quantize(x16)
+    y_ref = q.astype(np.float64) * np.repeat(s.astype(np.float64), 128)
+    assert np.array_equal(y_ref, oracle.sbvr_gemv_w4a8(planes, coeffs, x16))
+    ulp = fp16_ulp(y_ref.astype(np.float16))
+    bad = np.abs(y - y_ref.astype(np.float16).astype(np.float64)) > ulp
+    assert not bad.any(), (np.flatnonzero(bad)[:8], y[bad][:8], y_ref[bad][:8])
+    # zero groups give exact zeros
+    zero_groups = [g for g in range(G) if not np.any(x16[g * 128:(g + 1) * 128])]
+    for g in zero_groups:
+        assert np.all(y[g * 128:(g + 1) * 128] == 0)
+
+
+def test_a8_ties_round_to_even(sb):
+    """Groups whose maximum is 127 * 2^-7 have s = 2^-7 exactly, so x = m/2^7
+    + 1/2^8 lies halfway between two codes: the code is the even one, and
+    y = s q is exact in binary16."""
+    I = 512
+    m = np.arange(-126, 126, dtype=np.float64)
+    x = np.concatenate([(m + 0.5) / 128.0, [127 / 128.0, -127 / 128.0]])
+    x = np.resize(x, I)
+    for g in range(I // 128):  # every group holds its maximum 127/128
+        x[g * 128] = 127 / 128.0
+    x16 = x.astype(np.float16)
+    assert np.array_equal(x16.astype(np.float64), x)
+    planes, coeffs = selection_sbvr(I, I, 2, np.arange(I))
+    y = run_gemv_a8(sb, packed(sb, planes, coeffs), x16)
+    q_even = np.rint(x * 128.0)  # numpy rint: ties to even
+    assert np.array_equal(y, q_even / 128.0)
+
+
+def test_a8_within_quantisation_bound_of_fp16_path(sb):
+    """Independent of the oracle's conversion: |x - x_hat| <= s_g / 2 per
+    element, so the W4A8 and fp16-activation results differ by at most
+    sum_j |W_hat[o][j]| s_g(j) / 2 (plus the two binary16 output roundings)."""
+    O, I = 512, 4096
+    planes, coeffs = synth.random_sbvr(O, I, 4, seed=77)
+    x16 = synth.activations(I, seed=78)
+    W = packed(sb, planes, coeffs)
+    y8 = run_gemv_a8(sb, W, x16)
+    y16 = run_gemv(sb, W, x16)
+    What = oracle.decompress(planes, coeffs)
+    xg = np.abs(x16.astype(np.float64)).reshape(-1, 128).max(axis=1) / 127.0
+    bound = np.abs(What) @ np.repeat(xg, 128) / 2
+    slack = fp16_ulp(y8) + fp16_ulp(y16) + 1e-3 * np.abs(y16).max()
+    assert np.all(np.abs(y8 - y16) <= bound * (1 + 1e-6) + slack)
+    # and the conversion does change the result (the path is not the fp16 one)
+    assert not np.array_equal(y8, y16)
+
+
+def test_a8_error_paths_and_canary(sb):
+    O, I = 100, 512
+    planes, coeffs = synth.random_sbvr(O, I, 4, seed=5)
+    W = packed(sb, planes, coeffs)
+    xh = synth.activations(I, seed=6)
+    x = dev(xh)
+    buf = torch.full((O + 64,), 7.0, dtype=torch.float16, device="cuda")
+    st = sb.sbvr_gemv_a8(O, I, 4, W.planes.data_ptr(), W.coeffs.data_ptr(), x.data_ptr(),
+                         buf.data_ptr(), None, 0, 0)
+    torch.cuda.synchronize()
+    assert st == 0
+    assert torch.all(buf[O:] == 7.0)
+    assert rel_err(buf[:O].cpu().numpy().astype(np.float64),
+                   oracle.sbvr_gemv_w4a8(planes, coeffs, xh)) <= TOL
+    buf.fill_(5.0)
+    torch.cuda.synchronize()
+    for args in [(O, I, 5), (O, 100, 4), (0, I, 4)]:
+        st = sb.sbvr_gemv_a8(*args, W.planes.data_ptr(), W.coeffs.data_ptr(), x.data_ptr(),
+                             buf.data_ptr(), None, 0, 0)
+        assert st != 0
+    st = sb.sbvr_gemv_a8(O, I, 4, W.planes.data_ptr(), W.coeffs.data_ptr(), x.data_ptr() + 2,
+                         buf.data_ptr(), None, 0, 0)
+    assert st == sb.SBVR_E_ALIGNMENT
+    st = sb.sbvr_gemv_a8(O, I, 4, None, W.coeffs.data_ptr(), x.data_ptr(), buf.data_ptr(), None, 0, 0)
+    assert st == sb.SBVR_E_INVALID_ARG
+    torch.cuda.synchronize()
+    assert torch.all(buf == 5.0)
+
+
+def test_a8_codes_near_half_integers(sb):
+    """Elements whose x / s lies within 2^-12 of a half-integer (found by
+    scanning every binary16 value below the group maximum), where a code
+    taken from an approximate quotient could differ from the rounded
+    correctly-rounded quotient; includes quotients that round in binary32 to
+    a half-integer exactly (then ties go to even)."""
+    amaxes = [1.0, 0.7001953125, 3.140625, 0.0010004043579101562, 1000.5, 12.34375, 65504.0, 2.0 ** -14]
+    all16 = np.arange(1, 0x7c00, dtype=np.uint16).view(np.float16).astype(np.float64)
+    groups, n_ties = [], 0
+    for a in amaxes:
+        a16 = np.float16(a)
+        s = np.float32(np.float32(a16) / np.float32(127.0))
+        cand = all16[all16 < float(a16)]
+        t = cand / float(s)
+        near = cand[np.abs(np.abs(t - np.floor(t)) - 0.5) < 2.0 ** -12]
+        t32 = (near.astype(np.float32) / s).astype(np.float64)
+        n_ties += int(np.sum(t32 - np.floor(t32) == 0.5))
+        rng = np.random.default_rng(len(groups))
+        pick = rng.permutation(near)[:127] if near.size else near
+        g = np.resize(np.concatenate([pick, -pick]) if pick.size else [0.0], 127)
+        groups.append(np.concatenate([[float(a16)], g]))
+    assert n_ties > 0  # the scan does reach binary32 ties
+    x16 = np.concatenate(groups).astype(np.float16)
+    I = x16.size
+    planes, coeffs = selection_sbvr(I, I, 4, np.arange(I))
+    y = run_gemv_a8(sb, packed(sb, planes, coeffs), x16)
+    q, s = oracle.act_quantize(x16)
+    y_ref = q.astype(np.float64) * np.repeat(s.astype(np.float64), 128)
+    ulp = fp16_ulp(y_ref.astype(np.float16))
+    bad = np.abs(y - y_ref.astype(np.float16).astype(np.float64)) > ulp
+    assert not bad.any(), (np.flatnonzero(bad)[:8], y[bad][:8], y_ref[bad][:8])
