@@ -316,6 +316,50 @@ def act_decode(planes, s, l: int = ACT_BITS) -> np.ndarray:
     return out
 
 
+# --------------------------------------------------------------------------
+# Coefficient cache + per-group index (Sec. 4.4)
+# --------------------------------------------------------------------------
+
+def gather_coefficients(index, table) -> np.ndarray:
+    """Per-(row, group, plane) coefficients of the coefficient-cache format
+    (Sec. 4.4): the cache holds coefficient sets table[n][0..k-1] and the
+    index names the set each group's k bitvectors use, so
+    c[o][g][i] = table[index[o][g]][i].  uint16 (binary16 bits) [O][G][k]."""
+    index = np.asarray(index)
+    table = np.ascontiguousarray(table, dtype=np.uint16)
+    if index.size and int(index.max()) >= table.shape[0]:
+        raise ValueError("coefficient index past the end of the cache")
+    return table[index.astype(np.int64)]
+
+
+def coefficient_cache(coeffs):
+    """(index uint16 [O][G], table uint16 [N][k]): the distinct coefficient sets
+    of a per-group coefficient tensor, in order of first appearance (row-major
+    over (o, g)), and each group's position in that list.  Lossless; raises if
+    there are more than 65536 distinct sets (16-bit index)."""
+    coeffs = np.ascontiguousarray(coeffs, dtype=np.uint16)
+    O, G, K = coeffs.shape
+    seen = {}
+    rows = []
+    index = np.empty(O * G, dtype=np.uint16)
+    for n, c in enumerate(coeffs.reshape(O * G, K)):
+        key = c.tobytes()
+        pos = seen.get(key)
+        if pos is None:
+            pos = seen[key] = len(rows)
+            if pos > 65535:
+                raise ValueError("more than 65536 distinct coefficient sets")
+            rows.append(c)
+        index[n] = pos
+    return index.reshape(O, G), np.array(rows, dtype=np.uint16).reshape(len(rows), K)
+
+
+def sbvr_gemv_indexed(planes, index, table, x_fp16, rows=None, nthreads: int = 0) -> np.ndarray:
+    """y = W_hat x in binary64 for the coefficient-cache format: the
+    coefficients are gathered through the index, then the exact GEMV."""
+    return sbvr_gemv(planes, gather_coefficients(index, table), x_fp16, rows=rows, nthreads=nthreads)
+
+
 def sbvr_gemv_w4a8(planes: np.ndarray, coeffs: np.ndarray, x_fp16: np.ndarray, rows=None,
                    nthreads: int = 0) -> np.ndarray:
     """The W4A8 decode GEMV reference: y = W_hat x_hat in binary64, with x_hat

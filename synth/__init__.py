@@ -99,6 +99,22 @@ def random_sbvr(O: int, I: int, K: int, seed: int, coeff_sigma: float = 0.01):
     return planes, coeffs.reshape(O, G, K).copy()
 
 
+def random_indexed_sbvr(O: int, I: int, K: int, n_sets: int, seed: int, coeff_sigma: float = 0.01):
+    """Coefficient-cache SBVR tensors drawn directly: planes uint32 [O][G][K][4]
+    (uniform bits), a table uint16 [n_sets][K] of coefficient sets (fp16 of
+    N(0, coeff_sigma^2)) and index uint16 [O][G], uniform in [0, n_sets)
+    (multiply-shift of a raw 32-bit word)."""
+    assert 1 <= n_sets <= 65536
+    G = I // GROUP
+    st = Stream(seed)
+    raw = st.raw((O * G * K * 4 + 1) // 2)
+    planes = raw.view(np.uint32)[: O * G * K * 4].reshape(O, G, K, 4).copy()
+    table = (coeff_sigma * st.normal(n_sets * K)).astype(np.float16).view(np.uint16).reshape(n_sets, K).copy()
+    r32 = st.raw((O * G + 1) // 2).view(np.uint32)[: O * G].astype(np.uint64)
+    index = ((r32 * np.uint64(n_sets)) >> np.uint64(32)).astype(np.uint16).reshape(O, G)
+    return planes, index, table
+
+
 # Decode-projection shapes (out x in) of the Llama-3-8B / 70B decoder layers.
 LLAMA8B = {"q": (4096, 4096), "k": (1024, 4096), "v": (1024, 4096), "o": (4096, 4096),
            "gate": (14336, 4096), "up": (14336, 4096), "down": (4096, 14336)}

@@ -472,3 +472,69 @@ def test_w4a8_reference_is_dense_gemv_of_decoded_operands():
     np.testing.assert_allclose(y, oracle.decompress(planes, coeffs) @ x_hat, rtol=1e-12, atol=1e-15)
     rows = [3, 0, 15]
     np.testing.assert_array_equal(oracle.sbvr_gemv_w4a8(planes, coeffs, x, rows=rows), y[rows])
+
+
+# --------------------------------------------------------------------------
+# Coefficient cache + per-group index (Sec. 4.4)
+# --------------------------------------------------------------------------
+
+def _bit(planes, o, g, i, j):
+    return (int(planes[o, g, i, j // 32]) >> (j % 32)) & 1
+
+
+def test_coefficient_cache_worked_example():
+    """Three groups over two rows, two of them with the same set: the cache
+    holds the two distinct sets in order of first appearance."""
+    h = lambda v: np.float16(v).view(np.uint16)
+    a = [h(0.5), h(-0.25)]
+    b = [h(1.0), h(2.0)]
+    coeffs = np.array([[a, b, a], [b, b, a]], dtype=np.uint16)   # [O=2][G=3][k=2]
+    index, table = oracle.coefficient_cache(coeffs)
+    assert index.tolist() == [[0, 1, 0], [1, 1, 0]]
+    assert table.tolist() == [a, b]
+    assert np.array_equal(oracle.gather_coefficients(index, table), coeffs)
+
+
+def test_gathered_decompression_brute_force():
+    """Decoded weights of the cache format from the definition, element by
+    element: w[o][128 g + j] = sum_i table[index[o][g]][i] * b[o][g][i][j],
+    with exact rational arithmetic (asymmetric O, G, k, N so that a
+    transposed index or table fails)."""
+    O, G, K, N = 3, 2, 3, 5
+    planes, index, table = synth.random_indexed_sbvr(O, G * 128, K, N, seed=12)
+    assert index.shape == (O, G) and table.shape == (N, K)
+    What = oracle.decompress(planes, oracle.gather_coefficients(index, table))
+    tab = [[Fraction(float(np.uint16(v).view(np.float16))) for v in row] for row in table]
+    for o in range(O):
+        for g in range(G):
+            c = tab[int(index[o, g])]
+            for j in range(128):
+                w = sum((c[i] for i in range(K) if _bit(planes, o, g, i, j)), Fraction(0))
+                assert Fraction(What[o, 128 * g + j]) == w
+
+
+def test_coefficient_cache_round_trip_and_distinct_sets():
+    """Per-group coefficients drawn from a small pool of sets: the cache is
+    lossless, its sets are distinct and equal numpy's unique rows, and every
+    index is in range."""
+    rng = np.random.default_rng(3)
+    pool = (rng.standard_normal((37, 4)) * 0.01).astype(np.float16).view(np.uint16)
+    pick = rng.integers(0, 37, size=(64, 9))
+    coeffs = pool[pick]                                  # [64][9][4]
+    index, table = oracle.coefficient_cache(coeffs)
+    assert np.array_equal(oracle.gather_coefficients(index, table), coeffs)
+    assert table.shape[0] == len(np.unique(coeffs.reshape(-1, 4), axis=0))
+    assert len({r.tobytes() for r in table}) == table.shape[0]
+    assert index.dtype == np.uint16 and int(index.max()) < table.shape[0]
+    # first appearance order
+    first = [coeffs.reshape(-1, 4)[int(np.flatnonzero(index.reshape(-1) == n)[0])] for n in range(table.shape[0])]
+    assert np.array_equal(np.array(first), table)
+    with pytest.raises(ValueError):
+        oracle.gather_coefficients(np.array([[table.shape[0]]]), table)
+
+
+def test_indexed_generator_shapes_and_range():
+    planes, index, table = synth.random_indexed_sbvr(7, 384, 2, 65536, seed=1)
+    assert planes.shape == (7, 3, 2, 4) and index.shape == (7, 3) and table.shape == (65536, 2)
+    _, index1, _ = synth.random_indexed_sbvr(7, 384, 2, 1, seed=1)
+    assert np.all(index1 == 0)
