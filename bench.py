@@ -29,6 +29,10 @@ One JSON line is printed:
                 (sbvr_gemm_small_batch), same timing
   w4a8          per projection, batch 1 with the activations converted online
                 to 8-bit SBVR codes (sbvr_gemv_a8), same timing
+  indexed       per projection in the coefficient-cache format (one 16-bit
+                coefficient-set index per group, a table of one set per ten
+                groups): us and GB/s of its own algorithmic bytes, with fp16
+                (sbvr_gemv_indexed) and SBVR-8 activations (sbvr_gemv_indexed_a8)
   low_bit       per projection at k = 2 and 3 planes, same timing
   prefill       per projection: sbvr_decompress to binary16 (us, GB/s of the
                 SBVR bytes read plus the 2 bytes per weight written) and, for
@@ -38,8 +42,9 @@ One JSON line is printed:
                 GEMVs, bounded to ~10 s of work, in the same unit
 
 --traffic-probe runs, eagerly, four launches of every projection shape (fp16
-and W4A8 activations) and an elementwise negation over 256 MiB of float32
-(reads and writes 256 MiB: the counter calibration), for
+and W4A8 activations, and the coefficient-cache format) and an elementwise
+negation over 256 MiB of float32 (reads and writes 256 MiB: the counter
+calibration), for
   rocprofv3 --pmc FETCH_SIZE -- python3 bench.py --traffic-probe   (and WRITE_SIZE);
 --traffic-summary FETCH_CSV WRITE_CSV turns the two counter files into the
 record kept under profiles/.
@@ -155,23 +160,24 @@ def load_traffic(kernel: str):
     return None if k is None else k["bytes_per_launch"]
 
 
-def b1_kernel_instance(O: int, I: int, k: int, a8: bool = False) -> str:
+def b1_kernel_instance(O: int, I: int, k: int, a8: bool = False, ix: bool = False) -> str:
     """Name of the batch-1 kernel instance the library launches for an O x I
     matrix: the streaming kernel (ring depth D, several gblocks per wavefront
     or one) when a row has more than 16 gblocks of 512 elements or the matrix
     has at least 24576 (tile, gblock) blocks (tiles of 16/k rows, 4 at k = 3);
     otherwise the one-shot
     kernel with T tiles per workgroup, the most of 8/4/2/1 that still leaves
-    >= 256 workgroups.  The last template argument selects the W4A8 build
-    (activations converted online to SBVR-8)."""
+    >= 256 workgroups.  The last two template arguments select the W4A8 build
+    (activations converted online to SBVR-8) and the coefficient-cache format."""
     a8 = "true" if a8 else "false"
+    ix = "true" if ix else "false"
     tr = {1: 16, 2: 8}.get(k, 4)  # rows per tile: 16 matrix-core rows of (row, plane)
     n_tiles, n_gblocks = (O + tr - 1) // tr, (I + 511) // 512
     if n_gblocks > 16 or n_tiles * n_gblocks >= 24576:
         multi = n_gblocks > 16
-        return f"gemv_b1s_kernel<{k}, {3 if multi else 2}, {'true' if multi else 'false'}, {a8}>"
+        return f"gemv_b1s_kernel<{k}, {3 if multi else 2}, {'true' if multi else 'false'}, {a8}, {ix}>"
     T = next((t for t in (8, 4, 2) if n_tiles // t >= 256), 1)
-    return f"gemv_b1_kernel<{k}, {T}, {a8}>"
+    return f"gemv_b1_kernel<{k}, {T}, {a8}, {ix}>"
 
 
 ROTATE_BYTES = 320e6  # > 256 MB MALL + 8 x 4 MB L2
@@ -242,6 +248,15 @@ def main():
                 for li in range(L):
                     W, x, y = layers[li][name]
                     sb.gemv_a8(W, x, out=y, stream=stream)
+            for name in PROJ_ORDER:  # coefficient-cache format, one set per ten groups
+                O, I = shapes[name]
+                n_sets = max(1, min(65536, (O * (I // 128) + 9) // 10))
+                planes, index, table = synth.random_indexed_sbvr(O, I, k, n_sets, seed=synth.seed_for(6, 0, 0))
+                Wi = sb.pack_indexed(*(torch.from_numpy(a).to(dev) for a in (planes.view(np.int32), index.view(np.int16),
+                                                                              table.view(np.int16))))
+                x, y = layers[0][name][1], layers[0][name][2]
+                for _ in range(L):
+                    sb.gemv_indexed(Wi, x, out=y, stream=stream)
             # calibration: an elementwise kernel that reads and writes CALIB_BYTES
             src = torch.ones(CALIB_BYTES // 4, dtype=torch.float32, device=dev)
             dst = torch.empty_like(src)
@@ -433,6 +448,40 @@ def main():
             torch.cuda.empty_cache()
         return res
 
+    # ---- coefficient-cache format (index + table of coefficient sets), with
+    # fp16 and SBVR-8 activations; one set per ten groups (a 90 % encoder cache
+    # hit rate), at most 65536 ----
+    def indexed_table(shp, kk, seed_cfg):
+        res = {}
+        for pi, name in enumerate(PROJ_ORDER):
+            O, I = shp[name]
+            same = next((m for m in res if shp[m] == (O, I)), None)
+            if same is not None:
+                res[name] = res[same]
+                continue
+            n_sets = max(1, min(65536, (O * (I // 128) + 9) // 10))
+            planes, index, table = synth.random_indexed_sbvr(O, I, kk, n_sets, seed=synth.seed_for(seed_cfg, 0, pi))
+            p, ix, tb = (torch.from_numpy(a).to(dev) for a in (planes.view(np.int32), index.view(np.int16),
+                                                                  table.view(np.int16)))
+            per = sb.algorithmic_bytes_indexed(O, I, kk, n_sets)
+            ws = [sb.pack_indexed(p, ix, tb) for _ in range(int(np.ceil(ROTATE_BYTES / per)))]
+            x = torch.from_numpy(synth.activations(I, seed=seed_cfg + pi + synth.X_SEED_OFFSET)).to(dev)
+            y = torch.empty(O, dtype=torch.float16, device=dev)
+            entry = {"n_sets": n_sets, "bytes": per, "copies": len(ws)}
+            for tag, a8 in (("fp16", False), ("a8", True)):
+                fn = (lambda W, x, y, stream, a8=a8: sb.gemv_indexed(W, x, out=y, a8=a8, stream=stream))
+                us = launch_us([(fn, (w, x, y)) for w in ws])
+                entry[f"us_{tag}"] = round(us, 3)
+                entry[f"gbps_{tag}"] = round(per / (us * 1e3), 1)
+            res[name] = entry
+            del ws
+            torch.cuda.empty_cache()
+        return res
+
+    indexed = None
+    if not args.quick and k == 4:
+        indexed = indexed_table(shapes, k, 6)
+
     low_bit, other_model = {}, None
     if not args.quick:
         if args.model == "llama3-8b" and k == 4:
@@ -489,6 +538,7 @@ def main():
         "decode_step": decode_step,
         "small_batch": small_batch or None,
         "w4a8": w4a8 or None,
+        "indexed": indexed,
         "low_bit": low_bit or None,
         "prefill": prefill or None,
         ("llama3_70b" if args.model == "llama3-8b" else "llama3_8b"): other_model,

@@ -21,9 +21,9 @@
  *           i.  (The paper stores bitvectors "partitioned into 32-bit
  *           integers" in one contiguous tensor, Sec. 4.4.)
  *   coeffs  uint16_t [O][G][k], binary16 bit patterns of c[o][g][i].  The
- *           per-(row, group, plane) coefficient tensor stands in for the
- *           paper's coefficient cache + index (Sec. 4.4); it holds the same
- *           values.
+ *           per-(row, group, plane) coefficient tensor holds the values the
+ *           paper's coefficient cache + index (Sec. 4.4) decode to; that
+ *           format itself has its own entry points below.
  *
  * DEVICE FORMAT: an opaque, padded repacking of the canonical tensors that
  * the GEMV kernels stream with 128-bit coalesced loads.  It is produced by
@@ -71,7 +71,7 @@ enum sbvr_status {
 const char *sbvr_status_string(int status);
 
 /* Library ABI version (major * 100 + minor); 1.01 adds sbvr_decompress,
- * 1.02 sbvr_gemv_a8. */
+ * 1.02 sbvr_gemv_a8, 1.03 the coefficient-cache format entry points. */
 int sbvr_version(void);
 
 /*
@@ -144,6 +144,62 @@ int sbvr_gemm_small_batch(int O, int I, int k, const void *planes_dev, const voi
 int sbvr_gemv_a8(int O, int I, int k, const void *planes_dev, const void *coeffs_dev,
                  const uint16_t *x, uint16_t *y, void *workspace, size_t ws_bytes,
                  hipStream_t stream);
+
+/*
+ * COEFFICIENT-CACHE FORMAT (Sec. 4.4): the coefficients are stored once per
+ * distinct coefficient set in a cache, and each (row, group) names the set
+ * its k bitvectors use:
+ *   planes  uint32_t [O][G][k][4] as in the canonical format;
+ *   index   uint16_t [O][G]: coefficient-set index of (row o, group g);
+ *   table   uint16_t [n_sets][k]: binary16 coefficient sets, 1 <= n_sets <= 65536;
+ *     c[o][g][i] = table[index[o][g]][i].
+ * Per weight this stores 2 bytes per group instead of 2k (k = 4: 4.125
+ * instead of 4.5 bits per weight) plus the table.  An index >= n_sets is a
+ * caller error; the GEMV then reads zero coefficients for that group (the
+ * table is read through a bounds-checked path), nothing faults.
+ */
+
+/* Device bytes of the index blocks of an O x I matrix with k planes, and of
+ * a table of n_sets coefficient sets (8 bytes per set); 0 if invalid. */
+size_t sbvr_packed_index_bytes(int O, int I, int k);
+size_t sbvr_packed_table_bytes(int n_sets, int k);
+
+/*
+ * Repack the coefficient-cache format into its device format.
+ *   planes_canon uint32 [O][G][k][4], index_canon uint16 [O][G],
+ *   table_canon uint16 [n_sets][k]: inputs (device memory; planes_canon
+ *   16-byte aligned, the others 2).
+ *   planes_dev (sbvr_packed_plane_bytes), index_dev
+ *   (sbvr_packed_index_bytes), table_dev (sbvr_packed_table_bytes): outputs,
+ *   16-byte aligned, every byte written.  Inputs and outputs must not overlap.
+ */
+int sbvr_pack_indexed(int O, int I, int k, int n_sets, const uint32_t *planes_canon,
+                      const uint16_t *index_canon, const uint16_t *table_canon, void *planes_dev,
+                      void *index_dev, void *table_dev, hipStream_t stream);
+
+/* Inverse of sbvr_pack_indexed, bit for bit (roles of inputs and outputs
+ * exchanged). */
+int sbvr_unpack_indexed(int O, int I, int k, int n_sets, const void *planes_dev, const void *index_dev,
+                        const void *table_dev, uint32_t *planes_canon, uint16_t *index_canon,
+                        uint16_t *table_canon, hipStream_t stream);
+
+/*
+ * Batch-1 GEMV on the coefficient-cache format (Sec. 4.4):
+ *     y[o] = fp16_rne( sum_g sum_i table[index[o][g]][i] * sum_j b[o][g][i][j] x[128 g + j] )
+ * i.e. sbvr_gemv with the gathered coefficients.  planes_dev, index_dev,
+ * table_dev from sbvr_pack_indexed; x, y, workspace as sbvr_gemv.
+ */
+int sbvr_gemv_indexed(int O, int I, int k, int n_sets, const void *planes_dev, const void *index_dev,
+                      const void *table_dev, const uint16_t *x, uint16_t *y, void *workspace,
+                      size_t ws_bytes, hipStream_t stream);
+
+/*
+ * The same with SBVR-8 activations (the conversion of sbvr_gemv_a8): the
+ * paper's decode configuration, W4A8 with a coefficient cache (Sec. 4.3-4.4).
+ */
+int sbvr_gemv_indexed_a8(int O, int I, int k, int n_sets, const void *planes_dev, const void *index_dev,
+                         const void *table_dev, const uint16_t *x, uint16_t *y, void *workspace,
+                         size_t ws_bytes, hipStream_t stream);
 
 /*
  * Decompression for the prefill path: the decoded matrix as binary16,

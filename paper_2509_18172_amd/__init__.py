@@ -29,7 +29,8 @@ SBVR_E_HIP = -5
 EXPORTED = (
     "sbvr_status_string", "sbvr_version", "sbvr_packed_plane_bytes", "sbvr_packed_coeff_bytes",
     "sbvr_workspace_bytes", "sbvr_pack", "sbvr_unpack", "sbvr_gemv", "sbvr_gemm_small_batch",
-    "sbvr_decompress", "sbvr_gemv_a8",
+    "sbvr_decompress", "sbvr_gemv_a8", "sbvr_packed_index_bytes", "sbvr_packed_table_bytes",
+    "sbvr_pack_indexed", "sbvr_unpack_indexed", "sbvr_gemv_indexed", "sbvr_gemv_indexed_a8",
 )
 
 
@@ -66,6 +67,12 @@ def _load():
         "sbvr_gemm_small_batch": (i32, [i32, i32, i32, vp, vp, vp, vp, i32, vp, sz, vp]),
         "sbvr_decompress": (i32, [i32, i32, i32, vp, vp, vp, vp]),
         "sbvr_gemv_a8": (i32, [i32, i32, i32, vp, vp, vp, vp, vp, sz, vp]),
+        "sbvr_packed_index_bytes": (sz, [i32, i32, i32]),
+        "sbvr_packed_table_bytes": (sz, [i32, i32]),
+        "sbvr_pack_indexed": (i32, [i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp]),
+        "sbvr_unpack_indexed": (i32, [i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp]),
+        "sbvr_gemv_indexed": (i32, [i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "sbvr_gemv_indexed_a8": (i32, [i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, sz, vp]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -121,6 +128,38 @@ def sbvr_gemm_small_batch(O, I, k, planes_dev, coeffs_dev, X, Y, B, workspace=No
 
 def sbvr_gemv_a8(O, I, k, planes_dev, coeffs_dev, x, y, workspace=None, ws_bytes=0, stream=0) -> int:
     return _lib.sbvr_gemv_a8(O, I, k, planes_dev, coeffs_dev, x, y, workspace, ws_bytes, stream)
+
+
+def sbvr_packed_index_bytes(O: int, I: int, k: int) -> int:
+    return _lib.sbvr_packed_index_bytes(O, I, k)
+
+
+def sbvr_packed_table_bytes(n_sets: int, k: int) -> int:
+    return _lib.sbvr_packed_table_bytes(n_sets, k)
+
+
+def sbvr_pack_indexed(O, I, k, n_sets, planes_canon, index_canon, table_canon, planes_dev, index_dev,
+                      table_dev, stream=0) -> int:
+    return _lib.sbvr_pack_indexed(O, I, k, n_sets, planes_canon, index_canon, table_canon, planes_dev,
+                                  index_dev, table_dev, stream)
+
+
+def sbvr_unpack_indexed(O, I, k, n_sets, planes_dev, index_dev, table_dev, planes_canon, index_canon,
+                        table_canon, stream=0) -> int:
+    return _lib.sbvr_unpack_indexed(O, I, k, n_sets, planes_dev, index_dev, table_dev, planes_canon,
+                                    index_canon, table_canon, stream)
+
+
+def sbvr_gemv_indexed(O, I, k, n_sets, planes_dev, index_dev, table_dev, x, y, workspace=None, ws_bytes=0,
+                      stream=0) -> int:
+    return _lib.sbvr_gemv_indexed(O, I, k, n_sets, planes_dev, index_dev, table_dev, x, y, workspace,
+                                  ws_bytes, stream)
+
+
+def sbvr_gemv_indexed_a8(O, I, k, n_sets, planes_dev, index_dev, table_dev, x, y, workspace=None,
+                         ws_bytes=0, stream=0) -> int:
+    return _lib.sbvr_gemv_indexed_a8(O, I, k, n_sets, planes_dev, index_dev, table_dev, x, y, workspace,
+                                     ws_bytes, stream)
 
 
 def sbvr_decompress(O, I, k, planes_dev, coeffs_dev, W, stream=0) -> int:
@@ -227,6 +266,70 @@ def gemv_a8(W: PackedWeight, x, out=None, stream=None):
     return y
 
 
+class IndexedWeight:
+    """An O x I SBVR matrix in the coefficient-cache format (planes, index
+    blocks, table of n_sets coefficient sets), resident in device memory in
+    the library's device format."""
+
+    def __init__(self, O: int, I: int, k: int, n_sets: int, planes, index, table):
+        self.O, self.I, self.k, self.n_sets = O, I, k, n_sets
+        self.planes, self.index, self.table = planes, index, table
+
+    @property
+    def nbytes(self) -> int:
+        return self.planes.numel() + self.index.numel() + self.table.numel()
+
+
+def pack_indexed(planes_canon, index_canon, table_canon, stream=None) -> IndexedWeight:
+    """Repack canonical device tensors (int32/uint32 [O][G][k][4], int16/uint16
+    [O][G] index, int16/uint16 [n_sets][k] table) into an IndexedWeight."""
+    torch = _torch()
+    O, G, k, four = planes_canon.shape
+    n_sets = table_canon.shape[0]
+    assert four == 4 and tuple(index_canon.shape) == (O, G) and tuple(table_canon.shape) == (n_sets, k)
+    for t in (planes_canon, index_canon, table_canon):
+        assert t.is_contiguous()
+    assert planes_canon.element_size() == 4 and index_canon.element_size() == 2 and table_canon.element_size() == 2
+    I = G * GROUP
+    pb, ib, tb = sbvr_packed_plane_bytes(O, I, k), sbvr_packed_index_bytes(O, I, k), sbvr_packed_table_bytes(n_sets, k)
+    if pb == 0 or ib == 0 or tb == 0:
+        raise SBVRError(SBVR_E_INVALID_ARG, f"shape {O}x{I} k={k} n_sets={n_sets}")
+    dev = planes_canon.device
+    W = IndexedWeight(O, I, k, n_sets, torch.empty(pb, dtype=torch.uint8, device=dev),
+                      torch.empty(ib, dtype=torch.uint8, device=dev), torch.empty(tb, dtype=torch.uint8, device=dev))
+    _check(sbvr_pack_indexed(O, I, k, n_sets, planes_canon.data_ptr(), index_canon.data_ptr(), table_canon.data_ptr(),
+                             W.planes.data_ptr(), W.index.data_ptr(), W.table.data_ptr(), _stream(stream)),
+           "sbvr_pack_indexed")
+    return W
+
+
+def unpack_indexed(W: IndexedWeight, stream=None):
+    """Canonical (planes int32 [O][G][k][4], index int16 [O][G], table int16
+    [n_sets][k]) device tensors."""
+    torch = _torch()
+    G = W.I // GROUP
+    dev = W.planes.device
+    planes = torch.empty((W.O, G, W.k, 4), dtype=torch.int32, device=dev)
+    index = torch.empty((W.O, G), dtype=torch.int16, device=dev)
+    table = torch.empty((W.n_sets, W.k), dtype=torch.int16, device=dev)
+    _check(sbvr_unpack_indexed(W.O, W.I, W.k, W.n_sets, W.planes.data_ptr(), W.index.data_ptr(),
+                               W.table.data_ptr(), planes.data_ptr(), index.data_ptr(), table.data_ptr(),
+                               _stream(stream)), "sbvr_unpack_indexed")
+    return planes, index, table
+
+
+def gemv_indexed(W: IndexedWeight, x, out=None, a8: bool = False, stream=None):
+    """y = SBVR(W) x on the coefficient-cache format, x fp16 [I]; with
+    a8=True the activations are converted online to SBVR-8 (W4A8)."""
+    torch = _torch()
+    assert x.dtype == torch.float16 and x.is_contiguous() and x.shape == (W.I,)
+    y = torch.empty(W.O, dtype=torch.float16, device=x.device) if out is None else out
+    fn, name = (sbvr_gemv_indexed_a8, "sbvr_gemv_indexed_a8") if a8 else (sbvr_gemv_indexed, "sbvr_gemv_indexed")
+    _check(fn(W.O, W.I, W.k, W.n_sets, W.planes.data_ptr(), W.index.data_ptr(), W.table.data_ptr(),
+              x.data_ptr(), y.data_ptr(), None, 0, _stream(stream)), name)
+    return y
+
+
 def decompress(W: PackedWeight, out=None, stream=None):
     """The decoded matrix as fp16 [O][I] (prefill path)."""
     torch = _torch()
@@ -235,6 +338,13 @@ def decompress(W: PackedWeight, out=None, stream=None):
     _check(sbvr_decompress(W.O, W.I, W.k, W.planes.data_ptr(), W.coeffs.data_ptr(), M.data_ptr(),
                            _stream(stream)), "sbvr_decompress")
     return M
+
+
+def algorithmic_bytes_indexed(O: int, I: int, k: int, n_sets: int) -> int:
+    """Bytes per call in the coefficient-cache format: planes k*O*I/8, one
+    2-byte index per (row, group) 2*O*I/128, the coefficient sets 2*k*n_sets,
+    activations 2*I and outputs 2*O."""
+    return k * O * I // 8 + 2 * O * I // GROUP + 2 * k * n_sets + 2 * I + 2 * O
 
 
 def algorithmic_bytes(O: int, I: int, k: int, B: int = 1) -> int:

@@ -23,18 +23,39 @@ def library_path() -> str:
     return os.path.join(HERE, "_lib", "libsbvr.so")
 
 
-def build(verbose: bool = False, out: str | None = None, defines=()) -> str:
+def build(verbose: bool = False, out: str | None = None, defines=(), jobs: int = 0) -> str:
+    """Compile every source to an object (in parallel), then link libsbvr.so."""
+    from concurrent.futures import ThreadPoolExecutor
+
     out = out or library_path()
     os.makedirs(os.path.dirname(out), exist_ok=True)
-    tmp = out + ".tmp%d" % os.getpid()
-    cmd = [HIPCC, *FLAGS, *("-D" + d for d in defines), "-I", os.path.join(ROOT, "include"),
-           "-I", os.path.join(HERE, "csrc"), *SOURCES, "-o", tmp]
-    if verbose:
-        print(" ".join(cmd))
-    r = subprocess.run(cmd, capture_output=True, text=True)
-    if r.returncode != 0:
-        raise RuntimeError("hipcc failed:\n" + r.stdout + r.stderr)
-    os.replace(tmp, out)
+    objdir = os.path.join(os.path.dirname(out), "obj.%d" % os.getpid())
+    os.makedirs(objdir, exist_ok=True)
+    common = [*FLAGS, *("-D" + d for d in defines), "-I", os.path.join(ROOT, "include"),
+              "-I", os.path.join(HERE, "csrc")]
+
+    def run(cmd):
+        if verbose:
+            print(" ".join(cmd))
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError("hipcc failed:\n" + " ".join(cmd) + "\n" + r.stdout + r.stderr)
+
+    objs = [os.path.join(objdir, os.path.basename(src) + ".o") for src in SOURCES]
+    compile_flags = [f for f in common if f != "-shared"]
+    jobs = jobs or min(len(SOURCES), os.cpu_count() or 1, 8)
+    try:
+        with ThreadPoolExecutor(max_workers=jobs) as ex:
+            list(ex.map(run, [[HIPCC, *compile_flags, "-c", src, "-o", obj] for src, obj in zip(SOURCES, objs)]))
+        tmp = out + ".tmp%d" % os.getpid()
+        run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp])
+        os.replace(tmp, out)
+    finally:
+        for o in objs:
+            if os.path.exists(o):
+                os.remove(o)
+        if os.path.isdir(objdir):
+            os.rmdir(objdir)
     return out
 
 

@@ -55,6 +55,48 @@ int check_gemv(int O, int I, int k, const void *planes_dev, const void *coeffs_d
     return SBVR_OK;
 }
 
+int check_sets(int n_sets) { return n_sets >= 1 && n_sets <= MAX_SETS ? SBVR_OK : SBVR_E_INVALID_ARG; }
+
+int check_indexed_gemv(int O, int I, int k, int n_sets, const void *planes_dev, const void *index_dev,
+                       const void *table_dev, const uint16_t *x, const uint16_t *y, size_t ws_bytes)
+{
+    int st = check_shape(O, I, k);
+    if (st != SBVR_OK)
+        return st;
+    if ((st = check_sets(n_sets)) != SBVR_OK)
+        return st;
+    if (!planes_dev || !index_dev || !table_dev || !x || !y)
+        return SBVR_E_INVALID_ARG;
+    if (!aligned(planes_dev, 16) || !aligned(index_dev, 16) || !aligned(table_dev, 16) || !aligned(x, 16) ||
+        !aligned(y, 2))
+        return SBVR_E_ALIGNMENT;
+    if (ws_bytes < sbvr_workspace_bytes(O, I, k, 1))
+        return SBVR_E_WORKSPACE;
+    return SBVR_OK;
+}
+
+int check_indexed_repack(int O, int I, int k, int n_sets, const void *planes_canon, const void *index_canon,
+                         const void *table_canon, const void *planes_dev, const void *index_dev,
+                         const void *table_dev)
+{
+    int st = check_shape(O, I, k);
+    if (st != SBVR_OK)
+        return st;
+    if ((st = check_sets(n_sets)) != SBVR_OK)
+        return st;
+    if (!planes_canon || !index_canon || !table_canon || !planes_dev || !index_dev || !table_dev)
+        return SBVR_E_INVALID_ARG;
+    if (!aligned(planes_canon, 16) || !aligned(index_canon, 2) || !aligned(table_canon, 2) ||
+        !aligned(planes_dev, 16) || !aligned(index_dev, 16) || !aligned(table_dev, 16))
+        return SBVR_E_ALIGNMENT;
+    return SBVR_OK;
+}
+
+WeightRef indexed_weights(const void *planes, const void *index, const void *table, int n_sets)
+{
+    return WeightRef{planes, nullptr, index, table, n_sets};
+}
+
 }  // namespace
 
 extern "C" {
@@ -72,7 +114,7 @@ const char *sbvr_status_string(int status)
     }
 }
 
-int sbvr_version(void) { return 102; }
+int sbvr_version(void) { return 103; }
 
 size_t sbvr_packed_plane_bytes(int O, int I, int k)
 {
@@ -118,7 +160,7 @@ int sbvr_gemv(int O, int I, int k, const void *planes_dev, const void *coeffs_de
     int st = check_gemv(O, I, k, planes_dev, coeffs_dev, x, y, 1, ws_bytes);
     if (st != SBVR_OK)
         return st;
-    return launch_gemv_b1(make_dims(O, I, k), planes_dev, coeffs_dev, x, y, false, stream);
+    return launch_gemv_b1(make_dims(O, I, k), per_group_weights(planes_dev, coeffs_dev), x, y, false, stream);
 }
 
 int sbvr_gemm_small_batch(int O, int I, int k, const void *planes_dev, const void *coeffs_dev,
@@ -131,7 +173,7 @@ int sbvr_gemm_small_batch(int O, int I, int k, const void *planes_dev, const voi
         return st;
     const Dims d = make_dims(O, I, k);
     if (B == 1)
-        return launch_gemv_b1(d, planes_dev, coeffs_dev, X, Y, false, stream);
+        return launch_gemv_b1(d, per_group_weights(planes_dev, coeffs_dev), X, Y, false, stream);
     return launch_gemm_sbs(d, planes_dev, coeffs_dev, X, Y, B, stream);
 }
 
@@ -142,7 +184,65 @@ int sbvr_gemv_a8(int O, int I, int k, const void *planes_dev, const void *coeffs
     int st = check_gemv(O, I, k, planes_dev, coeffs_dev, x, y, 1, ws_bytes);
     if (st != SBVR_OK)
         return st;
-    return launch_gemv_b1(make_dims(O, I, k), planes_dev, coeffs_dev, x, y, true, stream);
+    return launch_gemv_b1(make_dims(O, I, k), per_group_weights(planes_dev, coeffs_dev), x, y, true, stream);
+}
+
+size_t sbvr_packed_index_bytes(int O, int I, int k)
+{
+    return check_shape(O, I, k) == SBVR_OK ? index_bytes(make_dims(O, I, k)) : 0;
+}
+
+size_t sbvr_packed_table_bytes(int n_sets, int k)
+{
+    return check_sets(n_sets) == SBVR_OK && k >= 1 && k <= MAX_K ? table_bytes(n_sets) : 0;
+}
+
+int sbvr_pack_indexed(int O, int I, int k, int n_sets, const uint32_t *planes_canon,
+                      const uint16_t *index_canon, const uint16_t *table_canon, void *planes_dev,
+                      void *index_dev, void *table_dev, hipStream_t stream)
+{
+    int st = check_indexed_repack(O, I, k, n_sets, planes_canon, index_canon, table_canon, planes_dev,
+                                  index_dev, table_dev);
+    if (st != SBVR_OK)
+        return st;
+    return launch_pack_indexed(make_dims(O, I, k), n_sets, planes_canon, index_canon, table_canon,
+                               planes_dev, index_dev, table_dev, stream);
+}
+
+int sbvr_unpack_indexed(int O, int I, int k, int n_sets, const void *planes_dev, const void *index_dev,
+                        const void *table_dev, uint32_t *planes_canon, uint16_t *index_canon,
+                        uint16_t *table_canon, hipStream_t stream)
+{
+    int st = check_indexed_repack(O, I, k, n_sets, planes_canon, index_canon, table_canon, planes_dev,
+                                  index_dev, table_dev);
+    if (st != SBVR_OK)
+        return st;
+    return launch_unpack_indexed(make_dims(O, I, k), n_sets, planes_dev, index_dev, table_dev, planes_canon,
+                                 index_canon, table_canon, stream);
+}
+
+int sbvr_gemv_indexed(int O, int I, int k, int n_sets, const void *planes_dev, const void *index_dev,
+                      const void *table_dev, const uint16_t *x, uint16_t *y, void *workspace,
+                      size_t ws_bytes, hipStream_t stream)
+{
+    (void)workspace;
+    int st = check_indexed_gemv(O, I, k, n_sets, planes_dev, index_dev, table_dev, x, y, ws_bytes);
+    if (st != SBVR_OK)
+        return st;
+    return launch_gemv_b1(make_dims(O, I, k), indexed_weights(planes_dev, index_dev, table_dev, n_sets), x, y,
+                          false, stream);
+}
+
+int sbvr_gemv_indexed_a8(int O, int I, int k, int n_sets, const void *planes_dev, const void *index_dev,
+                         const void *table_dev, const uint16_t *x, uint16_t *y, void *workspace,
+                         size_t ws_bytes, hipStream_t stream)
+{
+    (void)workspace;
+    int st = check_indexed_gemv(O, I, k, n_sets, planes_dev, index_dev, table_dev, x, y, ws_bytes);
+    if (st != SBVR_OK)
+        return st;
+    return launch_gemv_b1(make_dims(O, I, k), indexed_weights(planes_dev, index_dev, table_dev, n_sets), x, y,
+                          true, stream);
 }
 
 int sbvr_decompress(int O, int I, int k, const void *planes_dev, const void *coeffs_dev, uint16_t *W,

@@ -20,6 +20,8 @@
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "layout.h"
 
 namespace sbvr {
@@ -448,13 +450,59 @@ __device__ __forceinline__ uint2 buf_coefs4(buf_rsrc r, unsigned off)
     }
 }
 
+// Coefficient-cache format: a lane's NP = TR / 4 index entries (NP = 1, 2:
+// one dword; NP = 4: two) and the gather of its four D rows' coefficients
+// from the cache (TABLE_STRIDE entries per set).  The cache is read through a
+// descriptor bounded by the number of sets: an index past the end reads zero
+// coefficients instead of faulting.
+template <int K>
+struct IxLane {
+    typedef typename std::conditional<(index_per_lane(K) == 4), uint2, uint32_t>::type type;
+};
+
+template <int K>
+__device__ __forceinline__ typename IxLane<K>::type buf_index(buf_rsrc r, unsigned off)
+{
+    if constexpr (index_per_lane(K) == 4) {
+        const v2u_t v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, BUF_NT);
+        return make_uint2(v[0], v[1]);
+    } else if constexpr (index_per_lane(K) == 2) {
+        return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, BUF_NT);
+    } else {
+        return (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(r, off, 0, BUF_NT);
+    }
+}
+
+template <int K>
+__device__ __forceinline__ uint2 table_coefs4(buf_rsrc t, typename IxLane<K>::type ix)
+{
+    constexpr unsigned SET_B = TABLE_STRIDE * 2;
+    if constexpr (index_per_lane(K) == 4) {  // four rows, plane 0 of each
+        const unsigned c0 = __builtin_amdgcn_raw_buffer_load_b16(t, (ix.x & 0xffffu) * SET_B, 0, 0);
+        const unsigned c1 = __builtin_amdgcn_raw_buffer_load_b16(t, (ix.x >> 16) * SET_B, 0, 0);
+        const unsigned c2 = __builtin_amdgcn_raw_buffer_load_b16(t, (ix.y & 0xffffu) * SET_B, 0, 0);
+        const unsigned c3 = __builtin_amdgcn_raw_buffer_load_b16(t, (ix.y >> 16) * SET_B, 0, 0);
+        return make_uint2(c0 | (c1 << 16), c2 | (c3 << 16));
+    } else if constexpr (index_per_lane(K) == 2) {  // two rows, planes 0 and 1
+        const unsigned v0 = __builtin_amdgcn_raw_buffer_load_b32(t, (ix & 0xffffu) * SET_B, 0, 0);
+        const unsigned v1 = __builtin_amdgcn_raw_buffer_load_b32(t, (ix >> 16) * SET_B, 0, 0);
+        return make_uint2(v0, v1);
+    } else {  // one row, planes 0..3 (plane 3 of K = 3 is the zero padding)
+        const v2u_t v = __builtin_amdgcn_raw_buffer_load_b64(t, ix * SET_B, 0, 0);
+        return make_uint2(v[0], v[1]);
+    }
+}
+
 struct GemvArgs {
     const uint4 *planes;    // device plane blocks
-    const uint16_t *coeffs; // device coefficient blocks
+    const uint16_t *coeffs; // device coefficient blocks (per-group format)
     const uint16_t *x;      // binary16 [B][I]
     uint16_t *y;            // binary16 [B][O]
     int O, I, k, n_tiles, n_gblocks, gpw, B;
     int tpw;                // tiles per workgroup (streaming kernel)
+    const uint16_t *index;  // device index blocks (coefficient-cache format)
+    const uint16_t *table;  // coefficient sets [n_sets][TABLE_STRIDE]
+    int n_sets;
 };
 
 }  // namespace sbvr

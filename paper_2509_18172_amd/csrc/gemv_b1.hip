@@ -34,10 +34,13 @@ template <int K, int T>
 struct B1Regs {
     uint4 p[T];  // plane words of each tile (this lane's 16 bytes)
     uint2 c[T];  // the coefficients of this lane's four D rows, each tile
+    typename IxLane<K>::type ix[T];  // coefficient-cache format: their set indices
     uint4 x;     // this lane's 8 activations
 };
 
-template <int K, int T, bool A8>
+// A8: activations converted online to SBVR-8.  IX: coefficient-cache format
+// (index blocks + table of coefficient sets) instead of per-group coefficients.
+template <int K, int T, bool A8, bool IX>
 __global__ void __launch_bounds__(1024) gemv_b1_kernel(GemvArgs a)
 {
     extern __shared__ __align__(16) unsigned char smem[];
@@ -67,17 +70,34 @@ __global__ void __launch_bounds__(1024) gemv_b1_kernel(GemvArgs a)
     for (int t = 0; t < T; ++t)
         tblk[t] = min(tile0 + t, a.n_tiles - 1) * a.n_gblocks;
 
+    // coefficient-cache format: index blocks and the table, through
+    // descriptors (the table's bounds the set count)
+    constexpr unsigned IBLK_B = GB * TR * 2;
+    const unsigned i_lane = (unsigned)(((lane >> 4) * GB + ((lane & 15) >> 2)) * index_per_lane(K)) * 2u;
+    buf_rsrc irs, trs;
+    if constexpr (IX) {
+        irs = make_rsrc(a.index, (unsigned)((size_t)a.n_tiles * a.n_gblocks * IBLK_B));
+        trs = make_rsrc(a.table, (unsigned)a.n_sets * (TABLE_STRIDE * 2));
+    }
+
     auto fetch = [&](B1Regs<K, T> &R) {
         // activations first; lanes past I (ragged end) read a valid address
         // and are zeroed before use
         R.x = *(const uint4 *)(a.x + min(gb * (GB * GROUP) + lane * 8, a.I - 8));
         __builtin_amdgcn_sched_barrier(0);  // the operand build waits only for x
+        if constexpr (IX) {  // set indices before the planes: their gathers wait only for them
+#pragma unroll
+            for (int t = 0; t < T; ++t)
+                R.ix[t] = buf_index<K>(irs, (unsigned)(tblk[t] + gb) * IBLK_B + i_lane);
+            __builtin_amdgcn_sched_barrier(0);
+        }
 #pragma unroll
         for (int t = 0; t < T; ++t) {
             const size_t blk = (size_t)(tblk[t] + gb);
             const uint4 v = load_nt16(a.planes + blk * PBLK + a_off);
             R.p[t] = a_ok ? v : make_uint4(0u, 0u, 0u, 0u);
-            R.c[t] = load_coefs4<K>(a.coeffs + blk * CBLK + c_off);
+            if constexpr (!IX)
+                R.c[t] = load_coefs4<K>(a.coeffs + blk * CBLK + c_off);
         }
     };
 
@@ -150,6 +170,12 @@ __global__ void __launch_bounds__(1024) gemv_b1_kernel(GemvArgs a)
         B1Regs<K, T> R;
         fetch(R);
         __builtin_amdgcn_sched_barrier(0);  // all loads issued before arithmetic
+        if constexpr (IX) {  // coefficient sets, gathered while the operands are built
+#pragma unroll
+            for (int t = 0; t < T; ++t)
+                R.c[t] = table_coefs4<K>(trs, R.ix[t]);
+            __builtin_amdgcn_sched_barrier(0);
+        }
         v8i Bq[4];
         const float inv_scale = operands(R, Bq);
         __builtin_amdgcn_sched_barrier(0);
@@ -214,21 +240,23 @@ static int choose_b1_tiles(const Dims &d)
 #endif
 }
 
-template <int K, bool A8>
+template <int K, bool A8, bool IX>
 static const void *b1_kernel_for(int T)
 {
     switch (T) {
-    case 8: return (const void *)gemv_b1_kernel<K, 8, A8>;
-    case 4: return (const void *)gemv_b1_kernel<K, 4, A8>;
-    case 2: return (const void *)gemv_b1_kernel<K, 2, A8>;
-    default: return (const void *)gemv_b1_kernel<K, 1, A8>;
+    case 8: return (const void *)gemv_b1_kernel<K, 8, A8, IX>;
+    case 4: return (const void *)gemv_b1_kernel<K, 4, A8, IX>;
+    case 2: return (const void *)gemv_b1_kernel<K, 2, A8, IX>;
+    default: return (const void *)gemv_b1_kernel<K, 1, A8, IX>;
     }
 }
 
 template <int K>
-static const void *b1_kernel_for(int T, bool a8)
+static const void *b1_kernel_for(int T, bool a8, bool ix)
 {
-    return a8 ? b1_kernel_for<K, true>(T) : b1_kernel_for<K, false>(T);
+    if (ix)
+        return a8 ? b1_kernel_for<K, true, true>(T) : b1_kernel_for<K, false, true>(T);
+    return a8 ? b1_kernel_for<K, true, false>(T) : b1_kernel_for<K, false, false>(T);
 }
 
 // Matrices with more (tile, gblock) blocks than this, or more than 16
@@ -237,21 +265,23 @@ static const void *b1_kernel_for(int T, bool a8)
 #define SBVR_B1S_MIN_BLOCKS 24576
 #endif
 
-int launch_gemv_b1(const Dims &d, const void *planes_dev, const void *coeffs_dev,
-                   const uint16_t *x, uint16_t *y, bool a8, hipStream_t stream)
+int launch_gemv_b1(const Dims &d, const WeightRef &w, const uint16_t *x, uint16_t *y, bool a8,
+                   hipStream_t stream)
 {
     if (d.n_gblocks > B1_MAX_WAVES || (long)d.n_tiles * d.n_gblocks >= SBVR_B1S_MIN_BLOCKS)
-        return launch_gemv_b1s(d, planes_dev, coeffs_dev, x, y, a8, stream);
+        return launch_gemv_b1s(d, w, x, y, a8, stream);
     const int T = choose_b1_tiles(d);
     const int waves = d.n_gblocks;
-    GemvArgs a = {(const uint4 *)planes_dev, (const uint16_t *)coeffs_dev, x, y, d.O, d.I, d.k,
-                  d.n_tiles, d.n_gblocks, 1, 1, 0};
+    GemvArgs a = {(const uint4 *)w.planes, (const uint16_t *)w.coeffs, x, y, d.O, d.I, d.k,
+                  d.n_tiles, d.n_gblocks, 1, 1, 0, (const uint16_t *)w.index, (const uint16_t *)w.table,
+                  w.n_sets};
+    const bool ix = w.index != nullptr;
     const int grid = (d.n_tiles + T - 1) / T;
     const size_t lds = (size_t)waves * B1_WAVE_LDS + (size_t)waves * T * d.tr * 4;
-    const void *fn = d.k == 4   ? b1_kernel_for<4>(T, a8)
-                     : d.k == 3 ? b1_kernel_for<3>(T, a8)
-                     : d.k == 2 ? b1_kernel_for<2>(T, a8)
-                                : b1_kernel_for<1>(T, a8);
+    const void *fn = d.k == 4   ? b1_kernel_for<4>(T, a8, ix)
+                     : d.k == 3 ? b1_kernel_for<3>(T, a8, ix)
+                     : d.k == 2 ? b1_kernel_for<2>(T, a8, ix)
+                                : b1_kernel_for<1>(T, a8, ix);
     void *args[] = {&a};
     return launch_kernel(fn, dim3(grid), dim3(64 * waves), lds, stream, args);
 }

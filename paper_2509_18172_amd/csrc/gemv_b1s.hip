@@ -52,7 +52,13 @@ constexpr int B1S_WAVE_LDS = 2048;  // per wavefront: [q][s][l][32 B]
 #define SBVR_B1S_GROUPS_MULTI 256
 #endif
 
-template <int K, int D, bool MULTI, bool A8>
+// A8: activations converted online to SBVR-8.  IX: coefficient-cache format;
+// each item's coefficient sets are then gathered through its index block, and
+// the ring runs in three stages: the index block of item m+2D is loaded when
+// item m is consumed, and the sets of item m+D are gathered then from the
+// index block loaded D items earlier, so neither the index load nor the gather
+// waits on anything issued less than D items before.
+template <int K, int D, bool MULTI, bool A8, bool IX>
 __global__ void __launch_bounds__(1024) gemv_b1s_kernel(GemvArgs a)
 {
     extern __shared__ __align__(16) unsigned char smem[];
@@ -82,30 +88,63 @@ __global__ void __launch_bounds__(1024) gemv_b1s_kernel(GemvArgs a)
     const buf_rsrc prs = make_rsrc((const unsigned char *)a.planes + blk0 * PBLK_B, (unsigned)ntl * pstep);
     const buf_rsrc crs = make_rsrc((const unsigned char *)a.coeffs + blk0 * CBLK_B, (unsigned)ntl * cstep);
 
-    // Prefetch cursor (wavefront-uniform): next item whose loads are issued.
-    int pf_i = 0, pf_gb = wv;
-    uint4 P[D];
-    uint2 C[D];
-    auto issue = [&](int j) {
-        unsigned po, co;
+    // coefficient-cache format: index blocks (same block order) and the table
+    constexpr unsigned IBLK_B = GB * TR * 2;  // bytes per index block
+    const unsigned istep = (unsigned)a.n_gblocks * IBLK_B;
+    const unsigned i_lane = (unsigned)(((lane >> 4) * GB + ((lane & 15) >> 2)) * index_per_lane(K)) * 2u;
+    buf_rsrc irs, trs;
+    if constexpr (IX) {
+        irs = make_rsrc((const unsigned char *)a.index + blk0 * IBLK_B, (unsigned)ntl * istep);
+        trs = make_rsrc(a.table, (unsigned)a.n_sets * (TABLE_STRIDE * 2));
+    }
+
+    // Cursor (wavefront-uniform) over the wavefront's items: returns the item's
+    // block offset in units of blocks-per-tile (tile i * n_gblocks + gblock) or
+    // -1 past the end (MULTI; without MULTI, items past the last tile fall
+    // outside the descriptors' range by themselves).
+    auto advance = [&](int &ci, int &cg, unsigned &po, unsigned &co, unsigned &io) {
         if constexpr (MULTI) {
-            po = co = BUF_OOB;
-            if (pf_gb < a.n_gblocks) {
-                po = (unsigned)pf_i * pstep + (unsigned)pf_gb * PBLK_B;
-                co = (unsigned)pf_i * cstep + (unsigned)pf_gb * CBLK_B;
+            po = co = io = BUF_OOB;
+            if (cg < a.n_gblocks) {
+                po = (unsigned)ci * pstep + (unsigned)cg * PBLK_B;
+                co = (unsigned)ci * cstep + (unsigned)cg * CBLK_B;
+                io = (unsigned)ci * istep + (unsigned)cg * IBLK_B;
             }
-            if (++pf_i == ntl) {
-                pf_i = 0;
-                pf_gb += nw;
+            if (++ci == ntl) {
+                ci = 0;
+                cg += nw;
             }
         } else {
-            // items past the last tile fall outside the descriptors' range
-            po = (unsigned)pf_i * pstep + (unsigned)wv * PBLK_B;
-            co = (unsigned)pf_i * cstep + (unsigned)wv * CBLK_B;
-            ++pf_i;
+            po = (unsigned)ci * pstep + (unsigned)wv * PBLK_B;
+            co = (unsigned)ci * cstep + (unsigned)wv * CBLK_B;
+            io = (unsigned)ci * istep + (unsigned)wv * IBLK_B;
+            ++ci;
         }
+    };
+    // Prefetch cursors: next item whose planes (and coefficients) are loaded,
+    // and, for IX, next item whose index block is loaded (D items further).
+    int pf_i = 0, pf_gb = wv, ix_i = 0, ix_gb = wv;
+    uint4 P[D];
+    uint2 C[D];
+    typename IxLane<K>::type IXr[D];
+    auto load_ix = [&](int j) {
+        unsigned po, co, io;
+        advance(ix_i, ix_gb, po, co, io);
+        IXr[j] = buf_index<K>(irs, i_lane + io);
+    };
+    auto gather = [&](int j) { C[j] = table_coefs4<K>(trs, IXr[j]); };
+    auto issue = [&](int j) {
+        unsigned po, co, io;
+        advance(pf_i, pf_gb, po, co, io);
         P[j] = buf_load16(prs, p_lane + po);
-        C[j] = buf_coefs4<K>(crs, c_lane + co);
+        if constexpr (IX) {
+            __builtin_amdgcn_sched_barrier(0);
+            gather(j);  // the sets of this item (index loaded D items ago)
+            __builtin_amdgcn_sched_barrier(0);
+            load_ix(j);                           // index block D items further on
+        } else {
+            C[j] = buf_coefs4<K>(crs, c_lane + co);
+        }
     };
     // Activations of a gblock; lanes past I (ragged end) read a valid address
     // and are zeroed when the operand is built.
@@ -117,9 +156,35 @@ __global__ void __launch_bounds__(1024) gemv_b1s_kernel(GemvArgs a)
     // x first: the operand build waits only for it, not for the ring loads
     uint4 x_cur = load_x(wv);
     __builtin_amdgcn_sched_barrier(0);
+    if constexpr (IX) {
+        // first D index blocks, then the first D items' planes; only then the
+        // gathers that wait for those index blocks (and the next D index blocks)
 #pragma unroll
-    for (int j = 0; j < D; ++j)
-        issue(j);
+        for (int j = 0; j < D; ++j)
+            load_ix(j);
+#pragma unroll
+        for (int j = 0; j < D; ++j) {
+            unsigned po, co, io;
+            advance(pf_i, pf_gb, po, co, io);
+            P[j] = buf_load16(prs, p_lane + po);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int j = 0; j < D; ++j) {
+            gather(j);
+            __builtin_amdgcn_sched_barrier(0);
+            load_ix(j);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    } else {
+        // in the loop's order (planes, coefficients per item): the compiler's
+        // counted waits at the loop head then match on both incoming paths
+#pragma unroll
+        for (int j = 0; j < D; ++j) {
+            issue(j);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
     uint4 x_next;
     if constexpr (MULTI)
         x_next = load_x(wv + nw);
@@ -220,35 +285,39 @@ __global__ void __launch_bounds__(1024) gemv_b1s_kernel(GemvArgs a)
     }
 }
 
-template <int K, bool A8>
+template <int K, bool A8, bool IX>
 static const void *b1s_kernel_for(bool multi)
 {
-    return multi ? (const void *)gemv_b1s_kernel<K, SBVR_B1S_DEPTH_MULTI, true, A8>
-                 : (const void *)gemv_b1s_kernel<K, SBVR_B1S_DEPTH, false, A8>;
+    return multi ? (const void *)gemv_b1s_kernel<K, SBVR_B1S_DEPTH_MULTI, true, A8, IX>
+                 : (const void *)gemv_b1s_kernel<K, SBVR_B1S_DEPTH, false, A8, IX>;
 }
 
 template <int K>
-static const void *b1s_kernel_for(bool multi, bool a8)
+static const void *b1s_kernel_for(bool multi, bool a8, bool ix)
 {
-    return a8 ? b1s_kernel_for<K, true>(multi) : b1s_kernel_for<K, false>(multi);
+    if (ix)
+        return a8 ? b1s_kernel_for<K, true, true>(multi) : b1s_kernel_for<K, false, true>(multi);
+    return a8 ? b1s_kernel_for<K, true, false>(multi) : b1s_kernel_for<K, false, false>(multi);
 }
 
-int launch_gemv_b1s(const Dims &d, const void *planes_dev, const void *coeffs_dev,
-                    const uint16_t *x, uint16_t *y, bool a8, hipStream_t stream)
+int launch_gemv_b1s(const Dims &d, const WeightRef &w, const uint16_t *x, uint16_t *y, bool a8,
+                    hipStream_t stream)
 {
     const int gpw = (d.n_gblocks + SBVR_B1S_MAX_WAVES - 1) / SBVR_B1S_MAX_WAVES;
     const int waves = (d.n_gblocks + gpw - 1) / gpw;
     const int groups = gpw > 1 ? SBVR_B1S_GROUPS_MULTI : SBVR_B1S_GROUPS;
     const int tpw = (d.n_tiles + groups - 1) / groups;
     const int grid = (d.n_tiles + tpw - 1) / tpw;
-    GemvArgs a = {(const uint4 *)planes_dev, (const uint16_t *)coeffs_dev, x, y, d.O, d.I, d.k,
-                  d.n_tiles, d.n_gblocks, gpw, 1, tpw};
+    GemvArgs a = {(const uint4 *)w.planes, (const uint16_t *)w.coeffs, x, y, d.O, d.I, d.k,
+                  d.n_tiles, d.n_gblocks, gpw, 1, tpw, (const uint16_t *)w.index, (const uint16_t *)w.table,
+                  w.n_sets};
+    const bool ix = w.index != nullptr;
     const size_t lds = (size_t)waves * B1S_WAVE_LDS + (size_t)tpw * waves * d.tr * 4;
     const bool multi = gpw > 1;
-    const void *fn = d.k == 4   ? b1s_kernel_for<4>(multi, a8)
-                     : d.k == 3 ? b1s_kernel_for<3>(multi, a8)
-                     : d.k == 2 ? b1s_kernel_for<2>(multi, a8)
-                                : b1s_kernel_for<1>(multi, a8);
+    const void *fn = d.k == 4   ? b1s_kernel_for<4>(multi, a8, ix)
+                     : d.k == 3 ? b1s_kernel_for<3>(multi, a8, ix)
+                     : d.k == 2 ? b1s_kernel_for<2>(multi, a8, ix)
+                                : b1s_kernel_for<1>(multi, a8, ix);
     void *args[] = {&a};
     return launch_kernel(fn, dim3(grid), dim3(64 * waves), lds, stream, args);
 }

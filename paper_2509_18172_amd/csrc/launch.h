@@ -24,11 +24,33 @@ int launch_pack(const Dims &d, const uint32_t *planes_canon, const uint16_t *coe
                 void *planes_dev, void *coeffs_dev, hipStream_t stream);
 int launch_unpack(const Dims &d, const void *planes_dev, const void *coeffs_dev,
                   uint32_t *planes_canon, uint16_t *coeffs_canon, hipStream_t stream);
+// Device weights: planes plus either per-group coefficient blocks (index ==
+// nullptr) or the coefficient-cache format (index blocks + table of n_sets
+// coefficient sets).
+struct WeightRef {
+    const void *planes;
+    const void *coeffs;
+    const void *index;
+    const void *table;
+    int n_sets;
+};
+
+inline WeightRef per_group_weights(const void *planes, const void *coeffs)
+{
+    return WeightRef{planes, coeffs, nullptr, nullptr, 0};
+}
+
 // a8: activations converted online to SBVR-8 (the W4A8 decode path)
-int launch_gemv_b1(const Dims &d, const void *planes_dev, const void *coeffs_dev,
-                   const uint16_t *x, uint16_t *y, bool a8, hipStream_t stream);
-int launch_gemv_b1s(const Dims &d, const void *planes_dev, const void *coeffs_dev,
-                    const uint16_t *x, uint16_t *y, bool a8, hipStream_t stream);
+int launch_gemv_b1(const Dims &d, const WeightRef &w, const uint16_t *x, uint16_t *y, bool a8,
+                   hipStream_t stream);
+int launch_gemv_b1s(const Dims &d, const WeightRef &w, const uint16_t *x, uint16_t *y, bool a8,
+                    hipStream_t stream);
+int launch_pack_indexed(const Dims &d, int n_sets, const uint32_t *planes_canon, const uint16_t *index_canon,
+                        const uint16_t *table_canon, void *planes_dev, void *index_dev, void *table_dev,
+                        hipStream_t stream);
+int launch_unpack_indexed(const Dims &d, int n_sets, const void *planes_dev, const void *index_dev,
+                          const void *table_dev, uint32_t *planes_canon, uint16_t *index_canon,
+                          uint16_t *table_canon, hipStream_t stream);
 int launch_decompress(const Dims &d, const void *planes_dev, const void *coeffs_dev, uint16_t *W,
                       hipStream_t stream);
 int launch_gemm_sbs(const Dims &d, const void *planes_dev, const void *coeffs_dev,

@@ -91,6 +91,33 @@ SBVR_HD size_t coeff_bytes(const Dims &d)
     return (size_t)d.n_tiles * d.n_gblocks * coeff_block_entries(d.k) * 2;
 }
 
+// Coefficient-cache format (Sec. 4.4): one 16-bit coefficient-set index per
+// (row, group) instead of k coefficients.  Index block of a (tile, gblock)
+// block: GB * TR entries; the entry of (tile row r, group slot b) is
+// ((r / NP) * GB + b) * NP + r % NP with NP = TR / 4, so the lane that holds
+// the result rows of tile rows NP*q .. NP*q+NP-1 for group slot b finds their
+// indices in NP consecutive entries.  The cache itself (the table of
+// coefficient sets) is stored with TABLE_STRIDE entries per set, zero padded.
+constexpr int TABLE_STRIDE = 4;
+constexpr int MAX_SETS = 65536;  // 16-bit index
+
+SBVR_HD constexpr int index_per_lane(int k) { return tile_rows(k) / 4; }
+
+SBVR_HD int index_entry(int k, int r, int b)
+{
+    const int np = index_per_lane(k);
+    return ((r / np) * GB + b) * np + r % np;
+}
+
+SBVR_HD size_t index_block_entries(int k) { return (size_t)GB * tile_rows(k); }
+
+SBVR_HD size_t index_bytes(const Dims &d)
+{
+    return (size_t)d.n_tiles * d.n_gblocks * index_block_entries(d.k) * 2;
+}
+
+SBVR_HD size_t table_bytes(int n_sets) { return (size_t)n_sets * TABLE_STRIDE * 2; }
+
 // canonical bit t (element t of the word) -> device bit position
 SBVR_HD int device_bit_of(int t) { return 4 * (t % 8) + t / 8; }
 // device bit position d -> canonical bit (element index within the word)

@@ -12,16 +12,17 @@ import bench  # noqa: E402
 
 
 @pytest.mark.parametrize("O,I,name", [
-    (4096, 4096, "gemv_b1_kernel<4, 4, false>"),      # 8192 blocks: one-shot, 1024 tiles -> T = 4
-    (1024, 4096, "gemv_b1_kernel<4, 1, false>"),
-    (14336, 4096, "gemv_b1s_kernel<4, 2, false, false>"),  # 28672 blocks: streaming
-    (4096, 14336, "gemv_b1s_kernel<4, 3, true, false>"),   # 28 gblocks per row
-    (8192, 8192, "gemv_b1s_kernel<4, 2, false, false>"),
-    (1024, 8192, "gemv_b1_kernel<4, 1, false>"),
+    (4096, 4096, "gemv_b1_kernel<4, 4, false, false>"),      # 8192 blocks: one-shot, 1024 tiles -> T = 4
+    (1024, 4096, "gemv_b1_kernel<4, 1, false, false>"),
+    (14336, 4096, "gemv_b1s_kernel<4, 2, false, false, false>"),  # 28672 blocks: streaming
+    (4096, 14336, "gemv_b1s_kernel<4, 3, true, false, false>"),   # 28 gblocks per row
+    (8192, 8192, "gemv_b1s_kernel<4, 2, false, false, false>"),
+    (1024, 8192, "gemv_b1_kernel<4, 1, false, false>"),
 ])
 def test_kernel_instance_names(O, I, name):
     assert bench.b1_kernel_instance(O, I, 4) == name
-    assert bench.b1_kernel_instance(O, I, 4, a8=True) == name.replace("false>", "true>")
+    assert bench.b1_kernel_instance(O, I, 4, a8=True) == name.replace("false, false>", "true, false>")
+    assert bench.b1_kernel_instance(O, I, 4, ix=True) == name.replace("false, false>", "false, true>")
 
 
 def _write_counter_csv(path, counter, rows):
@@ -36,7 +37,7 @@ def _write_counter_csv(path, counter, rows):
 
 def test_traffic_summary_scales_by_copy(tmp_path):
     copy = "void at::native::vectorized_elementwise_kernel<4, at::native::neg_kernel_cuda(at::TensorIteratorBase&)::{lambda()#1}>"
-    kern = "void sbvr::gemv_b1s_kernel<4, 2, false, false>(sbvr::GemvArgs)"
+    kern = "void sbvr::gemv_b1s_kernel<4, 2, false, false, false>(sbvr::GemvArgs)"
     calib_kib = bench.CALIB_BYTES / 1024
     # counters that see half of what moves: the scale must double them back
     _write_counter_csv(tmp_path / "f.csv", "FETCH_SIZE",
@@ -47,7 +48,7 @@ def test_traffic_summary_scales_by_copy(tmp_path):
     import json
     import re
     rec = json.loads(re.search(r"^traffic-record: (\{.*\})$", text, re.M).group(1))
-    k = rec["kernels"]["gemv_b1s_kernel<4, 2, false, false>"]
+    k = rec["kernels"]["gemv_b1s_kernel<4, 2, false, false, false>"]
     assert k["dispatches"] == 3
     assert k["bytes_per_launch"] == round(16100.0 * 1024 * 2 + 7.0 * 1024 * 2)
     assert rec["source_sha256"] == bench.kernel_source_digest()

@@ -657,3 +657,144 @@ def test_a8_codes_near_half_integers(sb):
     ulp = fp16_ulp(y_ref.astype(np.float16))
     bad = np.abs(y - y_ref.astype(np.float16).astype(np.float64)) > ulp
     assert not bad.any(), (np.flatnonzero(bad)[:8], y[bad][:8], y_ref[bad][:8])
+
+
+# --------------------------------------------------------------------------
+# Coefficient-cache format (Sec. 4.4): table of coefficient sets + per-group
+# index; reference = oracle.sbvr_gemv_indexed (gathered coefficients)
+# --------------------------------------------------------------------------
+
+def packed_indexed(sb, planes, index, table):
+    W = sb.pack_indexed(dev(planes.view(np.int32)), dev(index.view(np.int16)), dev(table.view(np.int16)))
+    torch.cuda.synchronize()
+    return W
+
+
+def run_gemv_indexed(sb, W, x16, a8=False):
+    y = sb.gemv_indexed(W, dev(x16), a8=a8)
+    torch.cuda.synchronize()
+    return y.cpu().numpy().astype(np.float64)
+
+
+def cache_sets(O, I):
+    """Coefficient sets for an O x I matrix: one per ten groups (an encoder
+    cache with a 90 % hit rate), within the 16-bit index."""
+    return max(1, min(65536, (O * (I // 128) + 9) // 10))
+
+
+@pytest.mark.parametrize("O,I,k,N", [(1, 128, 4, 1), (5, 640, 3, 7), (17, 384, 2, 65536), (1000, 1024, 1, 300),
+                                     (4096, 4096, 4, 13108), (1024, 14336, 4, 2000), (9, 896, 4, 3)])
+def test_pack_indexed_round_trip(sb, O, I, k, N):
+    planes, index, table = synth.random_indexed_sbvr(O, I, k, N, seed=O + I + k + N)
+    W = packed_indexed(sb, planes, index, table)
+    p2, i2, t2 = sb.unpack_indexed(W)
+    torch.cuda.synchronize()
+    assert np.array_equal(p2.cpu().numpy().view(np.uint32), planes)
+    assert np.array_equal(i2.cpu().numpy().view(np.uint16), index)
+    assert np.array_equal(t2.cpu().numpy().view(np.uint16), table)
+    assert W.index.numel() == sb.sbvr_packed_index_bytes(O, I, k) >= 2 * O * (I // 128)
+    assert W.table.numel() == sb.sbvr_packed_table_bytes(N, k) == 8 * N
+
+
+@pytest.mark.parametrize("O,I", SHAPES_8B + SHAPES_70B)
+def test_indexed_full_size_k4(sb, O, I):
+    N = cache_sets(O, I)
+    planes, index, table = synth.random_indexed_sbvr(O, I, 4, N, seed=O + 13 * I)
+    x = synth.activations(I, seed=O + 3 * I + synth.X_SEED_OFFSET)
+    y = run_gemv_indexed(sb, packed_indexed(sb, planes, index, table), x)
+    err = rel_err(y, oracle.sbvr_gemv_indexed(planes, index, table, x))
+    log(f"indexed full {O}x{I} k=4 N={N} err={err:.3e}")
+    assert err <= TOL
+
+
+@pytest.mark.parametrize("k", [1, 2, 3])
+@pytest.mark.parametrize("O,I", [(4096, 4096), (4096, 14336), (14336, 4096)])
+def test_indexed_full_size_low_bit(sb, O, I, k):
+    N = cache_sets(O, I)
+    planes, index, table = synth.random_indexed_sbvr(O, I, k, N, seed=O + 13 * I + k)
+    x = synth.activations(I, seed=O + 3 * I + k + synth.X_SEED_OFFSET)
+    y = run_gemv_indexed(sb, packed_indexed(sb, planes, index, table), x)
+    err = rel_err(y, oracle.sbvr_gemv_indexed(planes, index, table, x))
+    log(f"indexed full {O}x{I} k={k} N={N} err={err:.3e}")
+    assert err <= TOL
+
+
+@pytest.mark.parametrize("O,I,k,N", [(1, 128, 4, 1), (3, 128, 1, 2), (1001, 640, 3, 50), (7, 896, 4, 65536),
+                                     (4097, 1152, 2, 999), (33, 2560, 4, 5), (1000, 16384, 1, 4000)])
+def test_indexed_ragged_shapes(sb, O, I, k, N):
+    planes, index, table = synth.random_indexed_sbvr(O, I, k, N, seed=2 * O + I + k)
+    x = synth.activations(I, seed=O * 7 + k)
+    y = run_gemv_indexed(sb, packed_indexed(sb, planes, index, table), x)
+    assert rel_err(y, oracle.sbvr_gemv_indexed(planes, index, table, x)) <= TOL
+
+
+@pytest.mark.parametrize("O,I,k", [(4096, 4096, 4), (1024, 4096, 2), (14336, 4096, 4), (4096, 14336, 3),
+                                   (520, 1920, 1)])
+def test_indexed_equals_per_group_bit_for_bit(sb, O, I, k):
+    """The same coefficients stored per group (gathered by the oracle) go
+    through the same arithmetic: identical binary16 results, for fp16 and
+    SBVR-8 activations, one-shot and streaming kernels."""
+    N = cache_sets(O, I)
+    planes, index, table = synth.random_indexed_sbvr(O, I, k, N, seed=O + I + 5 * k)
+    coeffs = oracle.gather_coefficients(index, table)
+    x = synth.activations(I, seed=O + 11)
+    Wi = packed_indexed(sb, planes, index, table)
+    Wp = packed(sb, planes, coeffs)
+    assert np.array_equal(run_gemv_indexed(sb, Wi, x), run_gemv(sb, Wp, x))
+    assert np.array_equal(run_gemv_indexed(sb, Wi, x, a8=True), run_gemv_a8(sb, Wp, x))
+
+
+@pytest.mark.parametrize("O,I", [(4096, 4096), (14336, 4096), (4096, 14336)])
+def test_indexed_a8_against_oracle(sb, O, I):
+    N = cache_sets(O, I)
+    planes, index, table = synth.random_indexed_sbvr(O, I, 4, N, seed=O + 2 * I + 1)
+    x = synth.activations(I, seed=O + 17)
+    y = run_gemv_indexed(sb, packed_indexed(sb, planes, index, table), x, a8=True)
+    err = rel_err(y, oracle.sbvr_gemv_w4a8(planes, oracle.gather_coefficients(index, table), x))
+    log(f"indexed W4A8 {O}x{I} err={err:.3e}")
+    assert err <= TOL
+
+
+def test_indexed_out_of_range_index_reads_zero(sb):
+    """An index past the table is a caller error the library does not fault
+    on: those groups decode with zero coefficients."""
+    for O, I in [(256, 2048), (14336, 4096)]:
+        N = 100
+        planes, index, table = synth.random_indexed_sbvr(O, I, 4, N, seed=O)
+        bad = index.copy()
+        rng = np.random.default_rng(1)
+        hit = rng.random(bad.shape) < 0.05
+        bad[hit] = rng.integers(N, 65536, size=int(hit.sum()))
+        coeffs = oracle.gather_coefficients(np.where(hit, 0, bad), table)
+        coeffs[hit] = 0
+        x = synth.activations(I, seed=3)
+        y = run_gemv_indexed(sb, packed_indexed(sb, planes, bad, table), x)
+        assert rel_err(y, oracle.sbvr_gemv(planes, coeffs, x)) <= TOL
+
+
+def test_indexed_error_paths_and_canary(sb):
+    O, I, N = 100, 512, 9
+    planes, index, table = synth.random_indexed_sbvr(O, I, 4, N, seed=8)
+    W = packed_indexed(sb, planes, index, table)
+    xh = synth.activations(I, seed=9)
+    x = dev(xh)
+    buf = torch.full((O + 64,), 7.0, dtype=torch.float16, device="cuda")
+    args = (W.planes.data_ptr(), W.index.data_ptr(), W.table.data_ptr())
+    st = sb.sbvr_gemv_indexed(O, I, 4, N, *args, x.data_ptr(), buf.data_ptr(), None, 0, 0)
+    torch.cuda.synchronize()
+    assert st == 0 and torch.all(buf[O:] == 7.0)
+    assert rel_err(buf[:O].cpu().numpy().astype(np.float64), oracle.sbvr_gemv_indexed(planes, index, table, xh)) <= TOL
+    buf.fill_(5.0)
+    torch.cuda.synchronize()
+    for fn in (sb.sbvr_gemv_indexed, sb.sbvr_gemv_indexed_a8):
+        for shape in [(O, I, 5, N), (O, 100, 4, N), (0, I, 4, N), (O, I, 4, 0), (O, I, 4, 65537)]:
+            assert fn(*shape, *args, x.data_ptr(), buf.data_ptr(), None, 0, 0) != 0
+        assert fn(O, I, 4, N, *args, x.data_ptr() + 2, buf.data_ptr(), None, 0, 0) == sb.SBVR_E_ALIGNMENT
+        assert fn(O, I, 4, N, args[0], args[1] + 2, args[2], x.data_ptr(), buf.data_ptr(), None, 0, 0) \
+            == sb.SBVR_E_ALIGNMENT
+        assert fn(O, I, 4, N, args[0], None, args[2], x.data_ptr(), buf.data_ptr(), None, 0, 0) \
+            == sb.SBVR_E_INVALID_ARG
+    torch.cuda.synchronize()
+    assert torch.all(buf == 5.0)
+    assert sb.sbvr_packed_table_bytes(N, 4) == 8 * N and sb.sbvr_packed_table_bytes(0, 4) == 0
+    assert sb.sbvr_packed_table_bytes(65537, 4) == 0
