@@ -38,6 +38,9 @@ One JSON line is printed:
                 SBVR bytes read plus the 2 bytes per weight written) and, for
                 context, a 512-token library GEMM (torch.matmul) on the result
   llama3_70b    per projection of the Llama-3-70B shapes, same timing
+  encoder       sbvr_encode (Algorithm 1 on the GPU, the 1024-entry grid) on an
+                fp32 q/o-shaped matrix: seconds and groups per second, and the
+                CPU oracle's encoder on a sample of its rows
   cpu_baseline  the CPU oracle (binary64 decompress + GEMV) on layer 0's seven
                 GEMVs, bounded to ~10 s of work, in the same unit
 
@@ -491,6 +494,31 @@ def main():
         elif args.model == "llama3-70b":
             other_model = shape_table(synth.LLAMA8B, k, 1)
 
+    # ---- encoder (Algorithm 1 on the GPU, bit-identical to the oracle's) on a
+    # q/o-shaped fp32 matrix, and the oracle's encoder on a sample of its rows ----
+    encoder = None
+    if not args.quick:
+        O, I = shapes["q"]
+        Wf = synth.weights(O, I, 0.02 if args.model == "llama3-8b" else 0.015, seed=synth.seed_for(cfg_index, 0, 0))
+        Wd = torch.from_numpy(Wf).to(dev)
+        with torch.cuda.stream(stream):
+            sb.encode(Wd, k, stream=stream)
+        torch.cuda.synchronize()
+        reps = [timed(lambda: sb.encode(Wd, k, stream=stream)) * 1e-3 for _ in range(3)]
+        sec = float(np.median(reps))
+        groups = O * (I // 128)
+        encoder = {"shape": [O, I], "k": k, "groups": groups, "entries_per_group": 1024,
+                   "gpu_s": round(sec, 4), "gpu_groups_per_s": round(groups / sec)}
+        if not args.no_cpu_baseline:
+            import oracle
+            rows = 128
+            ts = time.perf_counter()
+            oracle.encode_matrix(Wf[:rows], k)
+            el = time.perf_counter() - ts
+            encoder["oracle_groups_per_s"] = round(rows * (I // 128) / el, 1)
+            encoder["oracle_sample"] = f"{rows} rows ({rows * (I // 128)} groups), {el:.1f} s on {os.cpu_count()} threads"
+        del Wd
+
     # ---- CPU baseline: the oracle on layer 0, bounded ----
     cpu = None
     if not args.no_cpu_baseline:
@@ -539,6 +567,7 @@ def main():
         "small_batch": small_batch or None,
         "w4a8": w4a8 or None,
         "indexed": indexed,
+        "encoder": encoder,
         "low_bit": low_bit or None,
         "prefill": prefill or None,
         ("llama3_70b" if args.model == "llama3-8b" else "llama3_8b"): other_model,

@@ -71,7 +71,8 @@ enum sbvr_status {
 const char *sbvr_status_string(int status);
 
 /* Library ABI version (major * 100 + minor); 1.01 adds sbvr_decompress,
- * 1.02 sbvr_gemv_a8, 1.03 the coefficient-cache format entry points. */
+ * 1.02 sbvr_gemv_a8, 1.03 the coefficient-cache format entry points,
+ * 1.04 sbvr_encode. */
 int sbvr_version(void);
 
 /*
@@ -212,6 +213,31 @@ int sbvr_gemv_indexed_a8(int O, int I, int k, int n_sets, const void *planes_dev
  */
 int sbvr_decompress(int O, int I, int k, const void *planes_dev, const void *coeffs_dev, uint16_t *W,
                     hipStream_t stream);
+
+/*
+ * SBVR encoding on the GPU (Algorithm 1 and the bitvector assignment of
+ * Sec. 4.2): every 128-weight group of W takes, from the (r, s, b) grid of
+ * Eqs. 4-11 with |R1| = n_ratio1, |R2| = n_ratio2, N_scale = n_scale and
+ * N_bias = n_bias entries, the binary16 coefficient set with the smallest
+ * mean squared error of nearest-subset-sum reconstruction (first such entry
+ * in (r, s, b) order), and each weight the bit pattern of its nearest subset
+ * sum (lowest pattern index on ties).  normalise = 1 divides the geometric
+ * series of Eq. 4 by sum_i abs(r)^i (the span-normalised reading), 0 takes
+ * Eq. 4 literally.  Groups with no admissible entry (s <= 0 or a non-finite
+ * coefficient everywhere) get (fp16(mean), 0, ...).  All arithmetic is
+ * binary64 in a fixed order, so the output is deterministic and reproducible
+ * bit for bit by a CPU implementation of the same definition.
+ *   W             float32 [O][I] row-major, device, 4-byte aligned; finite.
+ *   planes_canon  uint32 [O][G][k][4] canonical planes (output, 16-byte aligned).
+ *   coeffs_canon  uint16 [O][G][k] binary16 coefficients (output).
+ *   mse           binary64 [O][G] (output, 8-byte aligned) or NULL.
+ * At most SBVR_ENCODE_MAX_ENTRIES grid entries ((n_ratio1 + n_ratio2) *
+ * n_scale * n_bias); more is SBVR_E_UNSUPPORTED.
+ */
+#define SBVR_ENCODE_MAX_ENTRIES 65536
+int sbvr_encode(int O, int I, int k, const float *W, int n_ratio1, int n_ratio2, int n_scale, int n_bias,
+                int normalise, uint32_t *planes_canon, uint16_t *coeffs_canon, double *mse,
+                hipStream_t stream);
 
 #ifdef __cplusplus
 }

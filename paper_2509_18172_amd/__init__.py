@@ -30,7 +30,7 @@ EXPORTED = (
     "sbvr_status_string", "sbvr_version", "sbvr_packed_plane_bytes", "sbvr_packed_coeff_bytes",
     "sbvr_workspace_bytes", "sbvr_pack", "sbvr_unpack", "sbvr_gemv", "sbvr_gemm_small_batch",
     "sbvr_decompress", "sbvr_gemv_a8", "sbvr_packed_index_bytes", "sbvr_packed_table_bytes",
-    "sbvr_pack_indexed", "sbvr_unpack_indexed", "sbvr_gemv_indexed", "sbvr_gemv_indexed_a8",
+    "sbvr_pack_indexed", "sbvr_unpack_indexed", "sbvr_gemv_indexed", "sbvr_gemv_indexed_a8", "sbvr_encode",
 )
 
 
@@ -73,6 +73,7 @@ def _load():
         "sbvr_unpack_indexed": (i32, [i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp]),
         "sbvr_gemv_indexed": (i32, [i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, sz, vp]),
         "sbvr_gemv_indexed_a8": (i32, [i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "sbvr_encode": (i32, [i32, i32, i32, vp, i32, i32, i32, i32, i32, vp, vp, vp, vp]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -160,6 +161,12 @@ def sbvr_gemv_indexed_a8(O, I, k, n_sets, planes_dev, index_dev, table_dev, x, y
                          ws_bytes=0, stream=0) -> int:
     return _lib.sbvr_gemv_indexed_a8(O, I, k, n_sets, planes_dev, index_dev, table_dev, x, y, workspace,
                                      ws_bytes, stream)
+
+
+def sbvr_encode(O, I, k, W, n_ratio1, n_ratio2, n_scale, n_bias, normalise, planes_canon, coeffs_canon,
+                mse=None, stream=0) -> int:
+    return _lib.sbvr_encode(O, I, k, W, n_ratio1, n_ratio2, n_scale, n_bias, normalise, planes_canon,
+                            coeffs_canon, mse, stream)
 
 
 def sbvr_decompress(O, I, k, planes_dev, coeffs_dev, W, stream=0) -> int:
@@ -328,6 +335,23 @@ def gemv_indexed(W: IndexedWeight, x, out=None, a8: bool = False, stream=None):
     _check(fn(W.O, W.I, W.k, W.n_sets, W.planes.data_ptr(), W.index.data_ptr(), W.table.data_ptr(),
               x.data_ptr(), y.data_ptr(), None, 0, _stream(stream)), name)
     return y
+
+
+def encode(W, k: int, n_ratio1: int = 8, n_ratio2: int = 8, n_scale: int = 16, n_bias: int = 4,
+           normalise: bool = True, want_mse: bool = False, stream=None):
+    """Encode a float32 [O][I] device matrix into canonical SBVR on the GPU:
+    returns (planes int32 [O][G][k][4], coeffs int16 [O][G][k][, mse float64
+    [O][G]]) device tensors.  Defaults: the 1024-entry search grid."""
+    torch = _torch()
+    assert W.dtype == torch.float32 and W.is_contiguous() and W.dim() == 2
+    O, I = W.shape
+    G = I // GROUP
+    planes = torch.empty((O, G, k, 4), dtype=torch.int32, device=W.device)
+    coeffs = torch.empty((O, G, k), dtype=torch.int16, device=W.device)
+    mse = torch.empty((O, G), dtype=torch.float64, device=W.device) if want_mse else None
+    _check(sbvr_encode(O, I, k, W.data_ptr(), n_ratio1, n_ratio2, n_scale, n_bias, int(normalise), planes.data_ptr(),
+                       coeffs.data_ptr(), mse.data_ptr() if want_mse else None, _stream(stream)), "sbvr_encode")
+    return (planes, coeffs, mse) if want_mse else (planes, coeffs)
 
 
 def decompress(W: PackedWeight, out=None, stream=None):

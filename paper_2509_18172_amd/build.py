@@ -8,7 +8,10 @@ import subprocess
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
-SOURCES = [os.path.join(HERE, "csrc", f) for f in ("api.hip", "pack.hip", "gemv_b1.hip", "gemv_b1s.hip", "gemm_sbs.hip", "decompress.hip")]
+SOURCES = [os.path.join(HERE, "csrc", f) for f in ("api.hip", "pack.hip", "gemv_b1.hip", "gemv_b1s.hip", "gemm_sbs.hip",
+                                                  "decompress.hip", "encode.hip")]
+# The encoder's binary64 arithmetic is its definition: no fused multiply-add.
+SOURCE_FLAGS = {"encode.hip": ["-ffp-contract=off"]}
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [
@@ -46,7 +49,8 @@ def build(verbose: bool = False, out: str | None = None, defines=(), jobs: int =
     jobs = jobs or min(len(SOURCES), os.cpu_count() or 1, 8)
     try:
         with ThreadPoolExecutor(max_workers=jobs) as ex:
-            list(ex.map(run, [[HIPCC, *compile_flags, "-c", src, "-o", obj] for src, obj in zip(SOURCES, objs)]))
+            list(ex.map(run, [[HIPCC, *compile_flags, *SOURCE_FLAGS.get(os.path.basename(src), []), "-c", src,
+                               "-o", obj] for src, obj in zip(SOURCES, objs)]))
         tmp = out + ".tmp%d" % os.getpid()
         run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp])
         os.replace(tmp, out)

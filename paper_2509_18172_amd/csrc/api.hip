@@ -114,7 +114,7 @@ const char *sbvr_status_string(int status)
     }
 }
 
-int sbvr_version(void) { return 103; }
+int sbvr_version(void) { return 104; }
 
 size_t sbvr_packed_plane_bytes(int O, int I, int k)
 {
@@ -243,6 +243,24 @@ int sbvr_gemv_indexed_a8(int O, int I, int k, int n_sets, const void *planes_dev
         return st;
     return launch_gemv_b1(make_dims(O, I, k), indexed_weights(planes_dev, index_dev, table_dev, n_sets), x, y,
                           true, stream);
+}
+
+int sbvr_encode(int O, int I, int k, const float *W, int n_ratio1, int n_ratio2, int n_scale, int n_bias,
+                int normalise, uint32_t *planes_canon, uint16_t *coeffs_canon, double *mse, hipStream_t stream)
+{
+    int st = check_shape(O, I, k);
+    if (st != SBVR_OK)
+        return st;
+    if (n_ratio1 < 1 || n_ratio2 < 1 || n_scale < 1 || n_bias < 1 || (normalise != 0 && normalise != 1))
+        return SBVR_E_INVALID_ARG;
+    if ((long long)(n_ratio1 + (long long)n_ratio2) * n_scale * n_bias > SBVR_ENCODE_MAX_ENTRIES)
+        return SBVR_E_UNSUPPORTED;
+    if (!W || !planes_canon || !coeffs_canon)
+        return SBVR_E_INVALID_ARG;
+    if (!aligned(W, 4) || !aligned(planes_canon, 16) || !aligned(coeffs_canon, 2) || (mse && !aligned(mse, 8)))
+        return SBVR_E_ALIGNMENT;
+    return launch_encode(O, I, k, W, n_ratio1, n_ratio2, n_scale, n_bias, normalise, planes_canon, coeffs_canon,
+                         mse, stream);
 }
 
 int sbvr_decompress(int O, int I, int k, const void *planes_dev, const void *coeffs_dev, uint16_t *W,

@@ -15,46 +15,10 @@
 // writes 16 bytes.  HBM-bound: per weight it reads k/8 + 2k/128 bytes and
 // writes 2.
 #include "device_ops.h"
+#include "f16_round.h"
 #include "launch.h"
 
 namespace sbvr {
-
-// binary64 -> binary16, round to nearest, ties to even (IEEE 754), from the
-// bit fields; overflow gives infinity.  (Rounding through binary32 with the
-// hardware conversions needs a tie fix-up and measured slower.)
-__device__ __forceinline__ uint16_t f64_to_f16_rne(double x)
-{
-    const uint64_t u = (uint64_t)__double_as_longlong(x);
-    const uint32_t sign = (uint32_t)(u >> 48) & 0x8000u;
-    const int e = (int)((u >> 52) & 0x7ff);
-    if (e == 0)  // zero or a binary64 subnormal: far below binary16's range
-        return (uint16_t)sign;
-    const uint64_t sig = (1ull << 52) | (u & ((1ull << 52) - 1));
-    int E = e - 1023;
-    int shift;  // bits of sig dropped
-    if (E >= -14) {
-        shift = 42;  // keep 11 significant bits
-    } else {
-        shift = 28 - E;  // subnormal: units of 2^-24
-        if (shift > 54)
-            return (uint16_t)sign;  // below half the smallest subnormal
-    }
-    uint64_t q = sig >> shift;
-    const uint64_t rem = sig & ((1ull << shift) - 1);
-    const uint64_t half = 1ull << (shift - 1);
-    if (rem > half || (rem == half && (q & 1)))
-        ++q;
-    if (E >= -14) {
-        if (q == (1ull << 11)) {  // rounded up to the next binade
-            q >>= 1;
-            ++E;
-        }
-        if (E > 15)
-            return (uint16_t)(sign | 0x7c00u);
-        return (uint16_t)(sign | (uint32_t)(E + 15) << 10 | (uint32_t)(q & 0x3ff));
-    }
-    return (uint16_t)(sign | (uint32_t)q);  // q == 0x400 is the smallest normal
-}
 
 // One workgroup per (tile, gblock) block; the plane words are loaded first so
 // that their latency overlaps the subset-sum table.  (Several blocks per

@@ -1,0 +1,273 @@
+// SBVR encoding (Algorithm 1 with the bitvector assignment of Sec. 4.2) on
+// the GPU: for every 128-weight group, search the coefficient sets of the
+// (r, s, b) grid (Eqs. 4-11) for the one with the smallest mean squared error
+// of nearest-subset-sum reconstruction, then give each weight the pattern of
+// its nearest subset sum.
+//
+// The arithmetic is the search's definition carried out in binary64 in a
+// fixed order, so the result is bit-identical to any implementation that
+// follows the same definition (this file is compiled without floating-point
+// contraction):
+//   - group statistics in element order: min, max, sum; mean = sum / n;
+//   - q95: the linearly interpolated 95th percentile of the sorted group,
+//     s[lo] + frac * (s[lo+1] - s[lo]) at position 0.95 (n - 1);
+//   - S_j = s_min + (j+1) s_gran, s_min = 2 q95, s_max = 1.1 (max - min),
+//     s_gran = (s_max - s_min) / N_scale (Eqs. 6, 8, 10, 11);
+//     B_k = b_min + k b_gran, b_max = 2 |mean| / K, b_min = -b_max,
+//     b_gran = (b_max - b_min) / N_bias (Eqs. 7, 9, 10, 11);
+//     R: -1 + (i+1) (0.5 / N_1) for i < N_1, then -2 + i (1 / N_2) for i < N_2;
+//   - entry coefficients c_i = fp16((s r^i) / N(r) + b), r^i by repeated
+//     multiplication, N(r) = sum_i abs(r^i) accumulated in i order (1 for the
+//     literal form of Eq. 4); entries with s <= 0 or a non-finite c are skipped;
+//   - subset sums in bit order, nearest = first strict minimum of
+//     abs(x - sum_p) over p ascending, MSE = (sum_j (x_j - sum)^2 in j order) / n,
+//     best entry = first strict minimum over entries in (r, s, b) order;
+//   - no admissible entry: c = (fp16(mean), 0, ...).
+//
+// Work split: one wavefront per group; lane l evaluates entries l, l+64, ...
+// (each entry's error sum runs over the elements in order, so entries -- not
+// elements -- are what is parallel), then the wavefront picks the smallest
+// error with the lowest entry index, which is the sequential first minimum.
+// The group's values sit in LDS and are read as broadcasts.
+#include "device_ops.h"
+#include "f16_round.h"
+#include "launch.h"
+
+namespace sbvr {
+
+constexpr int ENC_THREADS = 64;  // one wavefront per group
+
+__device__ __forceinline__ double f16_bits_to_double(uint16_t h)
+{
+    return (double)half_bits_to_float(h);  // both conversions exact
+}
+
+// Coefficients of one entry; false if a coefficient is not finite.
+template <int K>
+__device__ __forceinline__ bool entry_coeffs(double r, double s, double b, bool normalise, uint16_t *c)
+{
+    double norm = 1.0;
+    if (normalise) {
+        double a = 1.0, t = 0.0;
+#pragma unroll
+        for (int i = 0; i < K; ++i) {
+            t += fabs(a);
+            a *= r;
+        }
+        norm = t;
+    }
+    double pw = 1.0;
+    bool ok = true;
+#pragma unroll
+    for (int i = 0; i < K; ++i) {
+        const double v = (s * pw) / norm + b;
+        c[i] = f64_to_f16_rne(v);
+        ok = ok && (c[i] & 0x7c00u) != 0x7c00u;
+        pw *= r;
+    }
+    return ok;
+}
+
+template <int K>
+__device__ __forceinline__ void subset_sums(const uint16_t *c, double *sums)
+{
+    double cv[K];
+#pragma unroll
+    for (int i = 0; i < K; ++i)
+        cv[i] = f16_bits_to_double(c[i]);
+#pragma unroll
+    for (int p = 0; p < (1 << K); ++p) {
+        double t = 0.0;
+#pragma unroll
+        for (int i = 0; i < K; ++i)
+            if ((p >> i) & 1)
+                t += cv[i];
+        sums[p] = t;
+    }
+}
+
+// Nearest subset sum of x: pattern index and the signed difference x - sum.
+template <int K>
+__device__ __forceinline__ int nearest(const double *sums, double x, double &diff)
+{
+    int best = 0;
+    double bd = x - sums[0];
+#pragma unroll
+    for (int p = 1; p < (1 << K); ++p) {
+        const double d = x - sums[p];
+        if (fabs(d) < fabs(bd)) {
+            bd = d;
+            best = p;
+        }
+    }
+    diff = bd;
+    return best;
+}
+
+template <int K>
+__device__ __forceinline__ double entry_mse(const double *D, const double *sums)
+{
+    double err = 0.0;
+    for (int j = 0; j < GROUP; ++j) {
+        double d;
+        nearest<K>(sums, D[j], d);
+        err += d * d;
+    }
+    return err / (double)GROUP;
+}
+
+struct EncodeArgs {
+    const float *W;
+    uint32_t *planes;  // canonical [O][G][K][4]
+    uint16_t *coeffs;  // canonical [O][G][K]
+    double *mse;       // [O][G] or null
+    int O, I;
+    int n_ratio1, n_ratio2, n_scale, n_bias, normalise;
+};
+
+template <int K>
+__global__ void __launch_bounds__(ENC_THREADS) encode_kernel(EncodeArgs a)
+{
+    __shared__ double D[GROUP];
+    __shared__ double best_mse_l[ENC_THREADS];
+    __shared__ int best_e_l[ENC_THREADS];
+    __shared__ double q_pair[2];
+    const int lane = threadIdx.x;
+    const int G = a.I / GROUP;
+    const size_t grp = blockIdx.x;
+    const size_t o = grp / G, g = grp % G;
+    const float *src = a.W + o * (size_t)a.I + g * GROUP;
+
+    const double d0 = (double)src[lane], d1 = (double)src[lane + 64];
+    D[lane] = d0;
+    D[lane + 64] = d1;
+    __syncthreads();
+
+    // statistics in element order (every lane, from broadcast reads)
+    double mn = D[0], mx = D[0], sum = 0.0;
+    for (int j = 0; j < GROUP; ++j) {
+        const double v = D[j];
+        if (v < mn)
+            mn = v;
+        if (v > mx)
+            mx = v;
+        sum += v;
+    }
+    const double avg = sum / (double)GROUP;
+
+    // sorted positions lo and lo+1 of the linear-interpolation percentile:
+    // stable rank of each of the lane's two elements
+    const double pos = 0.95 * (double)(GROUP - 1);
+    const int lo = (int)floor(pos);
+    const double frac = pos - (double)lo;
+    {
+        int r0 = 0, r1 = 0;
+        for (int j = 0; j < GROUP; ++j) {
+            const double v = D[j];
+            r0 += (v < d0) || (v == d0 && j < lane);
+            r1 += (v < d1) || (v == d1 && j < lane + 64);
+        }
+        if (r0 == lo || r0 == lo + 1)
+            q_pair[r0 - lo] = d0;
+        if (r1 == lo || r1 == lo + 1)
+            q_pair[r1 - lo] = d1;
+    }
+    __syncthreads();
+    const double q95 = q_pair[0] + frac * (q_pair[1] - q_pair[0]);
+
+    const double s_max = 1.1 * (mx - mn);
+    const double s_min = 2.0 * q95;
+    const double s_gran = (s_max - s_min) / (double)a.n_scale;
+    const double b_max = 2.0 * fabs(avg) / (double)K;
+    const double b_min = -b_max;
+    const double b_gran = (b_max - b_min) / (double)a.n_bias;
+    const double r1_gran = 0.5 / (double)a.n_ratio1;
+    const double r2_gran = 1.0 / (double)a.n_ratio2;
+    const int per_r = a.n_scale * a.n_bias;
+    const int n_entries = (a.n_ratio1 + a.n_ratio2) * per_r;
+
+    auto entry_rsb = [&](int e, double &r, double &s, double &b) {
+        const int ir = e / per_r, js = (e / a.n_bias) % a.n_scale, kb = e % a.n_bias;
+        r = ir < a.n_ratio1 ? -1.0 + (double)(ir + 1) * r1_gran : -2.0 + (double)(ir - a.n_ratio1) * r2_gran;
+        s = s_min + (double)(js + 1) * s_gran;
+        b = b_min + (double)kb * b_gran;
+    };
+
+    double best_mse = __builtin_inf();
+    int best_e = -1;
+    for (int e = lane; e < n_entries; e += ENC_THREADS) {
+        double r, s, b;
+        entry_rsb(e, r, s, b);
+        if (!(s > 0.0))
+            continue;
+        uint16_t c[K];
+        if (!entry_coeffs<K>(r, s, b, a.normalise != 0, c))
+            continue;
+        double sums[1 << K];
+        subset_sums<K>(c, sums);
+        const double mse = entry_mse<K>(D, sums);
+        if (mse < best_mse) {
+            best_mse = mse;
+            best_e = e;
+        }
+    }
+    best_mse_l[lane] = best_mse;
+    best_e_l[lane] = best_e;
+    __syncthreads();
+    // smallest error, lowest entry index among equal errors
+    double m = __builtin_inf();
+    int be = -1;
+    for (int l = 0; l < ENC_THREADS; ++l) {
+        const int e = best_e_l[l];
+        const double v = best_mse_l[l];
+        if (e >= 0 && (be < 0 || v < m || (v == m && e < be))) {
+            m = v;
+            be = e;
+        }
+    }
+
+    uint16_t c[K];
+    if (be >= 0) {
+        double r, s, b;
+        entry_rsb(be, r, s, b);
+        entry_coeffs<K>(r, s, b, a.normalise != 0, c);
+    } else {  // no admissible entry
+        c[0] = f64_to_f16_rne(avg);
+#pragma unroll
+        for (int i = 1; i < K; ++i)
+            c[i] = 0;
+    }
+    double sums[1 << K];
+    subset_sums<K>(c, sums);
+    if (be < 0)
+        m = entry_mse<K>(D, sums);
+
+    double dd;
+    const int p0 = nearest<K>(sums, d0, dd), p1 = nearest<K>(sums, d1, dd);
+#pragma unroll
+    for (int i = 0; i < K; ++i) {
+        const uint64_t m0 = __ballot((p0 >> i) & 1), m1 = __ballot((p1 >> i) & 1);
+        if (lane == i) {
+            uint32_t *pl = a.planes + (grp * K + i) * 4;
+            *(uint4 *)pl = make_uint4((uint32_t)m0, (uint32_t)(m0 >> 32), (uint32_t)m1, (uint32_t)(m1 >> 32));
+            a.coeffs[grp * K + i] = c[i];
+        }
+    }
+    if (lane == 0 && a.mse)
+        a.mse[grp] = m;
+}
+
+int launch_encode(int O, int I, int k, const float *W, int n_ratio1, int n_ratio2, int n_scale, int n_bias,
+                  int normalise, uint32_t *planes, uint16_t *coeffs, double *mse, hipStream_t stream)
+{
+    EncodeArgs a = {W, planes, coeffs, mse, O, I, n_ratio1, n_ratio2, n_scale, n_bias, normalise};
+    const size_t groups = (size_t)O * (I / GROUP);
+    const void *fn = k == 4   ? (const void *)encode_kernel<4>
+                     : k == 3 ? (const void *)encode_kernel<3>
+                     : k == 2 ? (const void *)encode_kernel<2>
+                              : (const void *)encode_kernel<1>;
+    void *args[] = {&a};
+    return launch_kernel(fn, dim3((unsigned)groups), dim3(ENC_THREADS), 0, stream, args);
+}
+
+}  // namespace sbvr

@@ -1,0 +1,109 @@
+"""GPU SBVR encoder (Algorithm 1 + the bitvector assignment of Sec. 4.2)
+against the CPU oracle's encoder, bit for bit: planes, binary16 coefficients
+and the chosen entry's binary64 MSE.  Both follow the same fixed-order
+binary64 definition of the search, so any difference is a bug.  Inputs:
+seeded Gaussian weights with outliers, the Llama-70B weight scale, other
+search grids, and degenerate groups (constant, zero with mixed signs,
+single spikes, extreme magnitudes)."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def sb():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2509_18172_amd as m
+    return m
+
+
+def gpu_encode(sb, W, k, params=oracle.DEFAULT):
+    Wd = torch.from_numpy(np.ascontiguousarray(W, dtype=np.float32)).cuda()
+    planes, coeffs, mse = sb.encode(Wd, k, params.n_ratio1, params.n_ratio2, params.n_scale, params.n_bias,
+                                    params.normalise, want_mse=True)
+    torch.cuda.synchronize()
+    return (planes.cpu().numpy().view(np.uint32), coeffs.cpu().numpy().view(np.uint16), mse.cpu().numpy())
+
+
+def assert_same(sb, W, k, params=oracle.DEFAULT, what=""):
+    p_ref, c_ref, m_ref = oracle.encode_matrix(W, k, params, want_mse=True)
+    p, c, m = gpu_encode(sb, W, k, params)
+    bad = np.flatnonzero((c != c_ref).any(axis=-1).reshape(-1) | (p != p_ref).any(axis=(-1, -2)).reshape(-1))
+    assert bad.size == 0, (what, "groups differ", bad[:8])
+    assert np.array_equal(m.view(np.uint64), m_ref.view(np.uint64)), what
+    print(f"encode {what} {W.shape} k={k}: identical", flush=True)
+
+
+@pytest.mark.parametrize("k", [1, 2, 3, 4])
+def test_encoder_bit_exact_gaussian_with_outliers(sb, k):
+    W = synth.weights(64, 1024, 0.02, seed=synth.seed_for(1, 0, k), outlier_frac=0.001)
+    assert_same(sb, W, k, what="N(0, 0.02^2) + outliers")
+
+
+def test_encoder_bit_exact_70b_scale_and_ragged_rows(sb):
+    W = synth.weights(37, 896, 0.015, seed=synth.seed_for(3, 0, 0))
+    assert_same(sb, W, 4, what="N(0, 0.015^2)")
+    assert_same(sb, W[:1, :128], 4, what="one group")
+
+
+@pytest.mark.parametrize("params", [oracle.SearchParams(normalise=False),
+                                    oracle.SearchParams(2, 2, 3, 1),
+                                    oracle.SearchParams(1, 3, 5, 2),
+                                    oracle.SearchParams(16, 8, 32, 8)])
+def test_encoder_bit_exact_other_grids(sb, params):
+    W = synth.weights(8, 512, 0.02, seed=41)
+    for k in (2, 4):
+        assert_same(sb, W, k, params, what=str(params))
+
+
+def test_encoder_bit_exact_degenerate_groups(sb):
+    rng = np.random.default_rng(7)
+    rows = [
+        np.zeros(128),                                         # all +0
+        np.where(np.arange(128) % 2, -0.0, 0.0),               # +0 / -0 mixed
+        np.full(128, 0.0125),                                  # constant positive
+        np.full(128, -3.5),                                    # constant negative
+        np.r_[np.zeros(127), 1.0],                             # one spike
+        rng.standard_normal(128) * 1e30,                       # beyond binary16: every entry skipped
+        rng.standard_normal(128) * 1e-30,                      # below binary16's range
+        rng.standard_normal(128) * 60000.0,                    # near binary16's maximum
+        np.r_[np.full(64, 1.0), np.full(64, -1.0)],            # two values, ties in the percentile
+        np.round(rng.standard_normal(128) * 4) / 4,            # many repeated values
+    ]
+    W = np.stack(rows).astype(np.float32)
+    for k in (1, 2, 3, 4):
+        assert_same(sb, W, k, what="degenerate")
+
+
+def test_encoder_output_gemv_parity(sb):
+    """The GPU-encoded matrix through the GPU GEMV against the oracle's exact
+    GEMV of the same encoding."""
+    W = synth.weights(256, 2048, 0.02, seed=5, outlier_frac=0.001)
+    p, c, _ = gpu_encode(sb, W, 4)
+    x = synth.activations(2048, seed=6)
+    Wd = sb.pack(torch.from_numpy(p.view(np.int32)).cuda(), torch.from_numpy(c.view(np.int16)).cuda())
+    y = sb.gemv(Wd, torch.from_numpy(x).cuda()).cpu().numpy().astype(np.float64)
+    y_ref = oracle.sbvr_gemv(p, c, x)
+    assert np.abs(y - y_ref).max() / np.abs(y_ref).max() <= 1e-3
+
+
+def test_encoder_error_paths(sb):
+    W = torch.zeros((4, 256), dtype=torch.float32, device="cuda")
+    planes = torch.empty((4, 2, 4, 4), dtype=torch.int32, device="cuda")
+    coeffs = torch.empty((4, 2, 4), dtype=torch.int16, device="cuda")
+    p, c, w = planes.data_ptr(), coeffs.data_ptr(), W.data_ptr()
+    assert sb.sbvr_encode(4, 256, 4, w, 8, 8, 16, 4, 1, p, c, None, 0) == 0
+    assert sb.sbvr_encode(4, 256, 5, w, 8, 8, 16, 4, 1, p, c, None, 0) == sb.SBVR_E_UNSUPPORTED
+    assert sb.sbvr_encode(4, 200, 4, w, 8, 8, 16, 4, 1, p, c, None, 0) == sb.SBVR_E_INVALID_ARG
+    assert sb.sbvr_encode(4, 256, 4, w, 0, 8, 16, 4, 1, p, c, None, 0) == sb.SBVR_E_INVALID_ARG
+    assert sb.sbvr_encode(4, 256, 4, w, 8, 8, 16, 4, 2, p, c, None, 0) == sb.SBVR_E_INVALID_ARG
+    assert sb.sbvr_encode(4, 256, 4, w, 64, 64, 64, 64, 1, p, c, None, 0) == sb.SBVR_E_UNSUPPORTED
+    assert sb.sbvr_encode(4, 256, 4, w + 2, 8, 8, 16, 4, 1, p, c, None, 0) == sb.SBVR_E_ALIGNMENT
+    assert sb.sbvr_encode(4, 256, 4, w, 8, 8, 16, 4, 1, p + 4, c, None, 0) == sb.SBVR_E_ALIGNMENT
+    assert sb.sbvr_encode(4, 256, 4, None, 8, 8, 16, 4, 1, p, c, None, 0) == sb.SBVR_E_INVALID_ARG
+    torch.cuda.synchronize()
