@@ -72,7 +72,7 @@ const char *sbvr_status_string(int status);
 
 /* Library ABI version (major * 100 + minor); 1.01 adds sbvr_decompress,
  * 1.02 sbvr_gemv_a8, 1.03 the coefficient-cache format entry points,
- * 1.04 sbvr_encode. */
+ * 1.04 sbvr_encode and sbvr_decompress_indexed. */
 int sbvr_version(void);
 
 /*
@@ -234,6 +234,15 @@ int sbvr_decompress(int O, int I, int k, const void *planes_dev, const void *coe
  * At most SBVR_ENCODE_MAX_ENTRIES grid entries ((n_ratio1 + n_ratio2) *
  * n_scale * n_bias); more is SBVR_E_UNSUPPORTED.
  */
+/*
+ * Prefill decompression of the coefficient-cache format: as sbvr_decompress
+ * with c[o][g][i] = table[index[o][g]][i] (zero for an index >= n_sets).
+ * planes_dev, index_dev, table_dev from sbvr_pack_indexed; W as for
+ * sbvr_decompress.
+ */
+int sbvr_decompress_indexed(int O, int I, int k, int n_sets, const void *planes_dev, const void *index_dev,
+                            const void *table_dev, uint16_t *W, hipStream_t stream);
+
 #define SBVR_ENCODE_MAX_ENTRIES 65536
 int sbvr_encode(int O, int I, int k, const float *W, int n_ratio1, int n_ratio2, int n_scale, int n_bias,
                 int normalise, uint32_t *planes_canon, uint16_t *coeffs_canon, double *mse,

@@ -31,6 +31,7 @@ EXPORTED = (
     "sbvr_workspace_bytes", "sbvr_pack", "sbvr_unpack", "sbvr_gemv", "sbvr_gemm_small_batch",
     "sbvr_decompress", "sbvr_gemv_a8", "sbvr_packed_index_bytes", "sbvr_packed_table_bytes",
     "sbvr_pack_indexed", "sbvr_unpack_indexed", "sbvr_gemv_indexed", "sbvr_gemv_indexed_a8", "sbvr_encode",
+    "sbvr_decompress_indexed",
 )
 
 
@@ -74,6 +75,7 @@ def _load():
         "sbvr_gemv_indexed": (i32, [i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, sz, vp]),
         "sbvr_gemv_indexed_a8": (i32, [i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, sz, vp]),
         "sbvr_encode": (i32, [i32, i32, i32, vp, i32, i32, i32, i32, i32, vp, vp, vp, vp]),
+        "sbvr_decompress_indexed": (i32, [i32, i32, i32, i32, vp, vp, vp, vp, vp]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -171,6 +173,10 @@ def sbvr_encode(O, I, k, W, n_ratio1, n_ratio2, n_scale, n_bias, normalise, plan
 
 def sbvr_decompress(O, I, k, planes_dev, coeffs_dev, W, stream=0) -> int:
     return _lib.sbvr_decompress(O, I, k, planes_dev, coeffs_dev, W, stream)
+
+
+def sbvr_decompress_indexed(O, I, k, n_sets, planes_dev, index_dev, table_dev, W, stream=0) -> int:
+    return _lib.sbvr_decompress_indexed(O, I, k, n_sets, planes_dev, index_dev, table_dev, W, stream)
 
 
 # --------------------------------------------------------------------------
@@ -354,13 +360,18 @@ def encode(W, k: int, n_ratio1: int = 8, n_ratio2: int = 8, n_scale: int = 16, n
     return (planes, coeffs, mse) if want_mse else (planes, coeffs)
 
 
-def decompress(W: PackedWeight, out=None, stream=None):
-    """The decoded matrix as fp16 [O][I] (prefill path)."""
+def decompress(W, out=None, stream=None):
+    """The decoded matrix as fp16 [O][I] (prefill path), for a PackedWeight or
+    an IndexedWeight."""
     torch = _torch()
     M = torch.empty((W.O, W.I), dtype=torch.float16, device=W.planes.device) if out is None else out
     assert M.dtype == torch.float16 and M.is_contiguous() and tuple(M.shape) == (W.O, W.I)
-    _check(sbvr_decompress(W.O, W.I, W.k, W.planes.data_ptr(), W.coeffs.data_ptr(), M.data_ptr(),
-                           _stream(stream)), "sbvr_decompress")
+    if isinstance(W, IndexedWeight):
+        _check(sbvr_decompress_indexed(W.O, W.I, W.k, W.n_sets, W.planes.data_ptr(), W.index.data_ptr(),
+                                       W.table.data_ptr(), M.data_ptr(), _stream(stream)), "sbvr_decompress_indexed")
+    else:
+        _check(sbvr_decompress(W.O, W.I, W.k, W.planes.data_ptr(), W.coeffs.data_ptr(), M.data_ptr(),
+                               _stream(stream)), "sbvr_decompress")
     return M
 
 

@@ -273,7 +273,23 @@ int sbvr_decompress(int O, int I, int k, const void *planes_dev, const void *coe
         return SBVR_E_INVALID_ARG;
     if (!aligned(planes_dev, 16) || !aligned(coeffs_dev, 16) || !aligned(W, 16))
         return SBVR_E_ALIGNMENT;
-    return launch_decompress(make_dims(O, I, k), planes_dev, coeffs_dev, W, stream);
+    return launch_decompress(make_dims(O, I, k), per_group_weights(planes_dev, coeffs_dev), W, stream);
+}
+
+int sbvr_decompress_indexed(int O, int I, int k, int n_sets, const void *planes_dev, const void *index_dev,
+                            const void *table_dev, uint16_t *W, hipStream_t stream)
+{
+    int st = check_shape(O, I, k);
+    if (st != SBVR_OK)
+        return st;
+    if ((st = check_sets(n_sets)) != SBVR_OK)
+        return st;
+    if (!planes_dev || !index_dev || !table_dev || !W)
+        return SBVR_E_INVALID_ARG;
+    if (!aligned(planes_dev, 16) || !aligned(index_dev, 16) || !aligned(table_dev, 16) || !aligned(W, 16))
+        return SBVR_E_ALIGNMENT;
+    return launch_decompress(make_dims(O, I, k), indexed_weights(planes_dev, index_dev, table_dev, n_sets), W,
+                             stream);
 }
 
 }  // extern "C"

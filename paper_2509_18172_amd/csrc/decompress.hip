@@ -23,9 +23,13 @@ namespace sbvr {
 // One workgroup per (tile, gblock) block; the plane words are loaded first so
 // that their latency overlaps the subset-sum table.  (Several blocks per
 // workgroup in a software pipeline measured slower.)
-template <int K>
+// IX: coefficient-cache format -- coeffs is then the device index blocks and
+// the coefficients come from table (n_sets sets of TABLE_STRIDE entries; an
+// index past the end gives zero coefficients).
+template <int K, bool IX>
 __global__ void __launch_bounds__(1024) decompress_kernel(Dims d, const uint32_t *__restrict__ planes,
                                                           const uint16_t *__restrict__ coeffs,
+                                                          const uint16_t *__restrict__ table, int n_sets,
                                                           uint16_t *__restrict__ W)
 {
     constexpr int TR = tile_rows(K), NSUB = 1 << K;
@@ -45,14 +49,24 @@ __global__ void __launch_bounds__(1024) decompress_kernel(Dims d, const uint32_t
     for (int i = 0; i < K; ++i)
         w[i] = pw[i * 4];
 
-    const uint16_t *cb = coeffs + blk * coeff_block_entries(K);
+    const uint16_t *cb = coeffs + blk * (IX ? index_block_entries(K) : coeff_block_entries(K));
     for (int e = t; e < TR * GB * NSUB; e += blockDim.x) {
         const int sub = e % NSUB, rb = e / NSUB, lb = rb % GB, lr = rb / GB;
+        int set = 0;
+        if constexpr (IX)
+            set = cb[index_entry(K, lr, lb)];
         double s = 0.0;  // exact: at most K binary16 terms
 #pragma unroll
-        for (int i = 0; i < K; ++i)
-            if ((sub >> i) & 1)
-                s += (double)half_bits_to_float(cb[coeff_entry(K, lr, lb, i)]);
+        for (int i = 0; i < K; ++i) {
+            if (!((sub >> i) & 1))
+                continue;
+            uint16_t c;
+            if constexpr (IX)
+                c = set < n_sets ? table[(size_t)set * TABLE_STRIDE + i] : (uint16_t)0;
+            else
+                c = cb[coeff_entry(K, lr, lb, i)];
+            s += (double)half_bits_to_float(c);
+        }
         lut[e] = f64_to_f16_rne(s);
     }
     __syncthreads();
@@ -70,17 +84,25 @@ __global__ void __launch_bounds__(1024) decompress_kernel(Dims d, const uint32_t
     *(uint4 *)(W + (size_t)o * d.I + (size_t)g * GROUP + wq * 32 + 8 * v) = make_uint4(out[0], out[1], out[2], out[3]);
 }
 
-int launch_decompress(const Dims &d, const void *planes_dev, const void *coeffs_dev, uint16_t *W,
-                      hipStream_t stream)
+template <bool IX>
+static const void *decompress_kernel_for(int k)
+{
+    return k == 4   ? (const void *)decompress_kernel<4, IX>
+           : k == 3 ? (const void *)decompress_kernel<3, IX>
+           : k == 2 ? (const void *)decompress_kernel<2, IX>
+                    : (const void *)decompress_kernel<1, IX>;
+}
+
+int launch_decompress(const Dims &d, const WeightRef &w, uint16_t *W, hipStream_t stream)
 {
     Dims dd = d;
-    const uint32_t *p = (const uint32_t *)planes_dev;
-    const uint16_t *c = (const uint16_t *)coeffs_dev;
-    void *args[] = {&dd, &p, &c, &W};
-    const void *fn = d.k == 4   ? (const void *)decompress_kernel<4>
-                     : d.k == 3 ? (const void *)decompress_kernel<3>
-                     : d.k == 2 ? (const void *)decompress_kernel<2>
-                                : (const void *)decompress_kernel<1>;
+    const uint32_t *p = (const uint32_t *)w.planes;
+    const bool ix = w.index != nullptr;
+    const uint16_t *c = (const uint16_t *)(ix ? w.index : w.coeffs);
+    const uint16_t *t = (const uint16_t *)w.table;
+    int n_sets = w.n_sets;
+    void *args[] = {&dd, &p, &c, &t, &n_sets, &W};
+    const void *fn = ix ? decompress_kernel_for<true>(d.k) : decompress_kernel_for<false>(d.k);
     const unsigned grid = (unsigned)((size_t)d.n_tiles * d.n_gblocks);
     return launch_kernel(fn, dim3(grid), dim3(64 * d.tr), 0, stream, args);
 }

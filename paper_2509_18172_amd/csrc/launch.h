@@ -51,8 +51,7 @@ int launch_pack_indexed(const Dims &d, int n_sets, const uint32_t *planes_canon,
 int launch_unpack_indexed(const Dims &d, int n_sets, const void *planes_dev, const void *index_dev,
                           const void *table_dev, uint32_t *planes_canon, uint16_t *index_canon,
                           uint16_t *table_canon, hipStream_t stream);
-int launch_decompress(const Dims &d, const void *planes_dev, const void *coeffs_dev, uint16_t *W,
-                      hipStream_t stream);
+int launch_decompress(const Dims &d, const WeightRef &w, uint16_t *W, hipStream_t stream);
 int launch_encode(int O, int I, int k, const float *W, int n_ratio1, int n_ratio2, int n_scale, int n_bias,
                   int normalise, uint32_t *planes, uint16_t *coeffs, double *mse, hipStream_t stream);
 int launch_gemm_sbs(const Dims &d, const void *planes_dev, const void *coeffs_dev,

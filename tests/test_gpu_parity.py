@@ -367,30 +367,52 @@ def test_output_canary_and_error_paths(sb):
     assert torch.all(buf == 5.0)
 
 
-def test_graph_capture_replays_match_eager(sb):
-    O, I = 4096, 4096
+@pytest.mark.parametrize("O,I", [(4096, 4096), (14336, 4096)])
+def test_graph_capture_replays_match_eager(sb, O, I):
+    """Every GEMV-type entry point (one-shot and streaming kernels) and the
+    decompression and encoding kernels, captured in one graph: each replay
+    reproduces the eager results bit for bit."""
     planes, coeffs = synth.random_sbvr(O, I, 4, seed=123)
     W = packed(sb, planes, coeffs)
+    n_sets = (O * (I // 128) + 9) // 10
+    pi, ix, tb = synth.random_indexed_sbvr(O, I, 4, n_sets, seed=126)
+    Wi = packed_indexed(sb, pi, ix, tb)
     x = dev(synth.activations(I, seed=124))
     X = dev(synth.activations(I, seed=125, batch=4))
-    y_eager = sb.gemv(W, x).clone()
-    Y_eager = sb.gemm_small_batch(W, X).clone()
-    y = torch.empty_like(y_eager)
-    Y = torch.empty_like(Y_eager)
+    Wf = dev(synth.weights(64, I, 0.02, seed=127))
+    calls = {
+        "gemv": lambda out=None: sb.gemv(W, x, out=out),
+        "small_batch": lambda out=None: sb.gemm_small_batch(W, X, out=out),
+        "a8": lambda out=None: sb.gemv_a8(W, x, out=out),
+        "indexed": lambda out=None: sb.gemv_indexed(Wi, x, out=out),
+        "indexed_a8": lambda out=None: sb.gemv_indexed(Wi, x, out=out, a8=True),
+        "decompress": lambda out=None: sb.decompress(W, out=out),
+        "decompress_indexed": lambda out=None: sb.decompress(Wi, out=out),
+    }
+    eager = {n: f().clone() for n, f in calls.items()}
+    ep, ec = sb.encode(Wf, 4)
+    outs = {n: torch.empty_like(v) for n, v in eager.items()}
+    enc_p, enc_c = torch.empty_like(ep), torch.empty_like(ec)
     s = torch.cuda.Stream()
     s.wait_stream(torch.cuda.current_stream())
+    torch.cuda.synchronize()
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g, stream=s):
-        sb.gemv(W, x, out=y)
-        sb.gemm_small_batch(W, X, out=Y)
+        for n, f in calls.items():
+            f(out=outs[n])
+        assert sb.sbvr_encode(64, I, 4, Wf.data_ptr(), 8, 8, 16, 4, 1, enc_p.data_ptr(), enc_c.data_ptr(), None,
+                              int(s.cuda_stream)) == 0
     for rep in range(4):
-        y.zero_()
-        Y.zero_()
+        for v in outs.values():
+            v.zero_()
+        enc_p.zero_()
+        enc_c.zero_()
         torch.cuda.synchronize()
         g.replay()
         torch.cuda.synchronize()
-        assert torch.equal(y, y_eager), rep
-        assert torch.equal(Y, Y_eager), rep
+        for n in calls:
+            assert torch.equal(outs[n], eager[n]), (n, rep)
+        assert torch.equal(enc_p, ep) and torch.equal(enc_c, ec), rep
         _ = (x.float() * 2).sum().item()  # eager work between replays
 
 
@@ -798,3 +820,27 @@ def test_indexed_error_paths_and_canary(sb):
     assert torch.all(buf == 5.0)
     assert sb.sbvr_packed_table_bytes(N, 4) == 8 * N and sb.sbvr_packed_table_bytes(0, 4) == 0
     assert sb.sbvr_packed_table_bytes(65537, 4) == 0
+
+
+@pytest.mark.parametrize("O,I,k,N", [(1, 128, 4, 1), (1001, 640, 3, 50), (4097, 1152, 2, 999), (33, 2560, 1, 7),
+                                     (4096, 4096, 4, 13108)])
+def test_decompress_indexed_bit_exact(sb, O, I, k, N):
+    """Prefill decompression of the cache format: bit-exact against rounding
+    the oracle's exact decoding of the gathered coefficients, and identical to
+    the per-group decompression of the same coefficients; indices past the
+    table decode with zero coefficients."""
+    planes, index, table = synth.random_indexed_sbvr(O, I, k, N, seed=3 * O + I + k)
+    rng = np.random.default_rng(O)
+    bad = rng.random(index.shape) < 0.02
+    index = index.copy()
+    index[bad] = N + rng.integers(0, 65536 - N, size=int(bad.sum())) if N < 65536 else index[bad]
+    coeffs = oracle.gather_coefficients(np.where(bad, 0, index), table)
+    coeffs[bad] = 0
+    Wi = packed_indexed(sb, planes, index, table)
+    M = sb.decompress(Wi)
+    torch.cuda.synchronize()
+    got = M.cpu().numpy().view(np.uint16)
+    assert np.array_equal(got, oracle_fp16(planes, coeffs))
+    Mp = sb.decompress(packed(sb, planes, coeffs))
+    torch.cuda.synchronize()
+    assert np.array_equal(got, Mp.cpu().numpy().view(np.uint16))
