@@ -26,8 +26,17 @@
 
 namespace sbvr {
 
-#ifndef SBVR_SBS_DEPTH
-#define SBVR_SBS_DEPTH 3
+// Ring depth: 3 when a workgroup streams many tiles (long item sequences per
+// wavefront), 2 otherwise (its shorter prologue wins when each wavefront has
+// only a few items).
+#ifndef SBVR_SBS_DEPTH_LONG
+#define SBVR_SBS_DEPTH_LONG 3
+#endif
+#ifndef SBVR_SBS_DEPTH_SHORT
+#define SBVR_SBS_DEPTH_SHORT 2
+#endif
+#ifndef SBVR_SBS_LONG_TPW
+#define SBVR_SBS_LONG_TPW 12
 #endif
 #ifndef SBVR_SBS_MAX_WAVES
 #define SBVR_SBS_MAX_WAVES 8
@@ -302,17 +311,25 @@ __global__ void __launch_bounds__(512) gemm_sbs_kernel(GemvArgs a)
 
 // Kernels are compiled for NB = 2, 4 and 8 vectors; a call with B vectors
 // runs the smallest NB >= B (absent vectors are neither read nor written).
-template <int K, int NB>
+template <int K, int NB, int D>
 static const void *sbs_kernel_for(bool multi)
 {
-    return multi ? (const void *)gemm_sbs_kernel<K, NB, SBVR_SBS_DEPTH, true>
-                 : (const void *)gemm_sbs_kernel<K, NB, SBVR_SBS_DEPTH, false>;
+    return multi ? (const void *)gemm_sbs_kernel<K, NB, D, true> : (const void *)gemm_sbs_kernel<K, NB, D, false>;
+}
+
+template <int K, int D>
+static const void *sbs_kernel_kd(int nb, bool multi)
+{
+    return nb == 2   ? sbs_kernel_for<K, 2, D>(multi)
+           : nb == 4 ? sbs_kernel_for<K, 4, D>(multi)
+                     : sbs_kernel_for<K, 8, D>(multi);
 }
 
 template <int K>
-static const void *sbs_kernel_k(int nb, bool multi)
+static const void *sbs_kernel_k(int nb, bool multi, bool long_ring)
 {
-    return nb == 2 ? sbs_kernel_for<K, 2>(multi) : nb == 4 ? sbs_kernel_for<K, 4>(multi) : sbs_kernel_for<K, 8>(multi);
+    return long_ring ? sbs_kernel_kd<K, SBVR_SBS_DEPTH_LONG>(nb, multi)
+                     : sbs_kernel_kd<K, SBVR_SBS_DEPTH_SHORT>(nb, multi);
 }
 
 int launch_gemm_sbs(const Dims &d, const void *planes_dev, const void *coeffs_dev,
@@ -331,10 +348,11 @@ int launch_gemm_sbs(const Dims &d, const void *planes_dev, const void *coeffs_de
     GemvArgs a = {(const uint4 *)planes_dev, (const uint16_t *)coeffs_dev, X, Y, d.O, d.I, d.k,
                   d.n_tiles, d.n_gblocks, gpw, B, tpw};
     const size_t lds = fixed + (size_t)tpw * per_tile;
-    const void *fn = d.k == 4   ? sbs_kernel_k<4>(nb, multi)
-                     : d.k == 3 ? sbs_kernel_k<3>(nb, multi)
-                     : d.k == 2 ? sbs_kernel_k<2>(nb, multi)
-                                : sbs_kernel_k<1>(nb, multi);
+    const bool long_ring = tpw >= SBVR_SBS_LONG_TPW;
+    const void *fn = d.k == 4   ? sbs_kernel_k<4>(nb, multi, long_ring)
+                     : d.k == 3 ? sbs_kernel_k<3>(nb, multi, long_ring)
+                     : d.k == 2 ? sbs_kernel_k<2>(nb, multi, long_ring)
+                                : sbs_kernel_k<1>(nb, multi, long_ring);
     void *args[] = {&a};
     return launch_kernel(fn, dim3(grid), dim3(64 * waves), lds, stream, args);
 }
