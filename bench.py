@@ -19,7 +19,8 @@ One JSON line is printed:
   decode_step   the L-layer graph alone: microseconds per token, GB/s
   per_call_us   mean duration of each projection's launch, from HIP events
                 around a graph of 64 back-to-back launches of that shape
-                cycling through >= 320 MB of distinct weight copies
+                cycling through >= 1 GB of distinct weight copies (median
+                of 11 replays after 2 warm-up replays)
   roofline      the dominant kernel instance (largest time per step):
                 algorithmic bytes per launch / its mean launch duration, vs the
                 8 TB/s HBM peak; traffic = calibrated FETCH_SIZE + WRITE_SIZE
@@ -167,8 +168,9 @@ def b1_kernel_instance(O: int, I: int, k: int, a8: bool = False, ix: bool = Fals
     """Name of the batch-1 kernel instance the library launches for an O x I
     matrix: the streaming kernel (ring depth D, several gblocks per wavefront
     or one) when a row has more than 16 gblocks of 512 elements or the matrix
-    has at least 24576 (tile, gblock) blocks (tiles of 16/k rows, 4 at k = 3);
-    otherwise the one-shot
+    has at least 24576 (tile, gblock) blocks (tiles of 16/k rows, 4 at k = 3),
+    ring depth 2, or 3 with several gblocks per wavefront and >= 8 tiles per
+    workgroup (256 workgroups); otherwise the one-shot
     kernel with T tiles per workgroup, the most of 8/4/2/1 that still leaves
     >= 256 workgroups.  The last two template arguments select the W4A8 build
     (activations converted online to SBVR-8) and the coefficient-cache format."""
@@ -178,12 +180,14 @@ def b1_kernel_instance(O: int, I: int, k: int, a8: bool = False, ix: bool = Fals
     n_tiles, n_gblocks = (O + tr - 1) // tr, (I + 511) // 512
     if n_gblocks > 16 or n_tiles * n_gblocks >= 24576:
         multi = n_gblocks > 16
-        return f"gemv_b1s_kernel<{k}, {3 if multi else 2}, {'true' if multi else 'false'}, {a8}, {ix}>"
+        tpw = (n_tiles + 255) // 256 if multi else 0
+        depth = (3 if tpw >= 8 else 2) if multi else 2
+        return f"gemv_b1s_kernel<{k}, {depth}, {'true' if multi else 'false'}, {a8}, {ix}>"
     T = next((t for t in (8, 4, 2) if n_tiles // t >= 256), 1)
     return f"gemv_b1_kernel<{k}, {T}, {a8}, {ix}>"
 
 
-ROTATE_BYTES = 320e6  # > 256 MB MALL + 8 x 4 MB L2
+ROTATE_BYTES = 1e9  # 4x the 256 MB MALL: a cyclic sweep gets no cache reuse
 
 
 def main():
@@ -318,11 +322,12 @@ def main():
 
     # ---- per-launch durations: >= 64 back-to-back launches per graph, cycling
     # through distinct weight copies totalling >= ROTATE_BYTES ----
-    def launch_us(calls, n_launch=64):
+    def launch_us(calls, n_launch=64, replays=11):
         g = capture([calls[i % len(calls)] for i in range(max(n_launch, len(calls)))])
         n = max(n_launch, len(calls))
-        timed(g.replay)
-        reps = [timed(g.replay) * 1e3 / n for _ in range(5)]
+        for _ in range(2):
+            timed(g.replay)
+        reps = [timed(g.replay) * 1e3 / n for _ in range(replays)]
         del g
         return float(np.median(reps))
 

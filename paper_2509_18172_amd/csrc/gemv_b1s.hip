@@ -37,6 +37,12 @@ constexpr int B1S_WAVE_LDS = 2048;  // per wavefront: [q][s][l][32 B]
 #ifndef SBVR_B1S_DEPTH
 #define SBVR_B1S_DEPTH 2
 #endif
+// With several gblocks per wavefront, a workgroup with fewer than this many
+// tiles runs the depth-2 ring (a wavefront's item runs are short there and
+// the shallower ring starts sooner; 8B down: 8.7 -> 8.3 us).
+#ifndef SBVR_B1S_SHORT_TPW
+#define SBVR_B1S_SHORT_TPW 8
+#endif
 #ifndef SBVR_B1S_DEPTH_MULTI
 #define SBVR_B1S_DEPTH_MULTI 3
 #endif
@@ -286,18 +292,20 @@ __global__ void __launch_bounds__(1024) gemv_b1s_kernel(GemvArgs a)
 }
 
 template <int K, bool A8, bool IX>
-static const void *b1s_kernel_for(bool multi)
+static const void *b1s_kernel_for(bool multi, bool short_run)
 {
-    return multi ? (const void *)gemv_b1s_kernel<K, SBVR_B1S_DEPTH_MULTI, true, A8, IX>
-                 : (const void *)gemv_b1s_kernel<K, SBVR_B1S_DEPTH, false, A8, IX>;
+    if (!multi)
+        return (const void *)gemv_b1s_kernel<K, SBVR_B1S_DEPTH, false, A8, IX>;
+    return short_run ? (const void *)gemv_b1s_kernel<K, 2, true, A8, IX>
+                     : (const void *)gemv_b1s_kernel<K, SBVR_B1S_DEPTH_MULTI, true, A8, IX>;
 }
 
 template <int K>
-static const void *b1s_kernel_for(bool multi, bool a8, bool ix)
+static const void *b1s_kernel_for(bool multi, bool short_run, bool a8, bool ix)
 {
     if (ix)
-        return a8 ? b1s_kernel_for<K, true, true>(multi) : b1s_kernel_for<K, false, true>(multi);
-    return a8 ? b1s_kernel_for<K, true, false>(multi) : b1s_kernel_for<K, false, false>(multi);
+        return a8 ? b1s_kernel_for<K, true, true>(multi, short_run) : b1s_kernel_for<K, false, true>(multi, short_run);
+    return a8 ? b1s_kernel_for<K, true, false>(multi, short_run) : b1s_kernel_for<K, false, false>(multi, short_run);
 }
 
 int launch_gemv_b1s(const Dims &d, const WeightRef &w, const uint16_t *x, uint16_t *y, bool a8,
@@ -314,10 +322,11 @@ int launch_gemv_b1s(const Dims &d, const WeightRef &w, const uint16_t *x, uint16
     const bool ix = w.index != nullptr;
     const size_t lds = (size_t)waves * B1S_WAVE_LDS + (size_t)tpw * waves * d.tr * 4;
     const bool multi = gpw > 1;
-    const void *fn = d.k == 4   ? b1s_kernel_for<4>(multi, a8, ix)
-                     : d.k == 3 ? b1s_kernel_for<3>(multi, a8, ix)
-                     : d.k == 2 ? b1s_kernel_for<2>(multi, a8, ix)
-                                : b1s_kernel_for<1>(multi, a8, ix);
+    const bool short_run = tpw < SBVR_B1S_SHORT_TPW;
+    const void *fn = d.k == 4   ? b1s_kernel_for<4>(multi, short_run, a8, ix)
+                     : d.k == 3 ? b1s_kernel_for<3>(multi, short_run, a8, ix)
+                     : d.k == 2 ? b1s_kernel_for<2>(multi, short_run, a8, ix)
+                                : b1s_kernel_for<1>(multi, short_run, a8, ix);
     void *args[] = {&a};
     return launch_kernel(fn, dim3(grid), dim3(64 * waves), lds, stream, args);
 }

@@ -15,7 +15,8 @@ import bench  # noqa: E402
     (4096, 4096, "gemv_b1_kernel<4, 4, false, false>"),      # 8192 blocks: one-shot, 1024 tiles -> T = 4
     (1024, 4096, "gemv_b1_kernel<4, 1, false, false>"),
     (14336, 4096, "gemv_b1s_kernel<4, 2, false, false, false>"),  # 28672 blocks: streaming
-    (4096, 14336, "gemv_b1s_kernel<4, 3, true, false, false>"),   # 28 gblocks per row
+    (4096, 14336, "gemv_b1s_kernel<4, 2, true, false, false>"),   # 28 gblocks per row, 4 tiles per workgroup
+    (8192, 28672, "gemv_b1s_kernel<4, 3, true, false, false>"),   # 56 gblocks per row, 8 tiles per workgroup
     (8192, 8192, "gemv_b1s_kernel<4, 2, false, false, false>"),
     (1024, 8192, "gemv_b1_kernel<4, 1, false, false>"),
 ])
