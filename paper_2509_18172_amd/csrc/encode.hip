@@ -104,6 +104,16 @@ __device__ __forceinline__ int nearest(const double *sums, double x, double &dif
     return best;
 }
 
+constexpr int ENC_CHUNK = 16;  // elements between pruning checks
+
+__device__ __forceinline__ double wave_min_f64(double v)
+{
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1)
+        v = fmin(v, __shfl_xor(v, off));
+    return v;
+}
+
 template <int K>
 __device__ __forceinline__ double entry_mse(const double *D, const double *sums)
 {
@@ -193,23 +203,51 @@ __global__ void __launch_bounds__(ENC_THREADS) encode_kernel(EncodeArgs a)
         b = b_min + (double)kb * b_gran;
     };
 
+    // Pruning (exact): an entry's error sum only grows as elements are added
+    // (the terms are >= 0 and rounding is monotone), so once err / n exceeds
+    // the smallest MSE any lane has completed, the entry's final MSE is
+    // strictly larger than that and it can neither win nor tie; its remaining
+    // elements are skipped.  Lanes share their best MSE after every round of
+    // 64 entries.
     double best_mse = __builtin_inf();
     int best_e = -1;
-    for (int e = lane; e < n_entries; e += ENC_THREADS) {
-        double r, s, b;
-        entry_rsb(e, r, s, b);
-        if (!(s > 0.0))
-            continue;
-        uint16_t c[K];
-        if (!entry_coeffs<K>(r, s, b, a.normalise != 0, c))
-            continue;
+    double shared_best = __builtin_inf();
+    for (int e0 = 0; e0 < n_entries; e0 += ENC_THREADS) {
+        const int e = e0 + lane;
+        bool ok = false;
         double sums[1 << K];
-        subset_sums<K>(c, sums);
-        const double mse = entry_mse<K>(D, sums);
-        if (mse < best_mse) {
-            best_mse = mse;
-            best_e = e;
+        if (e < n_entries) {
+            double r, s, b;
+            entry_rsb(e, r, s, b);
+            uint16_t c[K];
+            ok = s > 0.0 && entry_coeffs<K>(r, s, b, a.normalise != 0, c);
+            if (ok)
+                subset_sums<K>(c, sums);
         }
+        if (ok) {
+            double err = 0.0;
+            bool pruned = false;
+            for (int j0 = 0; j0 < GROUP; j0 += ENC_CHUNK) {
+#pragma unroll 4
+                for (int j = j0; j < j0 + ENC_CHUNK; ++j) {
+                    double d;
+                    nearest<K>(sums, D[j], d);
+                    err += d * d;
+                }
+                if (err / (double)GROUP > shared_best) {
+                    pruned = true;
+                    break;
+                }
+            }
+            if (!pruned) {
+                const double mse = err / (double)GROUP;
+                if (mse < best_mse) {
+                    best_mse = mse;
+                    best_e = e;
+                }
+            }
+        }
+        shared_best = wave_min_f64(fmin(shared_best, best_mse));
     }
     best_mse_l[lane] = best_mse;
     best_e_l[lane] = best_e;
