@@ -111,3 +111,54 @@ def test_algorithmic_bytes_formula():
     assert sb.algorithmic_bytes(14336, 4096, 4) == 33_067_008
     assert sb.algorithmic_bytes(28672, 8192, 4) == 132_194_304
     assert sb.algorithmic_bytes(4096, 4096, 4, B=8) == 9_568_256
+
+
+def test_element_count_limit():
+    """O * I must stay below 2^31 (the kernels' element offsets are 32-bit):
+    the size queries return 0 and every entry point rejects the shape before
+    touching any pointer."""
+    big = [(32768, 65536), (65536, 32768), (16384, 131072)]
+    for O, I in big:
+        assert sb.sbvr_packed_plane_bytes(O, I, 4) == 0
+        assert sb.sbvr_packed_index_bytes(O, I, 4) == 0
+        assert gemv(O=O, I=I) == sb.SBVR_E_UNSUPPORTED
+        assert sb.sbvr_gemv_a8(O, I, 4, FAKE, FAKE, FAKE, FAKE, None, 0, 0) == sb.SBVR_E_UNSUPPORTED
+        assert sb.sbvr_encode(O, I, 4, FAKE, 8, 8, 16, 4, 1, FAKE, FAKE, None, 0) == sb.SBVR_E_UNSUPPORTED
+    # the largest accepted shape
+    assert sb.sbvr_packed_plane_bytes(16383, 131072, 4) == (16383 + 3) // 4 * 256 * 4 * 4 * 4 * 16
+
+
+def test_new_entry_points_validation():
+    a8 = lambda **kw: sb.sbvr_gemv_a8(kw.get("O", 16), kw.get("I", 256), kw.get("k", 4), kw.get("p", FAKE),
+                                      FAKE, kw.get("x", FAKE), FAKE, None, 0, 0)
+    assert a8(O=0) == sb.SBVR_E_INVALID_ARG
+    assert a8(k=5) == sb.SBVR_E_UNSUPPORTED
+    assert a8(p=None) == sb.SBVR_E_INVALID_ARG
+    assert a8(x=FAKE + 2) == sb.SBVR_E_ALIGNMENT
+    ix = lambda **kw: sb.sbvr_gemv_indexed(16, kw.get("I", 256), 4, kw.get("N", 10), FAKE, kw.get("i", FAKE),
+                                           kw.get("t", FAKE), FAKE, FAKE, None, 0, 0)
+    assert ix(N=0) == sb.SBVR_E_INVALID_ARG
+    assert ix(N=65537) == sb.SBVR_E_INVALID_ARG
+    assert ix(I=200) == sb.SBVR_E_INVALID_ARG
+    assert ix(i=None) == sb.SBVR_E_INVALID_ARG
+    assert ix(i=FAKE + 2) == sb.SBVR_E_ALIGNMENT
+    assert ix(t=FAKE + 8) == sb.SBVR_E_ALIGNMENT
+    assert sb.sbvr_gemv_indexed_a8(16, 256, 4, 0, FAKE, FAKE, FAKE, FAKE, FAKE, None, 0, 0) == sb.SBVR_E_INVALID_ARG
+    assert sb.sbvr_decompress_indexed(16, 256, 4, 0, FAKE, FAKE, FAKE, FAKE, 0) == sb.SBVR_E_INVALID_ARG
+    assert sb.sbvr_decompress_indexed(16, 256, 4, 5, FAKE, FAKE, FAKE, FAKE + 2, 0) == sb.SBVR_E_ALIGNMENT
+    pk = lambda **kw: sb.sbvr_pack_indexed(8, 256, 3, kw.get("N", 4), FAKE, kw.get("ic", FAKE), FAKE, FAKE,
+                                           kw.get("id", FAKE), FAKE, 0)
+    assert pk(N=0) == sb.SBVR_E_INVALID_ARG
+    assert pk(ic=FAKE + 1) == sb.SBVR_E_ALIGNMENT
+    assert pk(id=FAKE + 2) == sb.SBVR_E_ALIGNMENT
+    assert sb.sbvr_packed_table_bytes(3, 4) == 24 and sb.sbvr_packed_table_bytes(3, 9) == 0
+    enc = lambda **kw: sb.sbvr_encode(4, 256, kw.get("k", 4), kw.get("W", FAKE), kw.get("n1", 8), 8, 16,
+                                      kw.get("nb", 4), kw.get("norm", 1), FAKE, FAKE, kw.get("m", None), 0)
+    assert enc(k=0) == sb.SBVR_E_INVALID_ARG
+    assert enc(n1=0) == sb.SBVR_E_INVALID_ARG
+    assert enc(nb=-1) == sb.SBVR_E_INVALID_ARG
+    assert enc(norm=3) == sb.SBVR_E_INVALID_ARG
+    assert enc(n1=1100) == sb.SBVR_E_UNSUPPORTED  # (1100 + 8) * 16 * 4 > 65536 entries
+    assert enc(W=None) == sb.SBVR_E_INVALID_ARG
+    assert enc(W=FAKE + 2) == sb.SBVR_E_ALIGNMENT
+    assert enc(m=FAKE + 4) == sb.SBVR_E_ALIGNMENT

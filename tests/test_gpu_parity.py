@@ -844,3 +844,24 @@ def test_decompress_indexed_bit_exact(sb, O, I, k, N):
     Mp = sb.decompress(packed(sb, planes, coeffs))
     torch.cuda.synchronize()
     assert np.array_equal(got, Mp.cpu().numpy().view(np.uint16))
+
+
+def test_largest_accepted_shape_sampled_rows(sb):
+    """O * I just below 2^31 (the largest shape the library accepts; 1.2 GB of
+    packed weights, 256 gblocks per row): batch 1, W4A8 and B = 8 against the
+    oracle on sampled rows, including the first and last."""
+    O, I, k = 16383, 131072, 4
+    assert O * I < 2 ** 31 - 1
+    planes, coeffs = synth.random_sbvr(O, I, k, seed=2024)
+    W = packed(sb, planes, coeffs)
+    rows = np.unique(np.r_[0, 1, O - 2, O - 1, np.random.default_rng(0).integers(0, O, 44)])
+    x = synth.activations(I, seed=2025)
+    y = run_gemv(sb, W, x)
+    assert rel_err(y[rows], oracle.sbvr_gemv(planes, coeffs, x, rows=rows)) <= TOL
+    y8 = run_gemv_a8(sb, W, x)
+    assert rel_err(y8[rows], oracle.sbvr_gemv_w4a8(planes, coeffs, x, rows=rows)) <= TOL
+    X = synth.activations(I, seed=2026, batch=8)
+    Y = run_gemm(sb, W, X)
+    Y_ref = oracle.sbvr_gemv(planes, coeffs, X, rows=rows)
+    assert max(rel_err(Y[b][rows], Y_ref[b]) for b in range(8)) <= TOL
+    log(f"largest shape {O}x{I}: sampled rows within {TOL}")
