@@ -17,6 +17,7 @@ tests run these same shapes and launch configurations against the CPU oracle.
 One JSON line is printed:
   value         aggregate algorithmic HBM throughput (GB/s) of the timed steps
   decode_step   the L-layer graph alone: microseconds per token, GB/s
+  decode_step_w4a8  the same graph with SBVR-8 activations (sbvr_gemv_a8)
   per_call_us   mean duration of each projection's launch, from HIP events
                 around a graph of 64 back-to-back launches of that shape
                 cycling through >= 1 GB of distinct weight copies (median
@@ -319,6 +320,16 @@ def main():
                    "gbps": round(layer_bytes * L / (decode_us * 1e3), 1),
                    "replays": len(step_reps)}
     del decode_graph, layer_graphs
+    # the same decode step with SBVR-8 activations (the paper's W4A8 decode)
+    decode_step_a8 = None
+    if not args.quick:
+        a8_graph = capture([((lambda W, x, y, stream: sb.gemv_a8(W, x, out=y, stream=stream)), layers[li][n])
+                            for li in range(L) for n in PROJ_ORDER])
+        timed(a8_graph.replay)
+        reps = [timed(a8_graph.replay) * 1e3 for _ in range(5)]
+        us = float(np.median(reps))
+        decode_step_a8 = {"us_per_token": round(us, 2), "gbps": round(layer_bytes * L / (us * 1e3), 1)}
+        del a8_graph
 
     # ---- per-launch durations: >= 64 back-to-back launches per graph, cycling
     # through distinct weight copies totalling >= ROTATE_BYTES ----
@@ -569,6 +580,7 @@ def main():
         "per_call_gbps": {n: round(v, 1) for n, v in per_call_gbps.items()},
         "roofline": roofline,
         "decode_step": decode_step,
+        "decode_step_w4a8": decode_step_a8,
         "small_batch": small_batch or None,
         "w4a8": w4a8 or None,
         "indexed": indexed,
