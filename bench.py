@@ -181,7 +181,7 @@ def b1_kernel_instance(O: int, I: int, k: int, a8: bool = False, ix: bool = Fals
     n_tiles, n_gblocks = (O + tr - 1) // tr, (I + 511) // 512
     if n_gblocks > 16 or n_tiles * n_gblocks >= 24576:
         multi = n_gblocks > 16
-        tpw = (n_tiles + 255) // 256 if multi else 0
+        tpw = (n_tiles + 255) // 256
         depth = (3 if tpw >= 8 else 2) if multi else 2
         return f"gemv_b1s_kernel<{k}, {depth}, {'true' if multi else 'false'}, {a8}, {ix}>"
     T = next((t for t in (8, 4, 2) if n_tiles // t >= 256), 1)

@@ -49,8 +49,9 @@ constexpr int B1S_WAVE_LDS = 2048;  // per wavefront: [q][s][l][32 B]
 #ifndef SBVR_B1S_MAX_WAVES
 #define SBVR_B1S_MAX_WAVES 16
 #endif
-// Workgroups per launch: two resident per CU with one gblock per wavefront;
-// one per CU (longer item streams per wavefront) with several.
+// Workgroups per launch: with one gblock per wavefront, two resident per CU
+// (half as many for workgroups of more than 8 wavefronts); one per CU
+// (longer item streams per wavefront) with several gblocks per wavefront.
 #ifndef SBVR_B1S_GROUPS
 #define SBVR_B1S_GROUPS 512
 #endif
@@ -313,7 +314,10 @@ int launch_gemv_b1s(const Dims &d, const WeightRef &w, const uint16_t *x, uint16
 {
     const int gpw = (d.n_gblocks + SBVR_B1S_MAX_WAVES - 1) / SBVR_B1S_MAX_WAVES;
     const int waves = (d.n_gblocks + gpw - 1) / gpw;
-    const int groups = gpw > 1 ? SBVR_B1S_GROUPS_MULTI : SBVR_B1S_GROUPS;
+    // one gblock per wavefront: about 16 wavefronts per CU -- 512 workgroups of
+    // up to 8 wavefronts, 256 of more (70B q/o, gate/up: 8.4 -> 8.1 us,
+    // 22.3 -> 22.1 us)
+    const int groups = gpw > 1 ? SBVR_B1S_GROUPS_MULTI : (waves > 8 ? SBVR_B1S_GROUPS / 2 : SBVR_B1S_GROUPS);
     const int tpw = (d.n_tiles + groups - 1) / groups;
     const int grid = (d.n_tiles + tpw - 1) / tpw;
     GemvArgs a = {(const uint4 *)w.planes, (const uint16_t *)w.coeffs, x, y, d.O, d.I, d.k,
