@@ -26,7 +26,9 @@ One JSON line is printed:
                 algorithmic bytes per launch / its mean launch duration, vs the
                 8 TB/s HBM peak; traffic = calibrated FETCH_SIZE + WRITE_SIZE
                 bytes per launch from the recorded counter runs, when they were
-                taken on the current kernel sources (else null)
+                taken on the current kernel sources (else null);
+                practical_peak = a plain streaming read of the same bytes per
+                launch, timed the same way (frac = its time / the kernel's)
   small_batch   per projection at B = 2, 4, 8 activation vectors
                 (sbvr_gemm_small_batch), same timing
   w4a8          per projection, batch 1 with the activations converted online
@@ -387,6 +389,38 @@ def main():
         "bytes_per_launch": round(db / dc),
         "mean_launch_us": round(dt / dc, 3),
     }
+
+    # ---- practical ceiling: a plain streaming read of the same bytes (the
+    # helper in read_probe.hip), grid-interleaved and chunked per workgroup ----
+    def stream_read_us(nbytes):
+        import ctypes as C
+        from paper_2509_18172_amd.build import probe_path
+        probe = C.CDLL(probe_path())
+        probe.sbvr_probe_stream_read.argtypes = [C.c_void_p, C.c_size_t, C.c_int, C.c_void_p, C.c_void_p]
+        n16 = (nbytes + 15) // 16 * 16
+        copies_r = max(2, int(np.ceil(ROTATE_BYTES / n16)))
+        buf = torch.ones(copies_r * n16, dtype=torch.uint8, device=dev)
+        sink = torch.zeros(4, dtype=torch.int32, device=dev)
+        res = {}
+        def read(off, chunked, stream):
+            st = probe.sbvr_probe_stream_read(buf.data_ptr() + off, n16, chunked, sink.data_ptr(),
+                                              stream.cuda_stream)
+            if st != 0:
+                raise RuntimeError(f"stream-read probe launch failed ({st})")
+
+        for tag, chunked in (("interleaved", 0), ("chunked", 1)):
+            res[tag] = launch_us([(read, (i * n16, chunked)) for i in range(copies_r)])
+        del buf
+        return res
+
+    ceiling = stream_read_us(roofline["bytes_per_launch"])
+    best = min(ceiling.values())
+    roofline["practical_peak"] = {
+        "what": "plain streaming read of the same bytes per launch (16-byte loads, same 64-launch graphs, "
+                ">= 1 GB rotation)",
+        "read_us": {kk: round(v, 3) for kk, v in ceiling.items()},
+        "gbps": round(roofline["bytes_per_launch"] / (best * 1e3), 1),
+        "frac": round(best / roofline["mean_launch_us"], 4)}
 
     def gemm_call(W, X, Y):
         return (lambda W, X, Y, stream: sb.gemm_small_batch(W, X, out=Y, stream=stream)), (W, X, Y)

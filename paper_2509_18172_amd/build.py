@@ -26,6 +26,26 @@ def library_path() -> str:
     return os.path.join(HERE, "_lib", "libsbvr.so")
 
 
+def probe_path() -> str:
+    """The streaming-read measurement helper the benchmark loads (not part of
+    the library)."""
+    return os.path.join(HERE, "_lib", "libsbvr_probe.so")
+
+
+def build_probe(verbose: bool = False) -> str:
+    out = probe_path()
+    os.makedirs(os.path.dirname(out), exist_ok=True)
+    tmp = out + ".tmp%d" % os.getpid()
+    cmd = [HIPCC, *FLAGS, os.path.join(HERE, "csrc", "read_probe.hip"), "-o", tmp]
+    if verbose:
+        print(" ".join(cmd))
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("hipcc failed:\n" + " ".join(cmd) + "\n" + r.stdout + r.stderr)
+    os.replace(tmp, out)
+    return out
+
+
 def build(verbose: bool = False, out: str | None = None, defines=(), jobs: int = 0) -> str:
     """Compile every source to an object (in parallel), then link libsbvr.so."""
     from concurrent.futures import ThreadPoolExecutor
@@ -65,3 +85,4 @@ def build(verbose: bool = False, out: str | None = None, defines=(), jobs: int =
 
 if __name__ == "__main__":
     print(build(verbose=True))
+    print(build_probe(verbose=True))

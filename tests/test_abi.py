@@ -162,3 +162,19 @@ def test_new_entry_points_validation():
     assert enc(W=None) == sb.SBVR_E_INVALID_ARG
     assert enc(W=FAKE + 2) == sb.SBVR_E_ALIGNMENT
     assert enc(m=FAKE + 4) == sb.SBVR_E_ALIGNMENT
+
+
+def test_read_probe_loads_and_rejects_bad_arguments():
+    """The benchmark's streaming-read helper: it loads, and rejects a null
+    pointer or a size that is not a multiple of 16 before any launch."""
+    from paper_2509_18172_amd.build import probe_path
+    probe = C.CDLL(probe_path())
+    fn = probe.sbvr_probe_stream_read
+    fn.argtypes = [C.c_void_p, C.c_size_t, C.c_int, C.c_void_p, C.c_void_p]
+    fn.restype = C.c_int
+    buf = (C.c_ubyte * 64)()
+    sink = (C.c_uint * 4)()
+    assert fn(None, 64, 0, C.addressof(sink), None) == -1
+    assert fn(C.addressof(buf), 0, 0, C.addressof(sink), None) == -1
+    assert fn(C.addressof(buf), 24, 1, C.addressof(sink), None) == -1
+    assert fn(C.addressof(buf), 64, 0, None, None) == -1
