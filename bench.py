@@ -46,7 +46,9 @@ One JSON line is printed:
                 fp32 q/o-shaped matrix: seconds and groups per second, and the
                 CPU oracle's encoder on a sample of its rows
   cpu_baseline  the CPU oracle (binary64 decompress + GEMV) on layer 0's seven
-                GEMVs, bounded to ~10 s of work, in the same unit
+                GEMVs, bounded to ~10 s of work, in the same unit, on all host
+                threads; one_core: the same oracle on one thread over the q
+                projection (~2.5 s); cpu_model from /proc/cpuinfo
 
 --traffic-probe runs, eagerly, four launches of every projection shape (fp16
 and W4A8 activations, and the coefficient-cache format) and an elementwise
@@ -191,6 +193,17 @@ def b1_kernel_instance(O: int, I: int, k: int, a8: bool = False, ix: bool = Fals
 
 
 ROTATE_BYTES = 1e9  # 4x the 256 MB MALL: a cyclic sweep gets no cache reuse
+
+
+def cpu_model_name():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
 
 
 def main():
@@ -583,11 +596,26 @@ def main():
                 elapsed += time.perf_counter() - ts
                 done_bytes += nbytes[name]
             passes += 1
+        # the same oracle on one thread, over layer 0's q projection
+        one_bytes, one_el, one_passes = 0, 0.0, 0
+        planes, coeffs = host_layer0["q"]
+        xq = layers[0]["q"][1].cpu().numpy()
+        while one_el < args.cpu_seconds / 4 or one_passes == 0:
+            ts = time.perf_counter()
+            oracle.sbvr_gemv(planes, coeffs, xq, nthreads=1)
+            one_el += time.perf_counter() - ts
+            one_bytes += nbytes["q"]
+            one_passes += 1
         cpu = {"value": round(done_bytes / elapsed / 1e9, 4), "unit": "GB/s", "cores": threads,
                "kind": "oracle",
                "sample": f"{passes} pass(es) over layer 0's seven GEMVs ({args.model}, k={k}, batch 1): "
                          f"{elapsed:.1f} s of binary64 decompress + GEMV on {threads} threads "
-                         f"({os.cpu_count()} host CPUs, {platform.machine()})"}
+                         f"({os.cpu_count()} host CPUs, {platform.machine()})",
+               "cpu_model": cpu_model_name(),
+               "one_core": {"value": round(one_bytes / one_el / 1e9, 4), "unit": "GB/s",
+                            "us_per_gemv": round(one_el / one_passes * 1e6, 1),
+                            "sample": f"{one_passes} q GEMV(s) ({shapes['q'][0]}x{shapes['q'][1]}), "
+                                      f"{one_el:.1f} s on 1 thread"}}
 
     out = {
         "metric": "SBVR GEMV us/call and achieved HBM GB/s (% of MI355X peak), 4-bit, batch 1",

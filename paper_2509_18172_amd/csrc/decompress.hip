@@ -5,92 +5,160 @@
 // it once to binary16 (to nearest, ties to even) gives the correctly rounded
 // weight -- the same as rounding the exact decoded value.
 //
-// Workgroup = one (tile, gblock) block of the device format: TR rows x 512
-// columns.  Each of its TR x 4 (row, group) pairs has 2^k distinct decoded
-// values (the subset sums); the workgroup rounds them once into an LDS table
-// (one entry per thread), then thread = 8 consecutive columns of one row
-// gathers its k plane words (the device bit layout puts element 8v+p of a
-// word at bit 4p+v, so (w >> v) & 0x11111111 holds its 8 bits in nibbles
-// 0..7), forms the 4-bit subset index of each element and looks it up, and
-// writes 16 bytes.  HBM-bound: per weight it reads k/8 + 2k/128 bytes and
-// writes 2.
+// A (tile, gblock) block of the device format is TR rows x 512 columns.  Each
+// of its TR x 4 (row, group) pairs has 2^k distinct decoded values (the subset
+// sums), rounded once into an LDS table; then a lane = 8 consecutive columns
+// of one row takes its k plane words (the device bit layout puts element 8v+p
+// of a word at bit 4p+v, so (w >> v) & 0x11111111 holds its 8 bits in nibbles
+// 0..7), forms the subset index of each element, looks it up and writes 16
+// bytes.  HBM-bound: per weight it reads k/8 + 2k/128 bytes and writes 2.
 #include "device_ops.h"
 #include "f16_round.h"
 #include "launch.h"
 
 namespace sbvr {
 
-// One workgroup per (tile, gblock) block; the plane words are loaded first so
-// that their latency overlaps the subset-sum table.  (Several blocks per
-// workgroup in a software pipeline measured slower.)
+// Broadcast within each quad of lanes: every lane gets lane i's value.
+__device__ __forceinline__ uint32_t quad_bcast(uint32_t v, int i)
+{
+    switch (i) {
+    case 0:
+        return __builtin_amdgcn_update_dpp(0u, v, 0x00, 0xf, 0xf, false);  // quad_perm [0,0,0,0]
+    case 1:
+        return __builtin_amdgcn_update_dpp(0u, v, 0x55, 0xf, 0xf, false);  // [1,1,1,1]
+    case 2:
+        return __builtin_amdgcn_update_dpp(0u, v, 0xaa, 0xf, 0xf, false);  // [2,2,2,2]
+    default:
+        return __builtin_amdgcn_update_dpp(0u, v, 0xff, 0xf, 0xf, false);  // [3,3,3,3]
+    }
+}
+
+// A workgroup decodes NB consecutive gblocks of one tile; wavefront r of the
+// workgroup is row r of the tile.
+//   * Plane words: lane (slot b, word wq, v) loads word wq of plane v, so a
+//     group slot's 16 lanes read its 64 contiguous bytes with one load, and
+//     the quad (b, wq) then holds word wq of every plane; each lane takes all
+//     k of them from its quad by DPP broadcasts.
+//   * Table: wavefront r builds the 4 x 2^k entries of its own row (lane l:
+//     slot l / 2^k, subset l % 2^k) from the row's coefficients, read as one
+//     contiguous run per slot.  Only that wavefront reads them back, so no
+//     workgroup barrier is needed: one wavefront's LDS operations complete in
+//     order.
+//   * Output: 16 bytes per lane and gblock, stored non-temporally (the matrix
+//     is written once and read later by the GEMM).
 // IX: coefficient-cache format -- coeffs is then the device index blocks and
 // the coefficients come from table (n_sets sets of TABLE_STRIDE entries; an
 // index past the end gives zero coefficients).
-template <int K, bool IX>
+template <int K, bool IX, int NB>
 __global__ void __launch_bounds__(1024) decompress_kernel(Dims d, const uint32_t *__restrict__ planes,
                                                           const uint16_t *__restrict__ coeffs,
                                                           const uint16_t *__restrict__ table, int n_sets,
                                                           uint16_t *__restrict__ W)
 {
-    constexpr int TR = tile_rows(K), NSUB = 1 << K;
-    __shared__ uint16_t lut[TR * GB * NSUB];  // [row][group slot][subset]
-    const size_t blk = blockIdx.x;
-    const int tile = (int)(blk / d.n_gblocks), gb = (int)(blk % d.n_gblocks);
-    const int t = threadIdx.x;
-    const int r = t >> 6, c8 = t & 63;  // row in the tile, 8-column chunk in the gblock
-    const int b = c8 >> 4;               // group slot
-    const int wq = (c8 & 15) >> 2;       // word of the group
-    const int v = c8 & 3;                // elements 8v .. 8v+7 of the word
-    const int o = tile * TR + r, g = gb * GB + b;
-    // plane words first (padding rows and groups of the block are zero)
-    const uint32_t *pw = planes + blk * plane_block_words(K) + (size_t)((b * TR + r) * K) * 4 + wq;
-    uint32_t w[K];
-#pragma unroll
-    for (int i = 0; i < K; ++i)
-        w[i] = pw[i * 4];
+    constexpr int TR = tile_rows(K), NSUB = 1 << K, NE = TR * GB * NSUB, ROW_E = GB * NSUB;
+    __shared__ uint16_t lut[NB][NE];  // [gblock][row][group slot][subset]
+    const int gpt = (d.n_gblocks + NB - 1) / NB;
+    const int tile = (int)(blockIdx.x / gpt), gb0 = (int)(blockIdx.x % gpt) * NB;
+    const int r = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int b = lane >> 4;         // group slot
+    const int wq = (lane & 15) >> 2; // word of the group
+    const int v = lane & 3;          // elements 8v .. 8v+7 of the word; plane v for the load
+    const int o = tile * TR + r;
+    const size_t blk0 = (size_t)tile * d.n_gblocks + gb0;
 
-    const uint16_t *cb = coeffs + blk * (IX ? index_block_entries(K) : coeff_block_entries(K));
-    for (int e = t; e < TR * GB * NSUB; e += blockDim.x) {
-        const int sub = e % NSUB, rb = e / NSUB, lb = rb % GB, lr = rb / GB;
-        int set = 0;
-        if constexpr (IX)
-            set = cb[index_entry(K, lr, lb)];
+    // plane words first, so that their latency overlaps the table
+    uint32_t mine[NB];
+#pragma unroll
+    for (int u = 0; u < NB; ++u) {
+        const bool ok = gb0 + u < d.n_gblocks && v < K;
+        mine[u] = ok ? planes[(blk0 + u) * plane_block_words(K) + (size_t)((b * TR + r) * K + v) * 4 + wq] : 0u;
+    }
+
+    for (int e2 = lane; e2 < NB * ROW_E; e2 += 64) {
+        const int u = e2 / ROW_E, lb = (e2 % ROW_E) / NSUB, sub = e2 % NSUB;
+        if (gb0 + u >= d.n_gblocks)
+            continue;
+        const uint16_t *cb = coeffs + (blk0 + u) * (IX ? index_block_entries(K) : coeff_block_entries(K));
+        uint16_t c[K];
+        if constexpr (IX) {
+            const int set = cb[index_entry(K, r, lb)];
+            const bool in = set < n_sets;
+#pragma unroll
+            for (int i = 0; i < K; ++i)
+                c[i] = in ? table[(size_t)set * TABLE_STRIDE + i] : (uint16_t)0;
+        } else {
+            const uint16_t *cp = cb + coeff_entry(K, r, lb, 0);  // the row's K entries are contiguous
+            if constexpr (K == 4) {
+                const uint2 q = *(const uint2 *)cp;  // 8-byte aligned: entry (r * GB + lb) * 4
+                c[0] = (uint16_t)(q.x & 0xffffu);
+                c[1] = (uint16_t)(q.x >> 16);
+                c[2] = (uint16_t)(q.y & 0xffffu);
+                c[3] = (uint16_t)(q.y >> 16);
+            } else {
+#pragma unroll
+                for (int i = 0; i < K; ++i)
+                    c[i] = cp[i];
+            }
+        }
         double s = 0.0;  // exact: at most K binary16 terms
 #pragma unroll
-        for (int i = 0; i < K; ++i) {
-            if (!((sub >> i) & 1))
-                continue;
-            uint16_t c;
-            if constexpr (IX)
-                c = set < n_sets ? table[(size_t)set * TABLE_STRIDE + i] : (uint16_t)0;
-            else
-                c = cb[coeff_entry(K, lr, lb, i)];
-            s += (double)half_bits_to_float(c);
-        }
-        lut[e] = f64_to_f16_rne(s);
+        for (int i = 0; i < K; ++i)
+            s += ((sub >> i) & 1) ? (double)half_bits_to_float(c[i]) : 0.0;
+        lut[u][r * ROW_E + lb * NSUB + sub] = f64_to_f16_rne(s);
     }
-    __syncthreads();
-    if (o >= d.O || g >= d.G)
-        return;
-    uint32_t sub = 0;  // nibble p: subset index of element 8v+p
+
+    uint32_t w[NB][K];
 #pragma unroll
-    for (int i = 0; i < K; ++i)
-        sub |= ((w[i] >> v) & 0x11111111u) << i;
-    const uint16_t *L = lut + (r * GB + b) * NSUB;
-    uint32_t out[4];
+    for (int u = 0; u < NB; ++u)
 #pragma unroll
-    for (int h = 0; h < 4; ++h)
-        out[h] = (uint32_t)L[(sub >> (8 * h)) & 0xf] | ((uint32_t)L[(sub >> (8 * h + 4)) & 0xf] << 16);
-    *(uint4 *)(W + (size_t)o * d.I + (size_t)g * GROUP + wq * 32 + 8 * v) = make_uint4(out[0], out[1], out[2], out[3]);
+        for (int i = 0; i < K; ++i)
+            w[u][i] = quad_bcast(mine[u], i);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+
+    typedef unsigned v4u_t __attribute__((ext_vector_type(4)));
+#pragma unroll
+    for (int u = 0; u < NB; ++u) {
+        const int g = (gb0 + u) * GB + b;
+        if (o >= d.O || g >= d.G || gb0 + u >= d.n_gblocks)
+            continue;
+        uint32_t sub = 0;  // nibble p: subset index of element 8v+p
+#pragma unroll
+        for (int i = 0; i < K; ++i)
+            sub |= ((w[u][i] >> v) & 0x11111111u) << i;
+        const uint16_t *L = lut[u] + r * ROW_E + b * NSUB;
+        v4u_t out;
+#pragma unroll
+        for (int h = 0; h < 4; ++h)
+            out[h] = (uint32_t)L[(sub >> (8 * h)) & 0xf] | ((uint32_t)L[(sub >> (8 * h + 4)) & 0xf] << 16);
+        __builtin_nontemporal_store(out, (v4u_t *)(W + (size_t)o * d.I + (size_t)g * GROUP + wq * 32 + 8 * v));
+    }
+}
+
+// gblocks per workgroup: one for small matrices (enough workgroups to fill
+// the chip), more for large ones (more bytes in flight per wavefront).
+// Measured on the 8B shapes: k/v 1, q/o 2, gate/up/down 4 were fastest.
+static int decompress_nb(const Dims &d)
+{
+    const size_t blocks = (size_t)d.n_tiles * d.n_gblocks;
+    return blocks >= 16384 ? 4 : (blocks >= 4096 ? 2 : 1);
+}
+
+template <bool IX, int NB>
+static const void *decompress_kernel_for(int k)
+{
+    return k == 4   ? (const void *)decompress_kernel<4, IX, NB>
+           : k == 3 ? (const void *)decompress_kernel<3, IX, NB>
+           : k == 2 ? (const void *)decompress_kernel<2, IX, NB>
+                    : (const void *)decompress_kernel<1, IX, NB>;
 }
 
 template <bool IX>
-static const void *decompress_kernel_for(int k)
+static const void *decompress_kernel_for(int k, int nb)
 {
-    return k == 4   ? (const void *)decompress_kernel<4, IX>
-           : k == 3 ? (const void *)decompress_kernel<3, IX>
-           : k == 2 ? (const void *)decompress_kernel<2, IX>
-                    : (const void *)decompress_kernel<1, IX>;
+    return nb == 4 ? decompress_kernel_for<IX, 4>(k)
+                   : (nb == 2 ? decompress_kernel_for<IX, 2>(k) : decompress_kernel_for<IX, 1>(k));
 }
 
 int launch_decompress(const Dims &d, const WeightRef &w, uint16_t *W, hipStream_t stream)
@@ -102,8 +170,9 @@ int launch_decompress(const Dims &d, const WeightRef &w, uint16_t *W, hipStream_
     const uint16_t *t = (const uint16_t *)w.table;
     int n_sets = w.n_sets;
     void *args[] = {&dd, &p, &c, &t, &n_sets, &W};
-    const void *fn = ix ? decompress_kernel_for<true>(d.k) : decompress_kernel_for<false>(d.k);
-    const unsigned grid = (unsigned)((size_t)d.n_tiles * d.n_gblocks);
+    const int nb = decompress_nb(d);
+    const void *fn = ix ? decompress_kernel_for<true>(d.k, nb) : decompress_kernel_for<false>(d.k, nb);
+    const unsigned grid = (unsigned)((size_t)d.n_tiles * ((d.n_gblocks + nb - 1) / nb));
     return launch_kernel(fn, dim3(grid), dim3(64 * d.tr), 0, stream, args);
 }
 

@@ -433,8 +433,13 @@ def run_decompress(sb, planes, coeffs):
     return M.cpu().numpy().view(np.uint16)
 
 
+# Workgroups take 1, 2 or 4 gblocks by the matrix's block count; the larger
+# cases cover 2 and 4 with a gblock count that is not a multiple of them.
 @pytest.mark.parametrize("O,I,k", [(1, 128, 4), (3, 128, 1), (1001, 640, 3), (7, 896, 4), (4097, 1152, 2),
-                                   (130, 4224, 4), (16, 512, 1), (4096, 4096, 4), (1024, 14336, 2)])
+                                   (130, 4224, 4), (16, 512, 1), (4096, 4096, 4), (1024, 14336, 2),
+                                   (8192, 2560, 4), (16384, 2560, 4), (16000, 2176, 3), (16384, 2176, 1),
+                                   (32768, 2176, 2),
+                                   (14336, 4096, 4)])
 def test_decompress_bit_exact(sb, O, I, k):
     planes, coeffs = synth.random_sbvr(O, I, k, seed=O * 7 + I + k)
     got = run_decompress(sb, planes, coeffs)
@@ -823,7 +828,7 @@ def test_indexed_error_paths_and_canary(sb):
 
 
 @pytest.mark.parametrize("O,I,k,N", [(1, 128, 4, 1), (1001, 640, 3, 50), (4097, 1152, 2, 999), (33, 2560, 1, 7),
-                                     (4096, 4096, 4, 13108)])
+                                     (4096, 4096, 4, 13108), (14336, 2560, 3, 5000)])
 def test_decompress_indexed_bit_exact(sb, O, I, k, N):
     """Prefill decompression of the cache format: bit-exact against rounding
     the oracle's exact decoding of the gathered coefficients, and identical to
