@@ -18,6 +18,8 @@ One JSON line is printed:
   value         aggregate algorithmic HBM throughput (GB/s) of the timed steps
   decode_step   the L-layer graph alone: microseconds per token, GB/s
   decode_step_w4a8  the same graph with SBVR-8 activations (sbvr_gemv_a8)
+  decode_step_fused the same weights with q|k|v and gate|up packed as one
+                matrix each (rows concatenated), 4 GEMVs per layer
   per_call_us   mean duration of each projection's launch, from HIP events
                 around a graph of 64 back-to-back launches of that shape
                 cycling through >= 1 GB of distinct weight copies (median
@@ -346,6 +348,36 @@ def main():
         decode_step_a8 = {"us_per_token": round(us, 2), "gbps": round(layer_bytes * L / (us * 1e3), 1)}
         del a8_graph
 
+    # the same weights with the projections that share an input packed as one
+    # matrix each (rows concatenated: q|k|v and gate|up), as a serving stack
+    # lays them out: 4 GEMVs per layer instead of 7, same weight bytes
+    decode_step_fused = None
+    if not args.quick:
+        def fuse_rows(ws):
+            parts = [sb.unpack(w) for w in ws]
+            return sb.pack(torch.cat([p for p, _ in parts]), torch.cat([c for _, c in parts]))
+
+        fused_calls = []
+        fused_layers = []
+        for li in range(L):
+            lay = layers[li]
+            qkv = fuse_rows([lay[n][0] for n in ("q", "k", "v")])
+            gu = fuse_rows([lay[n][0] for n in ("gate", "up")])
+            y_qkv = torch.empty(qkv.O, dtype=torch.float16, device=dev)
+            y_gu = torch.empty(gu.O, dtype=torch.float16, device=dev)
+            fused_layers.append((qkv, gu, y_qkv, y_gu))
+            fused_calls += [gemv_call(qkv, lay["q"][1], y_qkv), gemv_call(*lay["o"]),
+                            gemv_call(gu, lay["gate"][1], y_gu), gemv_call(*lay["down"])]
+        torch.cuda.synchronize()
+        fused_graph = capture(fused_calls)
+        timed(fused_graph.replay)
+        reps = [timed(fused_graph.replay) * 1e3 for _ in range(5)]
+        us = float(np.median(reps))
+        decode_step_fused = {"gemvs": len(fused_calls), "us_per_token": round(us, 2),
+                             "gbps": round(layer_bytes * L / (us * 1e3), 1)}
+        del fused_graph, fused_layers
+        torch.cuda.empty_cache()
+
     # ---- per-launch durations: >= 64 back-to-back launches per graph, cycling
     # through distinct weight copies totalling >= ROTATE_BYTES ----
     def launch_us(calls, n_launch=64, replays=11):
@@ -643,6 +675,7 @@ def main():
         "roofline": roofline,
         "decode_step": decode_step,
         "decode_step_w4a8": decode_step_a8,
+        "decode_step_fused": decode_step_fused,
         "small_batch": small_batch or None,
         "w4a8": w4a8 or None,
         "indexed": indexed,
