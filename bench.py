@@ -53,7 +53,8 @@ One JSON line is printed:
                 projection (~2.5 s); cpu_model from /proc/cpuinfo
 
 --traffic-probe runs, eagerly, four launches of every projection shape (fp16
-and W4A8 activations, and the coefficient-cache format) and an elementwise
+and W4A8 activations, the coefficient-cache format, and the prefill
+decompression to binary16) and an elementwise
 negation over 256 MiB of float32 (reads and writes 256 MiB: the counter
 calibration), for
   rocprofv3 --pmc FETCH_SIZE -- python3 bench.py --traffic-probe   (and WRITE_SIZE);
@@ -282,6 +283,11 @@ def main():
                 x, y = layers[0][name][1], layers[0][name][2]
                 for _ in range(L):
                     sb.gemv_indexed(Wi, x, out=y, stream=stream)
+            for name in PROJ_ORDER:  # prefill decompression of the same weights
+                O, I = shapes[name]
+                M = torch.empty((O, I), dtype=torch.float16, device=dev)
+                for li in range(L):
+                    sb.decompress(layers[li][name][0], out=M, stream=stream)
             # calibration: an elementwise kernel that reads and writes CALIB_BYTES
             src = torch.ones(CALIB_BYTES // 4, dtype=torch.float32, device=dev)
             dst = torch.empty_like(src)
