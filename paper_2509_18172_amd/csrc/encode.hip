@@ -24,6 +24,11 @@
 //     best entry = first strict minimum over entries in (r, s, b) order;
 //   - no admissible entry: c = (fp16(mean), 0, ...).
 //
+// The search needs only each element's smallest squared distance to a subset
+// sum, min_p fl((x - sum_p)^2), which equals the square of the nearest
+// difference (the rounded square is monotone in |d|); the pattern itself is
+// found once, for the chosen entry.
+//
 // Work split: one wavefront per group; lane l evaluates entries l, l+64, ...
 // (each entry's error sum runs over the elements in order, so entries -- not
 // elements -- are what is parallel), then the wavefront picks the smallest
@@ -104,6 +109,22 @@ __device__ __forceinline__ int nearest(const double *sums, double x, double &dif
     return best;
 }
 
+// Smallest squared distance from x to a subset sum: the same value as the
+// square of the nearest difference (the rounded square is monotone in |d|),
+// without tracking which sum it was.
+template <int K>
+__device__ __forceinline__ double nearest_sq(const double *sums, double x)
+{
+    double d = x - sums[0];
+    double m = d * d;
+#pragma unroll
+    for (int p = 1; p < (1 << K); ++p) {
+        d = x - sums[p];
+        m = fmin(m, d * d);
+    }
+    return m;
+}
+
 constexpr int ENC_CHUNK = 16;  // elements between pruning checks
 
 __device__ __forceinline__ double wave_min_f64(double v)
@@ -119,9 +140,7 @@ __device__ __forceinline__ double entry_mse(const double *D, const double *sums)
 {
     double err = 0.0;
     for (int j = 0; j < GROUP; ++j) {
-        double d;
-        nearest<K>(sums, D[j], d);
-        err += d * d;
+        err += nearest_sq<K>(sums, D[j]);
     }
     return err / (double)GROUP;
 }
@@ -209,9 +228,34 @@ __global__ void __launch_bounds__(ENC_THREADS) encode_kernel(EncodeArgs a)
     // strictly larger than that and it can neither win nor tie; its remaining
     // elements are skipped.  Lanes share their best MSE after every round of
     // 64 entries.
+    //
+    // Seed for the pruning bound: one round of entries spread over the grid
+    // (lane l: ratio l mod |R|, the middle bias, scales spread over the
+    // range), each scored over all elements.  Their smallest MSE is an upper
+    // bound on the search's minimum (they are entries of the grid), so
+    // pruning against it from the first round on stays exact; the search
+    // below scores every entry it does not prune, these included, so the
+    // result does not depend on the seed.
+    double shared_best = __builtin_inf();
+    if (n_entries > ENC_THREADS) {
+        const int n_r = a.n_ratio1 + a.n_ratio2;
+        const int ir = lane % n_r;
+        const int per_lane_r = (ENC_THREADS + n_r - 1) / n_r;  // lanes sharing a ratio
+        const int js = ((lane / n_r) * a.n_scale + a.n_scale / 2) / per_lane_r % a.n_scale;
+        const int e = (ir * a.n_scale + js) * a.n_bias + a.n_bias / 2;
+        double r, sc, b;
+        entry_rsb(e, r, sc, b);
+        uint16_t c[K];
+        double mse = __builtin_inf();
+        if (sc > 0.0 && entry_coeffs<K>(r, sc, b, a.normalise != 0, c)) {
+            double sums[1 << K];
+            subset_sums<K>(c, sums);
+            mse = entry_mse<K>(D, sums);
+        }
+        shared_best = wave_min_f64(mse);
+    }
     double best_mse = __builtin_inf();
     int best_e = -1;
-    double shared_best = __builtin_inf();
     for (int e0 = 0; e0 < n_entries; e0 += ENC_THREADS) {
         const int e = e0 + lane;
         bool ok = false;
@@ -230,9 +274,7 @@ __global__ void __launch_bounds__(ENC_THREADS) encode_kernel(EncodeArgs a)
             for (int j0 = 0; j0 < GROUP; j0 += ENC_CHUNK) {
 #pragma unroll 4
                 for (int j = j0; j < j0 + ENC_CHUNK; ++j) {
-                    double d;
-                    nearest<K>(sums, D[j], d);
-                    err += d * d;
+                    err += nearest_sq<K>(sums, D[j]);
                 }
                 if (err / (double)GROUP > shared_best) {
                     pruned = true;

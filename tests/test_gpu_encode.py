@@ -54,7 +54,11 @@ def test_encoder_bit_exact_70b_scale_and_ragged_rows(sb):
 @pytest.mark.parametrize("params", [oracle.SearchParams(normalise=False),
                                     oracle.SearchParams(2, 2, 3, 1),
                                     oracle.SearchParams(1, 3, 5, 2),
-                                    oracle.SearchParams(16, 8, 32, 8)])
+                                    oracle.SearchParams(16, 8, 32, 8),
+                                    # entry counts that end in a partial round and a partial
+                                    # queued segment (351 and 935 entries)
+                                    oracle.SearchParams(5, 4, 13, 3),
+                                    oracle.SearchParams(8, 9, 11, 5)])
 def test_encoder_bit_exact_other_grids(sb, params):
     W = synth.weights(8, 512, 0.02, seed=41)
     for k in (2, 4):
