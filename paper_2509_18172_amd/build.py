@@ -11,7 +11,12 @@ ROOT = os.path.dirname(HERE)
 SOURCES = [os.path.join(HERE, "csrc", f) for f in ("api.hip", "pack.hip", "gemv_b1.hip", "gemv_b1s.hip", "gemm_sbs.hip",
                                                   "decompress.hip", "encode.hip")]
 # The encoder's binary64 arithmetic is its definition: no fused multiply-add.
-SOURCE_FLAGS = {"encode.hip": ["-ffp-contract=off"]}
+SOURCE_FLAGS = {
+    "encode.hip": ["-ffp-contract=off"],
+    # leading scalar kernel arguments preloaded into SGPRs (batch-1 kernels)
+    "gemv_b1.hip": ["-mllvm", "-amdgpu-kernarg-preload-count=6"],
+    "gemv_b1s.hip": ["-mllvm", "-amdgpu-kernarg-preload-count=7"],
+}
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

@@ -40,9 +40,23 @@ struct B1Regs {
 
 // A8: activations converted online to SBVR-8.  IX: coefficient-cache format
 // (index blocks + table of coefficient sets) instead of per-group coefficients.
+// The fields every wavefront needs before its first loads come again as
+// leading scalar arguments: the compiler preloads those into SGPRs at launch
+// (built with -amdgpu-kernarg-preload-count), so the first loads do not wait
+// for a kernel-argument fetch; the rest are read from the struct.
 template <int K, int T, bool A8, bool IX>
-__global__ void __launch_bounds__(1024) gemv_b1_kernel(GemvArgs a)
+__global__ void __launch_bounds__(1024) gemv_b1_kernel(const uint4 *planes_, const uint16_t *coeffs_,
+                                                       const uint16_t *x_, int I_, int n_tiles_, int n_gblocks_,
+                                                       GemvArgs a_rest)
 {
+    GemvArgs a = a_rest;
+    a.planes = planes_;
+    a.coeffs = coeffs_;
+    a.x = x_;
+    a.I = I_;
+    a.n_tiles = n_tiles_;
+    a.n_gblocks = n_gblocks_;
+
     extern __shared__ __align__(16) unsigned char smem[];
     const int lane = threadIdx.x & 63;
     const int wv = wave_id();
@@ -282,7 +296,7 @@ int launch_gemv_b1(const Dims &d, const WeightRef &w, const uint16_t *x, uint16_
                      : d.k == 3 ? b1_kernel_for<3>(T, a8, ix)
                      : d.k == 2 ? b1_kernel_for<2>(T, a8, ix)
                                 : b1_kernel_for<1>(T, a8, ix);
-    void *args[] = {&a};
+    void *args[] = {&a.planes, &a.coeffs, &a.x, &a.I, &a.n_tiles, &a.n_gblocks, &a};
     return launch_kernel(fn, dim3(grid), dim3(64 * waves), lds, stream, args);
 }
 

@@ -65,9 +65,24 @@ constexpr int B1S_WAVE_LDS = 2048;  // per wavefront: [q][s][l][32 B]
 // item m is consumed, and the sets of item m+D are gathered then from the
 // index block loaded D items earlier, so neither the index load nor the gather
 // waits on anything issued less than D items before.
+// The fields every wavefront needs before its first loads come again as
+// leading scalar arguments: the compiler preloads those into SGPRs at launch
+// (built with -amdgpu-kernarg-preload-count), so the first loads do not wait
+// for a kernel-argument fetch; the rest are read from the struct.
 template <int K, int D, bool MULTI, bool A8, bool IX>
-__global__ void __launch_bounds__(1024) gemv_b1s_kernel(GemvArgs a)
+__global__ void __launch_bounds__(1024) gemv_b1s_kernel(const uint4 *planes_, const uint16_t *coeffs_,
+                                                        const uint16_t *x_, int I_, int n_tiles_, int n_gblocks_, int tpw_,
+                                                        GemvArgs a_rest)
 {
+    GemvArgs a = a_rest;
+    a.planes = planes_;
+    a.coeffs = coeffs_;
+    a.x = x_;
+    a.I = I_;
+    a.n_tiles = n_tiles_;
+    a.n_gblocks = n_gblocks_;
+    a.tpw = tpw_;
+
     extern __shared__ __align__(16) unsigned char smem[];
     const int lane = threadIdx.x & 63;
     const int wv = wave_id();
@@ -331,7 +346,7 @@ int launch_gemv_b1s(const Dims &d, const WeightRef &w, const uint16_t *x, uint16
                      : d.k == 3 ? b1s_kernel_for<3>(multi, short_run, a8, ix)
                      : d.k == 2 ? b1s_kernel_for<2>(multi, short_run, a8, ix)
                                 : b1s_kernel_for<1>(multi, short_run, a8, ix);
-    void *args[] = {&a};
+    void *args[] = {&a.planes, &a.coeffs, &a.x, &a.I, &a.n_tiles, &a.n_gblocks, &a.tpw, &a};
     return launch_kernel(fn, dim3(grid), dim3(64 * waves), lds, stream, args);
 }
 
