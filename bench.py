@@ -16,7 +16,10 @@ tests run these same shapes and launch configurations against the CPU oracle.
 
 One JSON line is printed:
   value         aggregate algorithmic HBM throughput (GB/s) of the timed steps
-  decode_step   the L-layer graph alone: microseconds per token, GB/s
+  decode_step   the L-layer graph alone: microseconds per token (median and
+                mean of 50 replays), GB/s
+  per_call_events  per projection: median and mean of 200 single launches,
+                each between its own pair of events (after 20 warm-up calls)
   decode_step_w4a8  the same graph with SBVR-8 activations (sbvr_gemv_a8)
   decode_step_fused the same weights with q|k|v and gate|up packed as one
                 matrix each (rows concatenated), 4 GEMVs per layer
@@ -80,6 +83,8 @@ PEAK_GBPS = 8000.0
 PROJ_ORDER = ("q", "k", "v", "o", "gate", "up", "down")
 TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "hbm_traffic_llama3-8b_k4.md")
 CALIB_BYTES = 256 << 20
+DECODE_REPLAYS = 50   # replays of the L-layer decode graph
+EVENT_WARMUP, EVENT_CALLS = 20, 200  # per-call event timing
 PROBE_LAUNCHES = 4
 
 
@@ -337,10 +342,11 @@ def main():
     ms_per_step = total_ms / args.steps
     value = layer_bytes * args.steps / (total_ms * 1e-3) / 1e9
     # the decode step alone (configs: one token through all L layers)
-    step_reps = [timed(decode_graph.replay) * 1e3 for _ in range(5)]
+    step_reps = [timed(decode_graph.replay) * 1e3 for _ in range(DECODE_REPLAYS)]
     decode_us = float(np.median(step_reps))
     decode_step = {"layers": L, "gemvs": 7 * L, "bytes": layer_bytes * L, "us_per_token": round(decode_us, 2),
                    "gbps": round(layer_bytes * L / (decode_us * 1e3), 1),
+                   "mean_us_per_token": round(float(np.mean(step_reps)), 2),
                    "replays": len(step_reps)}
     del decode_graph, layer_graphs
     # the same decode step with SBVR-8 activations (the paper's W4A8 decode)
@@ -420,6 +426,29 @@ def main():
         ys = [torch.empty(O, dtype=torch.float16, device=dev) for _ in range(len(xs))]
         per_call_us[name] = launch_us([gemv_call(w, xs[i % len(xs)], ys[i % len(ys)]) for i, w in enumerate(ws)])
     per_call_gbps = {n: nbytes[n] / (per_call_us[n] * 1e3) for n in PROJ_ORDER}
+
+    # the same calls timed one by one: an event pair around each of
+    # EVENT_CALLS eager launches (after EVENT_WARMUP), cycling through the
+    # same copies; median and mean per call (these include each launch's
+    # share of the host-side enqueue gaps that a graph removes)
+    per_call_events = {}
+    for name in PROJ_ORDER:
+        O, I = shapes[name]
+        ws = weights[name]
+        x = layers[0][name][1]
+        y = torch.empty(O, dtype=torch.float16, device=dev)
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(EVENT_CALLS)]
+        with torch.cuda.stream(stream):
+            for i in range(EVENT_WARMUP):
+                sb.gemv(ws[i % len(ws)], x, out=y, stream=stream)
+            for i, (a, b) in enumerate(evs):
+                a.record(stream)
+                sb.gemv(ws[(EVENT_WARMUP + i) % len(ws)], x, out=y, stream=stream)
+                b.record(stream)
+        torch.cuda.synchronize()
+        t = np.array([a.elapsed_time(b) * 1e3 for a, b in evs])
+        per_call_events[name] = {"median_us": round(float(np.median(t)), 3), "mean_us": round(float(t.mean()), 3)}
 
     # dominant kernel instance: largest launch time per step
     by_kernel = {}
@@ -680,6 +709,7 @@ def main():
         "per_call_gbps": {n: round(v, 1) for n, v in per_call_gbps.items()},
         "roofline": roofline,
         "decode_step": decode_step,
+        "per_call_events": per_call_events,
         "decode_step_w4a8": decode_step_a8,
         "decode_step_fused": decode_step_fused,
         "small_batch": small_batch or None,
