@@ -550,12 +550,14 @@ def main():
             dec = (lambda W, M, stream: sb.decompress(W, out=M, stream=stream))
             us = launch_us([(dec, (w, outs[i % n_out])) for i, w in enumerate(ws)], n_launch=32)
             bb = sb.algorithmic_bytes(O, I, k, 0) + 2 * O * I
-            Xt = torch.from_numpy(synth.activations(I, seed=31, batch=T)).to(dev).t().contiguous()
+            # Y[T][O] = X[T][I] W^T, the layout of a linear layer (faster in
+            # the library than W X^T for these shapes)
+            Xs = torch.from_numpy(synth.activations(I, seed=31, batch=T)).to(dev)
             M = outs[0]
             with torch.cuda.stream(stream):
                 for _ in range(3):
-                    torch.matmul(M, Xt)
-            gemm = [timed(lambda: torch.matmul(M, Xt)) * 1e3 for _ in range(5)]
+                    torch.nn.functional.linear(Xs, M)
+            gemm = [timed(lambda: torch.nn.functional.linear(Xs, M)) * 1e3 for _ in range(5)]
             prefill[name] = {"decompress_us": round(us, 3), "decompress_gbps": round(bb / (us * 1e3), 1),
                              "decompress_bytes": bb, "gemm_us_512_tokens": round(float(np.median(gemm)), 2)}
             del outs

@@ -499,17 +499,17 @@ def test_decompress_rounding_edges(sb):
 
 
 def test_prefill_gemm_with_library_matmul(sb):
-    """Prefill: Y^T = W x^T over T tokens with the decompressed W and a
-    library GEMM (fp32 accumulation), against the oracle per token."""
+    """Prefill: Y = X W^T over T tokens (a linear layer's layout, as the
+    bench times it) with the decompressed W and a library GEMM (fp32
+    accumulation), against the oracle per token."""
     O, I, T = 1024, 4096, 64
     W = synth.weights(O, I, 0.02, seed=synth.seed_for(2, 0, 1), outlier_frac=0.001)
     planes, coeffs = oracle.encode_matrix(W, 4)
     X = synth.activations(I, seed=99, batch=T)
     M = sb.decompress(packed(sb, planes, coeffs))
-    Xt = dev(X).t().contiguous()                      # [I][T]
-    Yt = torch.matmul(M, Xt)                          # [O][T], fp16 in, fp32 accumulate
+    Y = torch.nn.functional.linear(dev(X), M)         # [T][O], fp16 in, fp32 accumulate
     torch.cuda.synchronize()
-    Y = Yt.t().cpu().numpy().astype(np.float64)
+    Y = Y.cpu().numpy().astype(np.float64)
     Y_ref = oracle.sbvr_gemv(planes, coeffs, X)
     errs = [rel_err(Y[t], Y_ref[t]) for t in range(T)]
     log(f"prefill {O}x{I} T={T} worst err={max(errs):.3e}")
