@@ -20,11 +20,12 @@
 // wavefronts in order, so the result is deterministic and no global
 // workspace is used.
 //
-// Memory behaviour: with D = 2 a wavefront keeps about 2.3 KB of weights in
-// flight and 32 wavefronts per CU keep ~70 KB per CU outstanding: enough to
-// cover DRAM latency, while each workgroup's requests stay in a narrow,
-// advancing address window.  Deeper rings or more workgroups measured slower
-// (more requests in flight than the memory system serves efficiently).
+// Memory behaviour: with D = 2 a wavefront keeps up to two items (about
+// 2.3 KB of weights) in flight, and 16 wavefronts per CU (512 workgroups of
+// 8) keep ~36 KB per CU outstanding, while each workgroup's requests stay in
+// a narrow, advancing address window.  Deeper rings and more workgroups
+// measured slower: every extra workgroup repeats the activation load and
+// operand build, and shortens the stream of items that amortises them.
 #include "device_ops.h"
 #include "launch.h"
 
