@@ -185,7 +185,7 @@ def b1_kernel_instance(O: int, I: int, k: int, a8: bool = False, ix: bool = Fals
     ring depth 2, or 3 with several gblocks per wavefront and >= 8 tiles per
     workgroup (256 workgroups); otherwise the one-shot
     kernel with T tiles per workgroup, the most of 8/4/2/1 that still leaves
-    >= 256 workgroups.  The last two template arguments select the W4A8 build
+    >= 256 workgroups and >= 2048 wavefronts (one per gblock).  The last two template arguments select the W4A8 build
     (activations converted online to SBVR-8) and the coefficient-cache format."""
     a8 = "true" if a8 else "false"
     ix = "true" if ix else "false"
@@ -196,7 +196,7 @@ def b1_kernel_instance(O: int, I: int, k: int, a8: bool = False, ix: bool = Fals
         tpw = (n_tiles + 255) // 256
         depth = (3 if tpw >= 8 else 2) if multi else 2
         return f"gemv_b1s_kernel<{k}, {depth}, {'true' if multi else 'false'}, {a8}, {ix}>"
-    T = next((t for t in (8, 4, 2) if n_tiles // t >= 256), 1)
+    T = next((t for t in (8, 4, 2) if n_tiles // t >= 256 and (n_tiles // t) * n_gblocks >= 2048), 1)
     return f"gemv_b1_kernel<{k}, {T}, {a8}, {ix}>"
 
 

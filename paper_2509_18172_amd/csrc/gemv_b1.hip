@@ -239,7 +239,11 @@ __global__ void __launch_bounds__(1024) gemv_b1_kernel(const uint4 *planes_, con
 }
 
 // Launch shape.  T tiles (T * TR rows) per workgroup: the most (<= 8) that still
-// leaves >= 256 workgroups for 256 CUs; one wavefront per gblock.
+// leaves >= 256 workgroups for 256 CUs and >= 2048 wavefronts in all; one
+// wavefront per gblock.  (Measured T = 1 / 2 / 4 / 8: 4096 x 4096 4.30 / 4.01 /
+// 3.99 / 4.53 us, 1024 x 4096 2.76 / 2.80 / 3.24 / 4.23, 2048 x 4096 3.27 /
+// 3.09 / 3.40 / 4.28, 8192 x 1024 3.59 / 3.26 / 3.45 / 3.45: the wavefront
+// count picks the fastest in each.)
 constexpr int B1_MAX_WAVES = 16;
 
 static int choose_b1_tiles(const Dims &d)
@@ -248,7 +252,7 @@ static int choose_b1_tiles(const Dims &d)
     return SBVR_TUNE_T;
 #else
     for (int t = 8; t > 1; t >>= 1)
-        if (d.n_tiles / t >= 256)
+        if (d.n_tiles / t >= 256 && (long)(d.n_tiles / t) * d.n_gblocks >= 2048)
             return t;
     return 1;
 #endif

@@ -19,6 +19,8 @@ import bench  # noqa: E402
     (8192, 28672, "gemv_b1s_kernel<4, 3, true, false, false>"),   # 56 gblocks per row, 8 tiles per workgroup
     (8192, 8192, "gemv_b1s_kernel<4, 2, false, false, false>"),
     (1024, 8192, "gemv_b1_kernel<4, 1, false, false>"),
+    (8192, 1024, "gemv_b1_kernel<4, 2, false, false>"),      # 2 gblocks: T = 2 keeps >= 2048 wavefronts
+    (2048, 4096, "gemv_b1_kernel<4, 2, false, false>"),
 ])
 def test_kernel_instance_names(O, I, name):
     assert bench.b1_kernel_instance(O, I, 4) == name

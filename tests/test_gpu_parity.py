@@ -284,7 +284,10 @@ def test_linearity_and_determinism(sb):
 # --------------------------------------------------------------------------
 
 @pytest.mark.parametrize("O,I,k", [(1, 128, 4), (3, 128, 1), (1001, 640, 3), (7, 896, 4),
-                                   (4097, 1152, 2), (130, 4224, 4), (2, 30720, 4)])
+                                   (4097, 1152, 2), (130, 4224, 4), (2, 30720, 4),
+                                   # few gblocks per row: the one-shot kernel's tiles per
+                                   # workgroup follow the wavefront count (T = 2 in all three)
+                                   (8192, 1024, 4), (8191, 896, 3), (2048, 4096, 4)])
 def test_ragged_shapes(sb, O, I, k):
     planes, coeffs = synth.random_sbvr(O, I, k, seed=O + I + k)
     x = synth.activations(I, seed=O * 3 + 1)
