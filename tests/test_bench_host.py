@@ -55,3 +55,13 @@ def test_traffic_summary_scales_by_copy(tmp_path):
     assert k["dispatches"] == 3
     assert k["bytes_per_launch"] == round(16100.0 * 1024 * 2 + 7.0 * 1024 * 2)
     assert rec["source_sha256"] == bench.kernel_source_digest()
+
+
+def test_more_than_one_gpu_is_refused():
+    """bench.py measures one GPU: --gpus N > 1 exits with a message (before
+    touching torch or the GPU)."""
+    import subprocess
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=60)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
