@@ -52,8 +52,8 @@ def rel_err(y, y_ref, W_hat, x):
 
     The second term only matters when every output is much smaller than its
     products (cancellation, e.g. a single row): the kernels' activation
-    limbs are exact down to 2^-9 of a 512-element block's maximum and off by
-    at most 2^-16 of it below that, an error on the scale of the products,
+    limbs are exact down to 1/32 of a 512-element block's maximum and off by
+    at most 2^-15 of it below that, an error on the scale of the products,
     not of a cancelled sum.  For matrices of many rows max|y_ref| is the
     larger term and this is the plain gate."""
     y = np.asarray(y, dtype=np.float64)
