@@ -111,3 +111,25 @@ def test_encoder_error_paths(sb):
     assert sb.sbvr_encode(4, 256, 4, w, 8, 8, 16, 4, 1, p + 4, c, None, 0) == sb.SBVR_E_ALIGNMENT
     assert sb.sbvr_encode(4, 256, 4, None, 8, 8, 16, 4, 1, p, c, None, 0) == sb.SBVR_E_INVALID_ARG
     torch.cuda.synchronize()
+
+
+# Property test over random shapes and search grids (Hypothesis, derandomised
+# so every run draws the same examples; no example database).
+hypothesis = pytest.importorskip("hypothesis")
+from hypothesis import HealthCheck, given, settings  # noqa: E402
+from hypothesis import strategies as st  # noqa: E402
+
+
+@settings(max_examples=30, deadline=None, derandomize=True, database=None,
+          suppress_health_check=[HealthCheck.function_scoped_fixture, HealthCheck.too_slow])
+@given(O=st.integers(1, 48), G=st.integers(1, 8), k=st.integers(1, 4),
+       grid=st.tuples(st.integers(1, 9), st.integers(1, 9), st.integers(1, 20), st.integers(1, 6)),
+       normalise=st.booleans(), sigma_exp=st.integers(-12, 2), outliers=st.booleans())
+def test_encoder_bit_exact_random_shapes_and_grids(sb, O, G, k, grid, normalise, sigma_exp, outliers):
+    """Random O x 128 G matrices at weight scales 2^-12 .. 2^2, with or without
+    +-8 sigma outliers, on random (|R1|, |R2|, N_scale, N_bias) grids and both
+    readings of Eq. 4: planes, coefficients and MSE identical to the oracle's."""
+    params = oracle.SearchParams(grid[0], grid[1], grid[2], grid[3], normalise=normalise)
+    W = synth.weights(O, 128 * G, 2.0 ** sigma_exp, seed=O * 1009 + G * 31 + k + sigma_exp + 64,
+                      outlier_frac=0.01 if outliers else 0.0)
+    assert_same(sb, W, k, params, what=f"{params} sigma=2^{sigma_exp}")
