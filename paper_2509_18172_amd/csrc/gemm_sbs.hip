@@ -183,7 +183,19 @@ __global__ void __launch_bounds__(512) gemm_sbs_kernel(GemvArgs a)
 
     v8i Bop[NS][GB];
     float oscale[NS];  // 2^-sigma of the lane's vector, per set
+    // With four or more vectors the activation maxima are reduced first, two
+    // per register, so that the reductions' latencies overlap, and every
+    // vector is split (vectors >= B hold zeros and give zero limbs in their
+    // own slots, which no operand reads); with two, each vector present is
+    // reduced and split in turn (measured faster there in the kernels that
+    // rebuild in the middle of the stream).
     auto build = [&](const uint4 *X) {
+        uint32_t amax2[(NB + 1) / 2] = {};
+        if constexpr (NB >= 4) {
+#pragma unroll
+            for (int p = 0; p < (NB + 1) / 2; ++p)
+                amax2[p] = wave_absmax2_bits(X[2 * p], X[2 * p + 1]);
+        }
 #pragma unroll
         for (int st = 0; st < NS; ++st) {
             float inv_scale[VPS];
@@ -191,8 +203,10 @@ __global__ void __launch_bounds__(512) gemm_sbs_kernel(GemvArgs a)
             for (int v = 0; v < VPS; ++v) {
                 const int b = st * SBS_VPS + v;
                 inv_scale[v] = 1.0f;
-                if (b < NB && b < B) {
-                    const int sigma = scale_exponent(wave_absmax_h(X[b]));
+                if (NB >= 4 || b < B) {
+                    const float amax = NB >= 4 ? half_bits_to_float((amax2[b / 2] >> (16 * (b & 1))) & 0xffffu)
+                                               : wave_absmax_h(X[b]);
+                    const int sigma = scale_exponent(amax);
                     inv_scale[v] = ldexpf(1.0f, -sigma);
                     const Limbs L = split_limbs(X[b], sigma, inv_alpha);
                     unsigned char *dst = stage + wr_off + v * 3 * GROUP;
