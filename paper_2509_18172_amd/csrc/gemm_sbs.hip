@@ -52,6 +52,42 @@ __host__ __device__ constexpr int sbs_sets(int nb) { return (nb + SBS_VPS - 1) /
 __host__ __device__ constexpr int sbs_vps(int nb) { return nb < SBS_VPS ? nb : SBS_VPS; }
 __host__ __device__ constexpr int sbs_stage_bytes(int nb) { return GB * sbs_vps(nb) * 3 * GROUP + 32; }
 
+// max |x| over the wavefront for two activation vectors at once (eight
+// binary16 values per lane each): the magnitudes' bit patterns are compared as
+// 16-bit integers, vector a in the low and vector b in the high half of one
+// register, reduced within each row of 16 lanes by DPP and across the rows by
+// two lane swaps (the semantics transpose_rows4 relies on), so the result
+// needs one read into a scalar register instead of one per row and vector.
+// Returns both maxima as binary16 bit patterns (a: bits 0-15, b: bits
+// 16-31), wavefront-uniform.
+__device__ __forceinline__ uint32_t wave_absmax2_bits(uint4 a, uint4 b)
+{
+    typedef unsigned short u2_t __attribute__((ext_vector_type(2)));
+    auto lane_max = [](uint4 v) {
+        const u2_t p = __builtin_bit_cast(u2_t, v.x & 0x7fff7fffu), q = __builtin_bit_cast(u2_t, v.y & 0x7fff7fffu);
+        const u2_t r = __builtin_bit_cast(u2_t, v.z & 0x7fff7fffu), t = __builtin_bit_cast(u2_t, v.w & 0x7fff7fffu);
+        return __builtin_elementwise_max(__builtin_elementwise_max(p, q), __builtin_elementwise_max(r, t));
+    };
+    const u2_t ma = lane_max(a), mb = lane_max(b);
+    const u2_t lo = {ma[0], mb[0]}, hi = {ma[1], mb[1]};
+    uint32_t w = __builtin_bit_cast(uint32_t, __builtin_elementwise_max(lo, hi));
+    auto pmax = [](uint32_t x, uint32_t y) {
+        return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(u2_t, x),
+                                                                      __builtin_bit_cast(u2_t, y)));
+    };
+    w = pmax(w, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)w, DPP_QUAD_XOR1, 0xf, 0xf, false));
+    w = pmax(w, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)w, DPP_QUAD_XOR2, 0xf, 0xf, false));
+    w = pmax(w, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)w, DPP_ROW_HALF_MIRROR, 0xf, 0xf, false));
+    w = pmax(w, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)w, DPP_ROW_MIRROR, 0xf, 0xf, false));
+    // every lane holds its row's maximum: lanes 32-63 trade with 0-31, then
+    // odd rows with even rows
+    const auto s32 = __builtin_amdgcn_permlane32_swap(w, w, false, false);
+    w = pmax(s32[0], s32[1]);
+    const auto s16 = __builtin_amdgcn_permlane16_swap(w, w, false, false);
+    w = pmax(s16[0], s16[1]);
+    return (uint32_t)__builtin_amdgcn_readfirstlane((int)w);
+}
+
 // The coefficients of a lane's four D rows for the four groups of a gblock:
 // 4 * CPL contiguous binary16 entries (q * GB * CPL ..), group g's at g * CPL.
 template <int K>
