@@ -183,7 +183,8 @@ def b1_kernel_instance(O: int, I: int, k: int, a8: bool = False, ix: bool = Fals
     or one) when a row has more than 16 gblocks of 512 elements or the matrix
     has at least 24576 (tile, gblock) blocks (tiles of 16/k rows, 4 at k = 3),
     ring depth 2, or 3 with several gblocks per wavefront and >= 8 tiles per
-    workgroup (256 workgroups); otherwise the one-shot
+    workgroup (256 workgroups), or 4 at k = 4 with one gblock per wavefront,
+    at most 8 of them and per-group coefficients (256 workgroups); otherwise the one-shot
     kernel with T tiles per workgroup, the most of 8/4/2/1 that still leaves
     >= 256 workgroups and >= 2048 wavefronts (one per gblock).  The last two template arguments select the W4A8 build
     (activations converted online to SBVR-8) and the coefficient-cache format."""
@@ -194,7 +195,8 @@ def b1_kernel_instance(O: int, I: int, k: int, a8: bool = False, ix: bool = Fals
     if n_gblocks > 16 or n_tiles * n_gblocks >= 24576:
         multi = n_gblocks > 16
         tpw = (n_tiles + 255) // 256
-        depth = (3 if tpw >= 8 else 2) if multi else 2
+        wide = k == 4 and not multi and n_gblocks <= 8 and ix == "false"
+        depth = (3 if tpw >= 8 else 2) if multi else (4 if wide else 2)
         return f"gemv_b1s_kernel<{k}, {depth}, {'true' if multi else 'false'}, {a8}, {ix}>"
     T = next((t for t in (8, 4, 2) if n_tiles // t >= 256 and (n_tiles // t) * n_gblocks >= 2048), 1)
     return f"gemv_b1_kernel<{k}, {T}, {a8}, {ix}>"

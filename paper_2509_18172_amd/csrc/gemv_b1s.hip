@@ -59,6 +59,17 @@ constexpr int B1S_WAVE_LDS = 2048;  // per wavefront: [q][s][l][32 B]
 #ifndef SBVR_B1S_GROUPS_MULTI
 #define SBVR_B1S_GROUPS_MULTI 256
 #endif
+// k = 4 with one gblock per wavefront and at most 8 wavefronts (Llama-3-8B
+// gate/up), per-group coefficients: one workgroup per CU with a depth-4 ring
+// -- about the same bytes in flight as two workgroups at depth 2, and half
+// the activation builds per CU (gate 7.55 -> 7.35 us, W4A8 7.87 -> 7.52; at
+// k = 3 the same shape was slower, 7.73 -> 8.17).
+#ifndef SBVR_B1S_GROUPS_WIDE
+#define SBVR_B1S_GROUPS_WIDE 256
+#endif
+#ifndef SBVR_B1S_DEPTH_WIDE
+#define SBVR_B1S_DEPTH_WIDE 4
+#endif
 
 // A8: activations converted online to SBVR-8.  IX: coefficient-cache format;
 // each item's coefficient sets are then gathered through its index block, and
@@ -309,8 +320,12 @@ __global__ void __launch_bounds__(1024) gemv_b1s_kernel(const uint4 *planes_, co
 }
 
 template <int K, bool A8, bool IX>
-static const void *b1s_kernel_for(bool multi, bool short_run)
+static const void *b1s_kernel_for(bool multi, bool short_run, bool wide)
 {
+    if constexpr (K == 4 && !IX) {
+        if (wide)
+            return (const void *)gemv_b1s_kernel<K, SBVR_B1S_DEPTH_WIDE, false, A8, IX>;
+    }
     if (!multi)
         return (const void *)gemv_b1s_kernel<K, SBVR_B1S_DEPTH, false, A8, IX>;
     return short_run ? (const void *)gemv_b1s_kernel<K, 2, true, A8, IX>
@@ -318,11 +333,13 @@ static const void *b1s_kernel_for(bool multi, bool short_run)
 }
 
 template <int K>
-static const void *b1s_kernel_for(bool multi, bool short_run, bool a8, bool ix)
+static const void *b1s_kernel_for(bool multi, bool short_run, bool wide, bool a8, bool ix)
 {
     if (ix)
-        return a8 ? b1s_kernel_for<K, true, true>(multi, short_run) : b1s_kernel_for<K, false, true>(multi, short_run);
-    return a8 ? b1s_kernel_for<K, true, false>(multi, short_run) : b1s_kernel_for<K, false, false>(multi, short_run);
+        return a8 ? b1s_kernel_for<K, true, true>(multi, short_run, wide)
+                  : b1s_kernel_for<K, false, true>(multi, short_run, wide);
+    return a8 ? b1s_kernel_for<K, true, false>(multi, short_run, wide)
+              : b1s_kernel_for<K, false, false>(multi, short_run, wide);
 }
 
 int launch_gemv_b1s(const Dims &d, const WeightRef &w, const uint16_t *x, uint16_t *y, bool a8,
@@ -333,20 +350,23 @@ int launch_gemv_b1s(const Dims &d, const WeightRef &w, const uint16_t *x, uint16
     // one gblock per wavefront: about 16 wavefronts per CU -- 512 workgroups of
     // up to 8 wavefronts, 256 of more (70B q/o, gate/up: 8.4 -> 8.1 us,
     // 22.3 -> 22.1 us)
-    const int groups = gpw > 1 ? SBVR_B1S_GROUPS_MULTI : (waves > 8 ? SBVR_B1S_GROUPS / 2 : SBVR_B1S_GROUPS);
+    const bool ix = w.index != nullptr;
+    const bool wide = d.k == 4 && gpw == 1 && waves <= 8 && !ix;
+    const int groups = gpw > 1 ? SBVR_B1S_GROUPS_MULTI
+                       : wide  ? SBVR_B1S_GROUPS_WIDE
+                               : (waves > 8 ? SBVR_B1S_GROUPS / 2 : SBVR_B1S_GROUPS);
     const int tpw = (d.n_tiles + groups - 1) / groups;
     const int grid = (d.n_tiles + tpw - 1) / tpw;
     GemvArgs a = {(const uint4 *)w.planes, (const uint16_t *)w.coeffs, x, y, d.O, d.I, d.k,
                   d.n_tiles, d.n_gblocks, gpw, 1, tpw, (const uint16_t *)w.index, (const uint16_t *)w.table,
                   w.n_sets};
-    const bool ix = w.index != nullptr;
     const size_t lds = (size_t)waves * B1S_WAVE_LDS + (size_t)tpw * waves * d.tr * 4;
     const bool multi = gpw > 1;
     const bool short_run = tpw < SBVR_B1S_SHORT_TPW;
-    const void *fn = d.k == 4   ? b1s_kernel_for<4>(multi, short_run, a8, ix)
-                     : d.k == 3 ? b1s_kernel_for<3>(multi, short_run, a8, ix)
-                     : d.k == 2 ? b1s_kernel_for<2>(multi, short_run, a8, ix)
-                                : b1s_kernel_for<1>(multi, short_run, a8, ix);
+    const void *fn = d.k == 4   ? b1s_kernel_for<4>(multi, short_run, wide, a8, ix)
+                     : d.k == 3 ? b1s_kernel_for<3>(multi, short_run, wide, a8, ix)
+                     : d.k == 2 ? b1s_kernel_for<2>(multi, short_run, wide, a8, ix)
+                                : b1s_kernel_for<1>(multi, short_run, wide, a8, ix);
     void *args[] = {&a.planes, &a.coeffs, &a.x, &a.I, &a.n_tiles, &a.n_gblocks, &a.tpw, &a};
     return launch_kernel(fn, dim3(grid), dim3(64 * waves), lds, stream, args);
 }

@@ -14,7 +14,7 @@ import bench  # noqa: E402
 @pytest.mark.parametrize("O,I,name", [
     (4096, 4096, "gemv_b1_kernel<4, 4, false, false>"),      # 8192 blocks: one-shot, 1024 tiles -> T = 4
     (1024, 4096, "gemv_b1_kernel<4, 1, false, false>"),
-    (14336, 4096, "gemv_b1s_kernel<4, 2, false, false, false>"),  # 28672 blocks: streaming
+    (14336, 4096, "gemv_b1s_kernel<4, 4, false, false, false>"),  # 28672 blocks: streaming, 8 gblocks: depth 4
     (4096, 14336, "gemv_b1s_kernel<4, 2, true, false, false>"),   # 28 gblocks per row, 4 tiles per workgroup
     (8192, 28672, "gemv_b1s_kernel<4, 3, true, false, false>"),   # 56 gblocks per row, 8 tiles per workgroup
     (8192, 8192, "gemv_b1s_kernel<4, 2, false, false, false>"),
@@ -25,7 +25,9 @@ import bench  # noqa: E402
 def test_kernel_instance_names(O, I, name):
     assert bench.b1_kernel_instance(O, I, 4) == name
     assert bench.b1_kernel_instance(O, I, 4, a8=True) == name.replace("false, false>", "true, false>")
-    assert bench.b1_kernel_instance(O, I, 4, ix=True) == name.replace("false, false>", "false, true>")
+    # the coefficient-cache format keeps the depth-2 ring of 512 workgroups
+    ix_name = name.replace("false, false>", "false, true>").replace("gemv_b1s_kernel<4, 4,", "gemv_b1s_kernel<4, 2,")
+    assert bench.b1_kernel_instance(O, I, 4, ix=True) == ix_name
 
 
 def _write_counter_csv(path, counter, rows):
