@@ -287,7 +287,11 @@ def test_linearity_and_determinism(sb):
                                    (4097, 1152, 2), (130, 4224, 4), (2, 30720, 4),
                                    # few gblocks per row: the one-shot kernel's tiles per
                                    # workgroup follow the wavefront count (T = 2 in all three)
-                                   (8192, 1024, 4), (8191, 896, 3), (2048, 4096, 4)])
+                                   (8192, 1024, 4), (8191, 896, 3), (2048, 4096, 4),
+                                   # streaming at k = 4 with 8 gblocks per row (256 workgroups,
+                                   # depth-4 ring): 3073 tiles, the last gblock holds 3 groups
+                                   # and the last workgroup 5 tiles
+                                   (12291, 3968, 4)])
 def test_ragged_shapes(sb, O, I, k):
     planes, coeffs = synth.random_sbvr(O, I, k, seed=O + I + k)
     x = synth.activations(I, seed=O * 3 + 1)
@@ -565,7 +569,7 @@ def test_a8_full_size_low_bit(sb, O, I, k):
 
 
 @pytest.mark.parametrize("O,I,k", [(1, 128, 4), (3, 128, 1), (1001, 640, 3), (7, 896, 4),
-                                   (4097, 1152, 2), (33, 2560, 4)])
+                                   (4097, 1152, 2), (33, 2560, 4), (12291, 3968, 4)])
 def test_a8_ragged_shapes(sb, O, I, k):
     """Both batch-1 kernels (one-shot for short rows, streaming for long),
     partial tiles and partial gblocks."""
