@@ -355,12 +355,17 @@ int launch_gemv_b1s(const Dims &d, const WeightRef &w, const uint16_t *x, uint16
     const int groups = gpw > 1 ? SBVR_B1S_GROUPS_MULTI
                        : wide  ? SBVR_B1S_GROUPS_WIDE
                                : (waves > 8 ? SBVR_B1S_GROUPS / 2 : SBVR_B1S_GROUPS);
-    const int tpw = (d.n_tiles + groups - 1) / groups;
+    // tiles per workgroup, capped so that the dynamic LDS (operand staging
+    // plus the [tile][wavefront][row] sums) stays within SBVR_MAX_DYN_LDS:
+    // very tall matrices get more workgroups instead
+    const size_t per_tile = (size_t)waves * d.tr * 4;
+    const int max_tpw = (int)((SBVR_MAX_DYN_LDS - (size_t)waves * B1S_WAVE_LDS) / per_tile);
+    const int tpw = min((d.n_tiles + groups - 1) / groups, max_tpw);
     const int grid = (d.n_tiles + tpw - 1) / tpw;
     GemvArgs a = {(const uint4 *)w.planes, (const uint16_t *)w.coeffs, x, y, d.O, d.I, d.k,
                   d.n_tiles, d.n_gblocks, gpw, 1, tpw, (const uint16_t *)w.index, (const uint16_t *)w.table,
                   w.n_sets};
-    const size_t lds = (size_t)waves * B1S_WAVE_LDS + (size_t)tpw * waves * d.tr * 4;
+    const size_t lds = (size_t)waves * B1S_WAVE_LDS + (size_t)tpw * per_tile;
     const bool multi = gpw > 1;
     const bool short_run = tpw < SBVR_B1S_SHORT_TPW;
     const void *fn = d.k == 4   ? b1s_kernel_for<4>(multi, short_run, wide, a8, ix)

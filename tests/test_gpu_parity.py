@@ -896,3 +896,22 @@ def test_largest_accepted_shape_sampled_rows(sb):
     Y_ref = oracle.sbvr_gemv(planes, coeffs, X, rows=rows)
     assert max(rel_err(Y[b][rows], Y_ref[b]) for b in range(8)) <= TOL
     log(f"largest shape {O}x{I}: sampled rows within {TOL}")
+
+@pytest.mark.parametrize("O,I,k", [(262143, 8192, 4), (524287, 4096, 4), (262143, 8192, 1)])
+def test_tallest_accepted_shapes_sampled_rows(sb, O, I, k):
+    """O * I just below 2^31 with short rows: the streaming kernel's tiles per
+    workgroup are capped by the dynamic LDS its per-tile row sums take
+    (16 wavefronts at I = 8192, the depth-4 launch of 256 workgroups at
+    I = 4096, 16-row tiles at k = 1), so these launches use more workgroups;
+    batch 1 and W4A8 against the oracle on sampled rows, first and last
+    included."""
+    assert O * I < 2 ** 31 - 1
+    planes, coeffs = synth.random_sbvr(O, I, k, seed=O + k)
+    W = packed(sb, planes, coeffs)
+    rows = np.unique(np.r_[0, 1, O - 2, O - 1, np.random.default_rng(1).integers(0, O, 44)])
+    x = synth.activations(I, seed=O + 7)
+    y = run_gemv(sb, W, x)
+    assert rel_err(y[rows], oracle.sbvr_gemv(planes, coeffs, x, rows=rows)) <= TOL
+    y8 = run_gemv_a8(sb, W, x)
+    assert rel_err(y8[rows], oracle.sbvr_gemv_w4a8(planes, coeffs, x, rows=rows)) <= TOL
+    log(f"tall shape {O}x{I} k={k}: sampled rows within {TOL}")
