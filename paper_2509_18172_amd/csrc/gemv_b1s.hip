@@ -23,9 +23,12 @@
 // Memory behaviour: with D = 2 a wavefront keeps up to two items (about
 // 2.3 KB of weights) in flight, and 16 wavefronts per CU (512 workgroups of
 // 8) keep ~36 KB per CU outstanding, while each workgroup's requests stay in
-// a narrow, advancing address window.  Deeper rings and more workgroups
-// measured slower: every extra workgroup repeats the activation load and
-// operand build, and shortens the stream of items that amortises them.
+// a narrow, advancing address window.  More workgroups measured slower:
+// every extra workgroup repeats the activation load and operand build, and
+// shortens the stream of items that amortises them.  For the same reason
+// k = 4 with at most 8 wavefronts runs one workgroup per CU with D = 4
+// (about the same bytes in flight, half the builds per CU); elsewhere deeper
+// rings measured slower.
 #include "device_ops.h"
 #include "launch.h"
 
@@ -349,7 +352,7 @@ int launch_gemv_b1s(const Dims &d, const WeightRef &w, const uint16_t *x, uint16
     const int waves = (d.n_gblocks + gpw - 1) / gpw;
     // one gblock per wavefront: about 16 wavefronts per CU -- 512 workgroups of
     // up to 8 wavefronts, 256 of more (70B q/o, gate/up: 8.4 -> 8.1 us,
-    // 22.3 -> 22.1 us)
+    // 22.3 -> 22.1 us) -- except the k = 4 depth-4 launch (256 of up to 8)
     const bool ix = w.index != nullptr;
     const bool wide = d.k == 4 && gpw == 1 && waves <= 8 && !ix;
     const int groups = gpw > 1 ? SBVR_B1S_GROUPS_MULTI
