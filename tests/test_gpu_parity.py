@@ -915,3 +915,20 @@ def test_tallest_accepted_shapes_sampled_rows(sb, O, I, k):
     y8 = run_gemv_a8(sb, W, x)
     assert rel_err(y8[rows], oracle.sbvr_gemv_w4a8(planes, coeffs, x, rows=rows)) <= TOL
     log(f"tall shape {O}x{I} k={k}: sampled rows within {TOL}")
+
+@pytest.mark.parametrize("O,I", [(4096, 4096), (14336, 4096), (4096, 14336)])
+def test_repeated_calls_are_bit_identical(sb, O, I):
+    """Each kernel reduces in a fixed order, so repeated calls on the same
+    inputs give the same bits: the one-shot kernel (4096 x 4096), the
+    streaming kernel with one gblock per wavefront (14336 x 4096) and with
+    several (4096 x 14336), for fp16 and SBVR-8 activations and a 5-vector
+    small batch."""
+    planes, coeffs = synth.random_sbvr(O, I, 4, seed=O + 3 * I)
+    W = packed(sb, planes, coeffs)
+    x = synth.activations(I, seed=O + 5)
+    X = synth.activations(I, seed=O + 6, batch=5)
+    first = (run_gemv(sb, W, x), run_gemv_a8(sb, W, x), run_gemm(sb, W, X))
+    for _ in range(3):
+        again = (run_gemv(sb, W, x), run_gemv_a8(sb, W, x), run_gemm(sb, W, X))
+        for a, b in zip(first, again):
+            assert np.array_equal(a.view(np.uint64), b.view(np.uint64))  # exact binary16 values as float64
