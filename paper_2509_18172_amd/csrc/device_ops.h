@@ -9,10 +9,14 @@
 //     nibble p holds element 8v+p of the word as 0 or alpha_v with
 //     alpha = (0.5, 1, 2, 2) (bit 3, the fp4 sign, is shifted down to bit 2).
 //     No per-element work is done on the bits.
-//   * B operand (activations): each binary16 activation, scaled by a power of
-//     two 2^sigma / alpha_v, is split exactly into three fp8 (E4M3) limbs
-//     hi + mid + lo (each limb is the round-to-nearest E4M3 value of what the
-//     previous limbs left), so alpha_v * (hi + mid + lo) = 2^sigma * x.
+//   * B operand (binary16 activations): each activation, scaled by a power of
+//     two 2^sigma / alpha_v, is split exactly into four E5M2 limbs, each the
+//     top byte of a binary16 piece with at most three significant bits
+//     (E5M2 is binary16 with the mantissa cut to two bits: same exponent
+//     range, so no conversion instruction is needed), and
+//     alpha_v * (l0 + l1 + l2 + l3) = 2^sigma * x.  With SBVR-8 activations
+//     (the W4A8 path) the operand holds the 8-bit code split into two E4M3
+//     limbs instead.
 //   * v_mfma_scale_f32_16x16x128_f8f6f4 with unit scales multiplies and sums
 //     128 k-slots per row in fp32.
 #pragma once
@@ -52,18 +56,6 @@ __device__ __forceinline__ float half_bits_to_float(uint32_t bits16)
     return __half2float(__ushort_as_half((unsigned short)bits16));
 }
 
-__device__ __forceinline__ float absmax8(uint4 v)
-{
-    float m = 0.f;
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        m = fmaxf(m, fabsf(half_bits_to_float(w[i] & 0xffffu)));
-        m = fmaxf(m, fabsf(half_bits_to_float(w[i] >> 16)));
-    }
-    return m;
-}
-
 // DPP lane exchange within rows of 16 lanes.
 template <int CTRL>
 __device__ __forceinline__ float dpp_f32(float v)
@@ -86,39 +78,95 @@ __device__ __forceinline__ float row16_sum(float v)
     return v;
 }
 
-// Maximum over the wavefront, returned uniformly.
-__device__ __forceinline__ float wave_max(float v)
-{
-    v = fmaxf(v, dpp_f32<DPP_QUAD_XOR1>(v));
-    v = fmaxf(v, dpp_f32<DPP_QUAD_XOR2>(v));
-    v = fmaxf(v, dpp_f32<DPP_ROW_HALF_MIRROR>(v));
-    v = fmaxf(v, dpp_f32<DPP_ROW_MIRROR>(v));
-    const float m0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
-    const float m1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
-    const float m2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
-    const float m3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
-    return fmaxf(fmaxf(m0, m1), fmaxf(m2, m3));
-}
-
 // Wavefront index within the workgroup as a scalar (uniform) value.
 __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
 
-// Power-of-two exponent sigma with max|x| * 2^sigma in [64, 128): scaled
-// activations times 1/alpha (<= 2) stay below the E4M3 maximum of 448.
+// Power-of-two exponent sigma with max|x| * 2^sigma in [2^13, 2^14): the
+// scaled activations times 1/alpha (<= 2) stay below 2^15, inside both the
+// binary16 and the E5M2 range (largest finite E5M2 value 57344).  A zero
+// block gets sigma = 0.
 __device__ __forceinline__ int scale_exponent(float amax)
 {
     if (!(amax > 0.f))
         return 0;
     int e;
     frexpf(amax, &e);
-    return 7 - e;
+    return 14 - e;
 }
 
-// Three E4M3 limbs of eight scaled activations, two words each (bytes in
-// element order).
+// Four 8-bit limbs of eight activations, two words each (bytes in element
+// order); limb j feeds the result column of limb j.
 struct Limbs {
-    uint32_t hi[2], mid[2], lo[2];
+    uint32_t l[4][2];
 };
+
+typedef _Float16 h2_t __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ uint32_t h2_sub(uint32_t a, uint32_t b)
+{
+    return __builtin_bit_cast(uint32_t, __builtin_bit_cast(h2_t, a) - __builtin_bit_cast(h2_t, b));
+}
+
+__device__ __forceinline__ uint32_t h2_mul(uint32_t a, uint32_t f)
+{
+    return __builtin_bit_cast(uint32_t, __builtin_bit_cast(h2_t, a) * __builtin_bit_cast(h2_t, f));
+}
+
+// binary16 2^e in both halves, -14 <= e <= 15
+__device__ __forceinline__ uint32_t h2_pow2(int e)
+{
+    const uint32_t b = (uint32_t)(e + 15) << 10;
+    return b | (b << 16);
+}
+
+// Exact split of eight binary16 activations into four E5M2 limbs.
+//
+// x' = x * 2^(sigma + inv_alpha) is formed in binary16 (powers of two, in
+// steps of at most 2^15: exact, the block maximum lands in [2^12, 2^15)).
+// The truncation split p0 = x' with its mantissa cut to two bits,
+// p1 = the same cut of x' - p0, p2 = the cut of x' - p0 - p1 and
+// p3 = x' - p0 - p1 - p2 is exact in binary16 (each difference is a multiple
+// of x''s unit in the last place, below the piece it is taken from), and
+// every piece whose bits lie at or above 2^-16 has its low byte zero: its top
+// byte is then the E5M2 encoding of the same value (E5M2 = sign, the five
+// binary16 exponent bits, the top two mantissa bits).  So
+// x' = p0 + p1 + p2 + p3 exactly whenever x' is at least 2^-6 (its 11
+// significant bits stay at or above 2^-16): for every element of at least
+// 2^-18 of its block's largest magnitude.  Smaller elements lose only bits
+// below 2^-16 in x' units, less than 2^-27 of the block maximum.
+// sigma: the block's scale exponent (scale_exponent, wavefront-uniform);
+// inv_alpha: log2(1/alpha) of the lane's elements.
+__device__ __forceinline__ Limbs split_limbs(uint4 xv, int sigma, int inv_alpha)
+{
+    constexpr uint32_t CUT = 0xFF00FF00u;  // sign, exponent and 2 mantissa bits of each half
+    const int s0 = min(sigma, 14);
+    const uint32_t f = h2_pow2(s0 + inv_alpha);
+    uint32_t w[4] = {h2_mul(xv.x, f), h2_mul(xv.y, f), h2_mul(xv.z, f), h2_mul(xv.w, f)};
+    for (int rem = sigma - s0; rem > 0; rem -= 15) {  // blocks below 2^-1: further exact steps
+        const uint32_t g = h2_pow2(min(rem, 15));
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            w[i] = h2_mul(w[i], g);
+    }
+    uint32_t p[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        uint32_t r = w[i];
+#pragma unroll
+        for (int j = 0; j < 3; ++j) {
+            p[j][i] = r & CUT;
+            r = h2_sub(r, p[j][i]);
+        }
+        p[3][i] = r;
+    }
+    Limbs L;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int h = 0; h < 2; ++h)  // top bytes of the four halves of two words
+            L.l[j][h] = __builtin_amdgcn_perm(p[j][2 * h + 1], p[j][2 * h], 0x07050301u);
+    return L;
+}
 
 __device__ __forceinline__ void pack8_fp8(const float *v, uint32_t *out)
 {
@@ -130,95 +178,6 @@ __device__ __forceinline__ void pack8_fp8(const float *v, uint32_t *out)
     }
 }
 
-__device__ __forceinline__ void sub_fp8(float *v, const uint32_t *q)
-{
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-        const int w = (int)q[h];
-        v[4 * h + 0] -= __builtin_amdgcn_cvt_f32_fp8(w, 0);
-        v[4 * h + 1] -= __builtin_amdgcn_cvt_f32_fp8(w, 1);
-        v[4 * h + 2] -= __builtin_amdgcn_cvt_f32_fp8(w, 2);
-        v[4 * h + 3] -= __builtin_amdgcn_cvt_f32_fp8(w, 3);
-    }
-}
-
-// Eight binary16 activations (one uint4) times `scale` -> three limbs.
-__device__ __forceinline__ Limbs make_limbs(uint4 xv, float scale)
-{
-    float y[8];
-    const uint32_t w[4] = {xv.x, xv.y, xv.z, xv.w};
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        y[2 * i] = half_bits_to_float(w[i] & 0xffffu) * scale;
-        y[2 * i + 1] = half_bits_to_float(w[i] >> 16) * scale;
-    }
-    Limbs L;
-    pack8_fp8(y, L.hi);
-    sub_fp8(y, L.hi);
-    pack8_fp8(y, L.mid);
-    sub_fp8(y, L.mid);
-    pack8_fp8(y, L.lo);
-    return L;
-}
-
-// Three E4M3 limbs by splitting in binary16 (cheaper than make_limbs).
-// The activations are first multiplied by 2^s1, s1 = min(sigma, 15) (a
-// binary16 power of two: exact), which makes every element that matters
-// (above 2^-9 of the block maximum) a normal binary16 number.  The truncation
-// split hi = x' with its mantissa cut to 3 bits, mid = the same cut of x' - hi,
-// lo = x' - hi - mid is then exact (every difference is representable) and
-// each piece has at most 4 significant bits, so the scaled conversion
-// fp8(piece * 2^(sigma - s1 + log2(1/alpha))) is exact while the result lies
-// in the E4M3 range.
-typedef _Float16 h2_t __attribute__((ext_vector_type(2)));
-typedef short s2_t __attribute__((ext_vector_type(2)));
-
-__device__ __forceinline__ uint32_t h2_sub(uint32_t a, uint32_t b)
-{
-    return __builtin_bit_cast(uint32_t, __builtin_bit_cast(h2_t, a) - __builtin_bit_cast(h2_t, b));
-}
-
-__device__ __forceinline__ uint32_t h2_mul(uint32_t a, h2_t f)
-{
-    return __builtin_bit_cast(uint32_t, __builtin_bit_cast(h2_t, a) * f);
-}
-
-__device__ __forceinline__ uint32_t cvt2_fp8(uint32_t lo_pair, uint32_t hi_pair, float scale_div)
-{
-    s2_t r = __builtin_amdgcn_cvt_scalef32_pk_fp8_f16(s2_t{0, 0}, __builtin_bit_cast(h2_t, lo_pair),
-                                                       scale_div, false);
-    r = __builtin_amdgcn_cvt_scalef32_pk_fp8_f16(r, __builtin_bit_cast(h2_t, hi_pair), scale_div, true);
-    return __builtin_bit_cast(uint32_t, r);
-}
-
-// sigma: the block's scale exponent (scale_exponent); inv_alpha: log2(1/alpha)
-// of the lane's elements.
-__device__ __forceinline__ Limbs split_limbs(uint4 xv, int sigma, int inv_alpha)
-{
-    constexpr uint32_t CUT = 0xFF80FF80u;  // sign, exponent and 3 mantissa bits of each half
-    const int s1 = min(sigma, 15);
-    const _Float16 f = (_Float16)ldexpf(1.0f, s1);
-    const h2_t f2 = {f, f};
-    const float scale_div = ldexpf(1.0f, -(sigma - s1 + inv_alpha));
-    const uint32_t w[4] = {h2_mul(xv.x, f2), h2_mul(xv.y, f2), h2_mul(xv.z, f2), h2_mul(xv.w, f2)};
-    uint32_t hi[4], mid[4], lo[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        hi[i] = w[i] & CUT;
-        const uint32_t r = h2_sub(w[i], hi[i]);
-        mid[i] = r & CUT;
-        lo[i] = h2_sub(r, mid[i]);
-    }
-    Limbs L;
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-        L.hi[h] = cvt2_fp8(hi[2 * h], hi[2 * h + 1], scale_div);
-        L.mid[h] = cvt2_fp8(mid[2 * h], mid[2 * h + 1], scale_div);
-        L.lo[h] = cvt2_fp8(lo[2 * h], lo[2 * h + 1], scale_div);
-    }
-    return L;
-}
-
 // Online conversion to SBVR-8 activations (Sec. 4.3, Eq. 12) for the W4A8
 // decode path.  The lanes 16r .. 16r+15 of a wavefront hold the 128 elements
 // of group r of the gblock (eight each).  Per group: s = absmax / 127 and the
@@ -226,7 +185,7 @@ __device__ __forceinline__ Limbs split_limbs(uint4 xv, int sigma, int inv_alpha)
 // division; a zero group has s = 0, q = 0).  Eq. 12's coefficients are the
 // two's-complement weights of q, so the matrix-core operand carries q itself,
 // split exactly into two E4M3 limbs: 16 * floor(q / 16) and q mod 16 (each
-// divided by alpha_v, still exact), in the hi and mid limb slots (lo = 0).
+// divided by alpha_v, still exact), in limb slots 0 and 1 (2 and 3 are zero).
 // Returns the limbs; `out_scale` receives the scale of the group of the
 // lane's result column (slot (lane % 16) / 4), which multiplies its sums.
 //
@@ -281,9 +240,9 @@ __device__ __forceinline__ Limbs a8_limbs(uint4 xv, int lane, int inv_alpha, flo
         lo[e] = fmaf(fl, -16.0f, q) * f;  // q mod 16, exact
     }
     Limbs L;
-    pack8_fp8(hi, L.hi);
-    pack8_fp8(lo, L.mid);
-    L.lo[0] = L.lo[1] = 0u;
+    pack8_fp8(hi, L.l[0]);
+    pack8_fp8(lo, L.l[1]);
+    L.l[2][0] = L.l[2][1] = L.l[3][0] = L.l[3][1] = 0u;
     const int slot = (lane & 15) >> 2;
     const float s0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sg), 0));
     const float s1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sg), 16));
@@ -325,10 +284,12 @@ __device__ __forceinline__ uint4 transpose_rows4(uint4 w)
     return make_uint4(t01[0], t01[1], t23[0], t23[1]);
 }
 
+// A: fp4 E2M1 (cbsz = 4); B: E5M2 (blgp = 1) for binary16 activations, E4M3
+// (blgp = 0) for the SBVR-8 codes; unit E8M0 scales (127).
+template <bool A8>
 __device__ __forceinline__ v4f mfma_fp4_fp8(const v8i &a, const v8i &b, const v4f &c)
 {
-    // A: fp4 E2M1 (cbsz = 4), B: fp8 E4M3 (blgp = 0), unit E8M0 scales (127).
-    return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 4, 0, 0, 127, 0, 127);
+    return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 4, A8 ? 0 : 1, 0, 127, 0, 127);
 }
 
 // An 8-register fp8 B operand from two 16-byte LDS chunks (k-slot halves).

@@ -10,9 +10,9 @@
 // Matrix-core formulation.  One 16x16x128 fp4 x fp8 instruction per (tile,
 // group, column set): the 128 k-slots are one whole group (its four plane
 // words, one per 32-slot k-block), rows are (tile row, plane) and the 16
-// columns are (vector, limb) with four columns per vector -- three E4M3 limbs
-// and a zero column -- so a column set serves four vectors (B <= 4: one set,
-// B <= 8: two).  The device layout gives lane (row m, k-block b) the four
+// columns are (vector, limb) with four columns per vector -- the four E5M2
+// limbs of its activations -- so a column set serves four vectors (B <= 4:
+// one set, B <= 8: two).  The device layout gives lane (row m, k-block b) the four
 // words of group b; a 4 x 4 cross-lane transpose turns that into word b of
 // the four groups, i.e. the A operands of the four instructions of an item.
 //
@@ -45,12 +45,14 @@ namespace sbvr {
 #define SBVR_SBS_GROUPS 256
 #endif
 
-// vectors per column set and LDS staging of one set's limbs per wavefront:
-// [group][vector][limb][128 bytes], then 32 zero bytes
+// vectors per column set, and the LDS staging per wavefront: the limbs of
+// two vectors at a time, [group][vector of the pair][limb][128 bytes], then
+// 32 zero bytes (a set of four vectors is staged in two phases, which keeps
+// eight wavefronts' staging within 33 KB)
 constexpr int SBS_VPS = 4;
 __host__ __device__ constexpr int sbs_sets(int nb) { return (nb + SBS_VPS - 1) / SBS_VPS; }
 __host__ __device__ constexpr int sbs_vps(int nb) { return nb < SBS_VPS ? nb : SBS_VPS; }
-__host__ __device__ constexpr int sbs_stage_bytes(int nb) { return GB * sbs_vps(nb) * 3 * GROUP + 32; }
+__host__ __device__ constexpr int sbs_stage_bytes(int) { return GB * 2 * 4 * GROUP + 32; }
 
 // max |x| over the wavefront for two activation vectors at once (eight
 // binary16 values per lane each): the magnitudes' bit patterns are compared as
@@ -209,13 +211,16 @@ __global__ void __launch_bounds__(512) gemm_sbs_kernel(GemvArgs a)
         *(uint4 *)(stage + ZERO + 16 * lane) = make_uint4(0u, 0u, 0u, 0u);
     // B operand reads: lane (column n = lane%16 = (vector n/4, limb n%4),
     // k-block lane/16) takes k = 16 kb + [0,16) and 64 + 16 kb + [0,16) of
-    // its vector's limb; limb 3 and absent vectors read the zero chunk.
+    // its vector's limb; absent vectors read the zero chunk.
     const int n = lane & 15, kb = lane >> 4;
     const int vb = n >> 2, limb = n & 3;
     // limb writes: lane owns elements 8*lane.. of the gblock = group lane/16,
     // elements 8*(lane%16).. of it
-    const int wr_off = (lane >> 4) * (VPS * 3 * GROUP) + 8 * (lane & 15);
+    const int wr_off = (lane >> 4) * (2 * 4 * GROUP) + 8 * (lane & 15);
     const int inv_alpha = inv_alpha_exp(lane & 3);
+    // staging phases per column set (vector pairs) and the lane's phase
+    constexpr int NPH = (VPS + 1) / 2;
+    const int my_phase = min(vb >> 1, NPH - 1);
 
     v8i Bop[NS][GB];
     float oscale[NS];  // 2^-sigma of the lane's vector, per set
@@ -224,7 +229,8 @@ __global__ void __launch_bounds__(512) gemm_sbs_kernel(GemvArgs a)
     // vector is split (vectors >= B hold zeros and give zero limbs in their
     // own slots, which no operand reads); with two, each vector present is
     // reduced and split in turn (measured faster there in the kernels that
-    // rebuild in the middle of the stream).
+    // rebuild in the middle of the stream).  The limbs of a vector pair are
+    // staged, then the lanes of that pair's columns read their operands.
     auto build = [&](const uint4 *X) {
         uint32_t amax2[(NB + 1) / 2] = {};
         if constexpr (NB >= 4) {
@@ -236,33 +242,43 @@ __global__ void __launch_bounds__(512) gemm_sbs_kernel(GemvArgs a)
         for (int st = 0; st < NS; ++st) {
             float inv_scale[VPS];
 #pragma unroll
-            for (int v = 0; v < VPS; ++v) {
-                const int b = st * SBS_VPS + v;
-                inv_scale[v] = 1.0f;
-                if (NB >= 4 || b < B) {
-                    const float amax = NB >= 4 ? half_bits_to_float((amax2[b / 2] >> (16 * (b & 1))) & 0xffffu)
-                                               : wave_absmax_h(X[b]);
-                    const int sigma = scale_exponent(amax);
-                    inv_scale[v] = ldexpf(1.0f, -sigma);
-                    const Limbs L = split_limbs(X[b], sigma, inv_alpha);
-                    unsigned char *dst = stage + wr_off + v * 3 * GROUP;
-                    *(uint2 *)(dst + 0 * GROUP) = make_uint2(L.hi[0], L.hi[1]);
-                    *(uint2 *)(dst + 1 * GROUP) = make_uint2(L.mid[0], L.mid[1]);
-                    *(uint2 *)(dst + 2 * GROUP) = make_uint2(L.lo[0], L.lo[1]);
+            for (int ph = 0; ph < NPH; ++ph) {
+#pragma unroll
+                for (int vv = 0; vv < 2; ++vv) {
+                    const int v = 2 * ph + vv;
+                    if (v >= VPS)
+                        break;
+                    const int b = st * SBS_VPS + v;
+                    inv_scale[v] = 1.0f;
+                    if (NB >= 4 || b < B) {
+                        const float amax = NB >= 4 ? half_bits_to_float((amax2[b / 2] >> (16 * (b & 1))) & 0xffffu)
+                                                   : wave_absmax_h(X[b]);
+                        const int sigma = scale_exponent(amax);
+                        inv_scale[v] = ldexpf(1.0f, -sigma);
+                        const Limbs L = split_limbs(X[b], sigma, inv_alpha);
+                        unsigned char *dst = stage + wr_off + vv * 4 * GROUP;
+#pragma unroll
+                        for (int j = 0; j < 4; ++j)
+                            *(uint2 *)(dst + j * GROUP) = make_uint2(L.l[j][0], L.l[j][1]);
+                    }
+                }
+                // same wavefront: the reads below follow these writes, and the
+                // next phase's writes follow the reads
+                if (my_phase == ph) {
+                    const bool act = vb < VPS && st * SBS_VPS + vb < B;
+#pragma unroll
+                    for (int g = 0; g < GB; ++g) {
+                        const int lo = act ? ((g * 2 + (vb & 1)) * 4 + limb) * GROUP + 16 * kb : ZERO;
+                        const int hi = act ? lo + 64 : ZERO;
+                        Bop[st][g] = lds_operand(stage + lo, stage + hi);
+                    }
                 }
             }
-            const bool act = limb < 3 && vb < VPS && st * SBS_VPS + vb < B;
             float os = inv_scale[0];
 #pragma unroll
             for (int v = 1; v < VPS; ++v)
                 os = vb == v ? inv_scale[v] : os;
             oscale[st] = os;
-#pragma unroll
-            for (int g = 0; g < GB; ++g) {
-                const int lo = act ? ((g * VPS + vb) * 3 + limb) * GROUP + 16 * kb : ZERO;
-                const int hi = act ? lo + 64 : ZERO;
-                Bop[st][g] = lds_operand(stage + lo, stage + hi);
-            }
         }
     };
     build(Xc);
@@ -297,7 +313,7 @@ __global__ void __launch_bounds__(512) gemm_sbs_kernel(GemvArgs a)
                 const v8i A = fp4_operand(words[g]);
 #pragma unroll
                 for (int st = 0; st < NS; ++st)
-                    d[g][st] = mfma_fp4_fp8(A, Bop[st][g], v4f{0.f, 0.f, 0.f, 0.f});
+                    d[g][st] = mfma_fp4_fp8<false>(A, Bop[st][g], v4f{0.f, 0.f, 0.f, 0.f});
             }
             const CoefGroups<K> cr = C[j];
             issue(j);

@@ -11,7 +11,8 @@
 // Block-diagonal activation operand.  One 16x16x128 instruction takes, in its
 // four 32-slot k-blocks, word q of four different groups (the four groups of a
 // gblock), and the 16 output columns are (group slot s, limb l): column 4s+l
-// holds limb l of group s's activations in k-block s and zeros elsewhere.
+// holds limb l (of four) of group s's activations in k-block s and zeros
+// elsewhere.
 // Four chained instructions (q = 0..3) therefore leave in D[row][4s+l] the
 // complete per-plane sum of group s for limb l, and the coefficients are
 // applied once per four instructions: D rows are (tile row, plane), so a lane
@@ -28,7 +29,8 @@
 
 namespace sbvr {
 
-constexpr int B1_WAVE_LDS = 2048;  // per wavefront: [q][s][l][32 B]
+// per wavefront: [q][s][l][32 B] limb chunks, then 32 zero bytes
+constexpr int B1_WAVE_LDS = 2048 + 32;
 
 template <int K, int T>
 struct B1Regs {
@@ -123,11 +125,15 @@ __global__ void __launch_bounds__(1024) gemv_b1_kernel(const uint4 *planes_, con
     // k = 64 + 16 kb + [0,16); slot s covers k = 32 s + [0,32).
     const int n = lane & 15, kb = lane >> 4;
     const int s = n >> 2, l = n & 3;
-    const bool act = (l < 3) && ((kb >> 1) == (s & 1));
+    // limbs 2 and 3 of the SBVR-8 codes are zero: those columns read zeros
+    const bool act = (!A8 || l < 2) && ((kb >> 1) == (s & 1));
     const int data_off = (s * 4 + l) * 32 + 16 * (kb & 1);
-    const int zero_off = (s * 4 + 3) * 32;
+    const int zero_off = 2048;
+    // the k-block half a lane does not cover reads the zero chunk for every q
     const int lo_off = (act && s < 2) ? data_off : zero_off;
     const int hi_off = (act && s >= 2) ? data_off : zero_off;
+    const int lo_step = (act && s < 2) ? 512 : 0;
+    const int hi_step = (act && s >= 2) ? 512 : 0;
     const int inv_alpha = inv_alpha_exp(lane & 3);
 
     float acc[T][NP];
@@ -152,12 +158,12 @@ __global__ void __launch_bounds__(1024) gemv_b1_kernel(const uint4 *planes_, con
             out_scale = ldexpf(1.0f, -sigma);
         }
         // same wavefront: the LDS writes complete before the reads below
-        *(uint2 *)(lds + wr_off + 0 * 32) = make_uint2(L.hi[0], L.hi[1]);
-        *(uint2 *)(lds + wr_off + 1 * 32) = make_uint2(L.mid[0], L.mid[1]);
-        *(uint2 *)(lds + wr_off + 2 * 32) = make_uint2(L.lo[0], L.lo[1]);
+#pragma unroll
+        for (int j = 0; j < (A8 ? 2 : 4); ++j)
+            *(uint2 *)(lds + wr_off + j * 32) = make_uint2(L.l[j][0], L.l[j][1]);
 #pragma unroll
         for (int q = 0; q < 4; ++q)
-            Bq[q] = lds_operand(lds + lo_off + q * 512, lds + hi_off + q * 512);
+            Bq[q] = lds_operand(lds + lo_off + q * lo_step, lds + hi_off + q * hi_step);
         return out_scale;
     };
     // The T tiles of the gblock in R.
@@ -165,10 +171,10 @@ __global__ void __launch_bounds__(1024) gemv_b1_kernel(const uint4 *planes_, con
 #pragma unroll
         for (int t = 0; t < T; ++t) {
             v4f d = {0.f, 0.f, 0.f, 0.f};
-            d = mfma_fp4_fp8(fp4_operand(R.p[t].x), Bq[0], d);
-            d = mfma_fp4_fp8(fp4_operand(R.p[t].y), Bq[1], d);
-            d = mfma_fp4_fp8(fp4_operand(R.p[t].z), Bq[2], d);
-            d = mfma_fp4_fp8(fp4_operand(R.p[t].w), Bq[3], d);
+            d = mfma_fp4_fp8<A8>(fp4_operand(R.p[t].x), Bq[0], d);
+            d = mfma_fp4_fp8<A8>(fp4_operand(R.p[t].y), Bq[1], d);
+            d = mfma_fp4_fp8<A8>(fp4_operand(R.p[t].z), Bq[2], d);
+            d = mfma_fp4_fp8<A8>(fp4_operand(R.p[t].w), Bq[3], d);
             float part[NP];
             apply_coefs<K>(R.c[t], d, part);
 #pragma unroll
@@ -177,8 +183,9 @@ __global__ void __launch_bounds__(1024) gemv_b1_kernel(const uint4 *planes_, con
         }
     };
 
-    // zero the limb-3 chunks: they feed the unused 4th column of each slot
-    *(uint2 *)(lds + ((lane >> 2) * 4 + 3) * 32 + 8 * (lane & 3)) = make_uint2(0u, 0u);
+    // the zero chunk read by the columns of the other k-blocks
+    if (lane < 2)
+        *(uint4 *)(lds + zero_off + 16 * lane) = make_uint4(0u, 0u, 0u, 0u);
 
     {
         B1Regs<K, T> R;

@@ -34,7 +34,8 @@
 
 namespace sbvr {
 
-constexpr int B1S_WAVE_LDS = 2048;  // per wavefront: [q][s][l][32 B]
+// per wavefront: [q][s][l][32 B] limb chunks, then 32 zero bytes
+constexpr int B1S_WAVE_LDS = 2048 + 32;
 // Ring depth: one gblock per wavefront keeps 64 VGPRs (8 wavefronts per
 // SIMD) at depth 2; with several gblocks the workgroups are fewer and a
 // deeper ring keeps enough bytes in flight.
@@ -232,14 +233,18 @@ __global__ void __launch_bounds__(1024) gemv_b1s_kernel(const uint4 *planes_, co
     const int wr_off = ((((lane & 15) >> 2) * 4 + (lane >> 4)) * 4) * 32 + 8 * (lane & 3);
     const int n = lane & 15, kb = lane >> 4;
     const int s = n >> 2, l = n & 3;
-    const bool act = (l < 3) && ((kb >> 1) == (s & 1));
+    // limbs 2 and 3 of the SBVR-8 codes are zero: those columns read zeros
+    const bool act = (!A8 || l < 2) && ((kb >> 1) == (s & 1));
     const int data_off = (s * 4 + l) * 32 + 16 * (kb & 1);
-    const int zero_off = (s * 4 + 3) * 32;
+    const int zero_off = 2048;
+    // the k-block half a lane does not cover reads the zero chunk for every q
     const int lo_off = (act && s < 2) ? data_off : zero_off;
     const int hi_off = (act && s >= 2) ? data_off : zero_off;
+    const int lo_step = (act && s < 2) ? 512 : 0;
+    const int hi_step = (act && s >= 2) ? 512 : 0;
     const int inv_alpha = inv_alpha_exp(lane & 3);
-    // zero the limb-3 chunks: they feed the unused 4th column of each slot
-    *(uint2 *)(lds + ((lane >> 2) * 4 + 3) * 32 + 8 * (lane & 3)) = make_uint2(0u, 0u);
+    if (lane < 2)
+        *(uint4 *)(lds + zero_off + 16 * lane) = make_uint4(0u, 0u, 0u, 0u);
 
     v8i Bq[4];
     float inv_scale;
@@ -255,12 +260,12 @@ __global__ void __launch_bounds__(1024) gemv_b1s_kernel(const uint4 *planes_, co
         }
         // same wavefront: these writes land before the reads below, and after
         // the reads of the previous gblock's operand
-        *(uint2 *)(lds + wr_off + 0 * 32) = make_uint2(L.hi[0], L.hi[1]);
-        *(uint2 *)(lds + wr_off + 1 * 32) = make_uint2(L.mid[0], L.mid[1]);
-        *(uint2 *)(lds + wr_off + 2 * 32) = make_uint2(L.lo[0], L.lo[1]);
+#pragma unroll
+        for (int j = 0; j < (A8 ? 2 : 4); ++j)
+            *(uint2 *)(lds + wr_off + j * 32) = make_uint2(L.l[j][0], L.l[j][1]);
 #pragma unroll
         for (int q = 0; q < 4; ++q)
-            Bq[q] = lds_operand(lds + lo_off + q * 512, lds + hi_off + q * 512);
+            Bq[q] = lds_operand(lds + lo_off + q * lo_step, lds + hi_off + q * hi_step);
     };
     build(x_cur, wv);
     __builtin_amdgcn_sched_barrier(0);
@@ -280,10 +285,10 @@ __global__ void __launch_bounds__(1024) gemv_b1s_kernel(const uint4 *planes_, co
                 }
                 const uint4 pw = a_ok ? P[j] : make_uint4(0u, 0u, 0u, 0u);
                 v4f d = {0.f, 0.f, 0.f, 0.f};
-                d = mfma_fp4_fp8(fp4_operand(pw.x), Bq[0], d);
-                d = mfma_fp4_fp8(fp4_operand(pw.y), Bq[1], d);
-                d = mfma_fp4_fp8(fp4_operand(pw.z), Bq[2], d);
-                d = mfma_fp4_fp8(fp4_operand(pw.w), Bq[3], d);
+                d = mfma_fp4_fp8<A8>(fp4_operand(pw.x), Bq[0], d);
+                d = mfma_fp4_fp8<A8>(fp4_operand(pw.y), Bq[1], d);
+                d = mfma_fp4_fp8<A8>(fp4_operand(pw.z), Bq[2], d);
+                d = mfma_fp4_fp8<A8>(fp4_operand(pw.w), Bq[3], d);
                 float part[NP];
                 apply_coefs<K>(C[j], d, part);
 #pragma unroll

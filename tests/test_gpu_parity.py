@@ -344,6 +344,58 @@ def test_activation_dynamic_range(sb):
                     assert rel_err(Y[b], Y_ref[b]) <= TOL, (cscale, B, b, rel_err(Y[b], Y_ref[b]))
 
 
+def test_cancellation_regression_single_row(sb):
+    """O = 1, I = 128, k = 1, B = 8 (uniform planes, N(0, 0.01^2) binary16
+    coefficients, N(0, 1) activations; the seed a random-shape sweep drew):
+    vector 0's output cancels to -1.0e-4 against products whose root sum of
+    squares is 0.063.  Plain gate per vector, through the small-batch kernel
+    and through the batch-1 kernel."""
+    O, I, k, B = 1, 128, 1, 8
+    seed = O * 131 + I + 7 * k + B
+    planes, coeffs = synth.random_sbvr(O, I, k, seed=seed)
+    X = synth.activations(I, seed=seed + synth.X_SEED_OFFSET, batch=B)
+    W = packed(sb, planes, coeffs)
+    Y_ref = oracle.sbvr_gemv(planes, coeffs, X)
+    assert abs(Y_ref[0, 0]) < 2e-4
+    Y = run_gemm(sb, W, X)
+    for b in range(B):
+        assert rel_err(Y[b], Y_ref[b]) <= TOL, (b, rel_err(Y[b], Y_ref[b]))
+        assert rel_err(run_gemv(sb, W, X[b]), Y_ref[b]) <= TOL, b
+
+
+def outlier_activations(I, ratio, seed, batch=1, per_block=3):
+    """N(0, 1) binary16 activations with `per_block` elements of every
+    512-element block replaced by +-ratio (activation outliers: a few
+    channels far above the rest)."""
+    rng = np.random.default_rng(seed)
+    X = rng.standard_normal((batch, I))
+    for b in range(batch):
+        for g0 in range(0, I, 512):
+            pos = g0 + rng.choice(min(512, I - g0), size=min(per_block, I - g0), replace=False)
+            X[b, pos] = ratio * rng.choice([-1.0, 1.0], size=pos.size)
+    return X.astype(np.float16)
+
+
+@pytest.mark.parametrize("ratio", [100.0, 1000.0, 30000.0])
+@pytest.mark.parametrize("O,I", [(1024, 4096), (4096, 4096), (14336, 4096), (4096, 14336)])
+def test_activation_outliers_plain_gate(sb, O, I, ratio):
+    """Activation blocks with a few outliers 100x, 1000x and 30000x above the
+    N(0, 1) bulk: every other element of the block is many binary16 binades
+    below the block maximum.  Batch 1 (one-shot and streaming kernels) and
+    B = 2, 8 against the oracle with the plain gate."""
+    planes, coeffs = synth.random_sbvr(O, I, 4, seed=O + 3 * I + int(ratio))
+    W = packed(sb, planes, coeffs)
+    X = outlier_activations(I, ratio, seed=int(ratio) + O, batch=8)
+    Y_ref = oracle.sbvr_gemv(planes, coeffs, X)
+    err1 = rel_err(run_gemv(sb, W, X[0]), Y_ref[0])
+    Y2 = run_gemm(sb, W, X[:2])
+    Y8 = run_gemm(sb, W, X)
+    err2 = max(rel_err(Y2[b], Y_ref[b]) for b in range(2))
+    err8 = max(rel_err(Y8[b], Y_ref[b]) for b in range(8))
+    log(f"outliers x{ratio:g} {O}x{I}: B=1 {err1:.3e} B=2 {err2:.3e} B=8 {err8:.3e}")
+    assert max(err1, err2, err8) <= TOL
+
+
 def test_output_canary_and_error_paths(sb):
     O, I = 100, 512
     planes, coeffs = synth.random_sbvr(O, I, 4, seed=3)

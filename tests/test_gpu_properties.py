@@ -7,8 +7,7 @@ k in 1..4, B in 1..8.  Each example checks, on the same seeded SBVR tensors
 activations:
   - sbvr_gemv (B = 1) or sbvr_gemm_small_batch (B > 1) against the oracle's
     binary64 GEMV of the exactly decoded matrix, per vector, within the gate
-    max|y - y_ref| / max|y_ref| <= 1e-3 (with a denominator that does not
-    collapse when a few rows cancel to tiny outputs: see rel_err);
+    max|y - y_ref| / max|y_ref| <= 1e-3;
   - sbvr_gemv_a8 against the oracle's W4A8 result (SBVR-8 activations);
   - sbvr_decompress bit for bit against rounding the oracle's exact decoding;
   - the coefficient-cache format (a random table and index) against the
@@ -17,6 +16,8 @@ The launch shape (one-shot or streaming kernel, tiles and gblocks per
 workgroup, ring depth) follows from O and I, so the draws cover ragged row
 tiles, ragged gblocks and every kernel variant of these sizes.
 """
+import os
+
 import numpy as np
 import pytest
 
@@ -31,7 +32,9 @@ from hypothesis import strategies as st  # noqa: E402
 pytestmark = pytest.mark.gpu
 
 TOL = 1e-3
-SETTINGS = settings(max_examples=40, deadline=None, derandomize=True, database=None,
+# 40 draws per test by default; SBVR_PROPERTY_EXAMPLES raises it for a wider sweep
+EXAMPLES = int(os.environ.get("SBVR_PROPERTY_EXAMPLES", "40"))
+SETTINGS = settings(max_examples=EXAMPLES, deadline=None, derandomize=True, database=None,
                     suppress_health_check=[HealthCheck.function_scoped_fixture, HealthCheck.too_slow])
 
 
@@ -46,19 +49,11 @@ def dev(a):
     return torch.from_numpy(np.ascontiguousarray(a)).cuda()
 
 
-def rel_err(y, y_ref, W_hat, x):
-    """max|y - y_ref| over the larger of max|y_ref| and the largest
-    root-sum-square of a row's products sqrt(sum_j (w_hat[o][j] x[j])^2).
-
-    The second term only matters when every output is much smaller than its
-    products (cancellation, e.g. a single row): the kernels' activation
-    limbs are exact down to 1/32 of a 512-element block's maximum and off by
-    at most 2^-15 of it below that, an error on the scale of the products,
-    not of a cancelled sum.  For matrices of many rows max|y_ref| is the
-    larger term and this is the plain gate."""
+def rel_err(y, y_ref):
+    """The gate's measure for one vector: max|y - y_ref| / max|y_ref| (an
+    all-zero reference asks for an all-zero result)."""
     y = np.asarray(y, dtype=np.float64)
-    rss = np.sqrt(((W_hat * np.asarray(x, dtype=np.float64)[None, :]) ** 2).sum(axis=1)).max()
-    den = max(np.abs(y_ref).max(), rss)
+    den = np.abs(y_ref).max()
     return float(np.abs(y - y_ref).max() / den) if den > 0 else float(np.abs(y).max())
 
 
@@ -86,9 +81,8 @@ def test_random_shapes_gemv_and_small_batch(sb, shape, B):
     torch.cuda.synchronize()
     Y = Y.cpu().numpy().astype(np.float64)
     Y_ref = np.atleast_2d(oracle.sbvr_gemv(planes, coeffs, X))
-    W_hat = decoded(planes, coeffs)
     for b in range(B):
-        assert rel_err(Y[b], Y_ref[b], W_hat, X[b].astype(np.float64)) <= TOL, (O, I, k, B, b)
+        assert rel_err(Y[b], Y_ref[b]) <= TOL, (O, I, k, B, b, rel_err(Y[b], Y_ref[b]))
 
 
 @SETTINGS
@@ -104,7 +98,7 @@ def test_random_shapes_w4a8_and_decompress(sb, shape):
     M = sb.decompress(W)
     torch.cuda.synchronize()
     W_hat = decoded(planes, coeffs)
-    assert rel_err(y.cpu().numpy(), oracle.sbvr_gemv_w4a8(planes, coeffs, x), W_hat, x.astype(np.float64)) <= TOL
+    assert rel_err(y.cpu().numpy(), oracle.sbvr_gemv_w4a8(planes, coeffs, x)) <= TOL
     with np.errstate(over="ignore"):
         want = W_hat.astype(np.float16).view(np.uint16)
     assert np.array_equal(M.cpu().numpy().view(np.uint16), want)
@@ -123,6 +117,4 @@ def test_random_shapes_coefficient_cache(sb, shape, sets_per_ten):
     x = synth.activations(I, seed=seed + synth.X_SEED_OFFSET)
     y = sb.gemv_indexed(Wi, dev(x))
     torch.cuda.synchronize()
-    W_hat = decoded(planes, oracle.gather_coefficients(index, table))
-    assert rel_err(y.cpu().numpy(), oracle.sbvr_gemv_indexed(planes, index, table, x), W_hat,
-                   x.astype(np.float64)) <= TOL
+    assert rel_err(y.cpu().numpy(), oracle.sbvr_gemv_indexed(planes, index, table, x)) <= TOL
