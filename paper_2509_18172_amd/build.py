@@ -14,8 +14,8 @@ SOURCES = [os.path.join(HERE, "csrc", f) for f in ("api.hip", "pack.hip", "gemv_
 SOURCE_FLAGS = {
     "encode.hip": ["-ffp-contract=off"],
     # leading scalar kernel arguments preloaded into SGPRs (batch-1 kernels)
-    "gemv_b1.hip": ["-mllvm", "-amdgpu-kernarg-preload-count=6"],
-    "gemv_b1s.hip": ["-mllvm", "-amdgpu-kernarg-preload-count=7"],
+    "gemv_b1.hip": ["-mllvm", "-amdgpu-kernarg-preload-count=8"],
+    "gemv_b1s.hip": ["-mllvm", "-amdgpu-kernarg-preload-count=10"],
 }
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

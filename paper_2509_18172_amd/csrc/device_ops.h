@@ -83,15 +83,17 @@ __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane
 
 // Power-of-two exponent sigma with max|x| * 2^sigma in [2^13, 2^14): the
 // scaled activations times 1/alpha (<= 2) stay below 2^15, inside both the
-// binary16 and the E5M2 range (largest finite E5M2 value 57344).  A zero
-// block gets sigma = 0.
+// binary16 and the E5M2 range (largest finite E5M2 value 57344).  sigma is
+// capped at 29: a block whose maximum is below 2^-16 holds only binary16
+// subnormals, multiples of 2^-24, which 2^28 already lifts to multiples of
+// 2^4 (exact in the split below).  A zero block gets sigma = 0.
 __device__ __forceinline__ int scale_exponent(float amax)
 {
     if (!(amax > 0.f))
         return 0;
     int e;
     frexpf(amax, &e);
-    return 14 - e;
+    return min(14 - e, 29);
 }
 
 // Four 8-bit limbs of eight activations, two words each (bytes in element
@@ -121,8 +123,10 @@ __device__ __forceinline__ uint32_t h2_pow2(int e)
 
 // Exact split of eight binary16 activations into four E5M2 limbs.
 //
-// x' = x * 2^(sigma + inv_alpha) is formed in binary16 (powers of two, in
-// steps of at most 2^15: exact, the block maximum lands in [2^12, 2^15)).
+// x' = x * 2^(sigma + inv_alpha) is formed in binary16 as two exact
+// power-of-two products, 2^(min(sigma, 14) + inv_alpha) and then
+// 2^(sigma - min(sigma, 14)) <= 2^15 (no branch); the block maximum lands in
+// [2^12, 2^15) (or below, all of it exact, for blocks of subnormals).
 // The truncation split p0 = x' with its mantissa cut to two bits,
 // p1 = the same cut of x' - p0, p2 = the cut of x' - p0 - p1 and
 // p3 = x' - p0 - p1 - p2 is exact in binary16 (each difference is a multiple
@@ -140,14 +144,9 @@ __device__ __forceinline__ Limbs split_limbs(uint4 xv, int sigma, int inv_alpha)
 {
     constexpr uint32_t CUT = 0xFF00FF00u;  // sign, exponent and 2 mantissa bits of each half
     const int s0 = min(sigma, 14);
-    const uint32_t f = h2_pow2(s0 + inv_alpha);
-    uint32_t w[4] = {h2_mul(xv.x, f), h2_mul(xv.y, f), h2_mul(xv.z, f), h2_mul(xv.w, f)};
-    for (int rem = sigma - s0; rem > 0; rem -= 15) {  // blocks below 2^-1: further exact steps
-        const uint32_t g = h2_pow2(min(rem, 15));
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-            w[i] = h2_mul(w[i], g);
-    }
+    const uint32_t f = h2_pow2(s0 + inv_alpha), g = h2_pow2(sigma - s0);
+    uint32_t w[4] = {h2_mul(h2_mul(xv.x, f), g), h2_mul(h2_mul(xv.y, f), g), h2_mul(h2_mul(xv.z, f), g),
+                     h2_mul(h2_mul(xv.w, f), g)};
     uint32_t p[4][4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {

@@ -47,12 +47,13 @@ namespace sbvr {
 
 // vectors per column set, and the LDS staging per wavefront: the limbs of
 // two vectors at a time, [group][vector of the pair][limb][128 bytes], then
-// 32 zero bytes (a set of four vectors is staged in two phases, which keeps
-// eight wavefronts' staging within 33 KB)
+// 256 zero bytes, read by the columns of absent vectors at a different 16
+// bytes per lane of a 16-lane group (a set of four vectors is staged in two
+// phases, which keeps eight wavefronts' staging within 35 KB)
 constexpr int SBS_VPS = 4;
 __host__ __device__ constexpr int sbs_sets(int nb) { return (nb + SBS_VPS - 1) / SBS_VPS; }
 __host__ __device__ constexpr int sbs_vps(int nb) { return nb < SBS_VPS ? nb : SBS_VPS; }
-__host__ __device__ constexpr int sbs_stage_bytes(int) { return GB * 2 * 4 * GROUP + 32; }
+__host__ __device__ constexpr int sbs_stage_bytes(int) { return GB * 2 * 4 * GROUP + 256; }
 
 // max |x| over the wavefront for two activation vectors at once (eight
 // binary16 values per lane each): the magnitudes' bit patterns are compared as
@@ -138,7 +139,7 @@ __global__ void __launch_bounds__(512) gemm_sbs_kernel(GemvArgs a)
     constexpr int NS = sbs_sets(NB);
     constexpr int VPS = sbs_vps(NB);
     constexpr int STAGE = sbs_stage_bytes(NB);
-    constexpr int ZERO = STAGE - 32;
+    constexpr int ZERO0 = STAGE - 256;
     extern __shared__ __align__(16) unsigned char smem[];
     const int lane = threadIdx.x & 63;
     const int wv = wave_id();
@@ -207,8 +208,8 @@ __global__ void __launch_bounds__(512) gemm_sbs_kernel(GemvArgs a)
         issue(j);
     __builtin_amdgcn_sched_barrier(0);
 
-    if (lane < 2)
-        *(uint4 *)(stage + ZERO + 16 * lane) = make_uint4(0u, 0u, 0u, 0u);
+    *(uint32_t *)(stage + ZERO0 + 4 * lane) = 0u;  // the zero region
+    const int ZERO = ZERO0 + 16 * (lane & 15);
     // B operand reads: lane (column n = lane%16 = (vector n/4, limb n%4),
     // k-block lane/16) takes k = 16 kb + [0,16) and 64 + 16 kb + [0,16) of
     // its vector's limb; absent vectors read the zero chunk.

@@ -29,8 +29,11 @@
 
 namespace sbvr {
 
-// per wavefront: [q][s][l][32 B] limb chunks, then 32 zero bytes
-constexpr int B1_WAVE_LDS = 2048 + 32;
+// per wavefront: [q][s][l][32 B] limb chunks, then 256 zero bytes (the
+// operand halves a lane does not cover read 16 of them, a different 16 for
+// each lane of a 16-lane group: reading one shared chunk from most lanes
+// serialised the LDS reads, about 0.3 us on the latency-bound launches)
+constexpr int B1_WAVE_LDS = 2048 + 256;
 
 template <int K, int T>
 struct B1Regs {
@@ -42,14 +45,16 @@ struct B1Regs {
 
 // A8: activations converted online to SBVR-8.  IX: coefficient-cache format
 // (index blocks + table of coefficient sets) instead of per-group coefficients.
-// The fields every wavefront needs before its first loads come again as
-// leading scalar arguments: the compiler preloads those into SGPRs at launch
-// (built with -amdgpu-kernarg-preload-count), so the first loads do not wait
-// for a kernel-argument fetch; the rest are read from the struct.
+// The fields every wavefront needs (its first loads' addresses and sizes, and
+// the output) come again as leading scalar arguments: the compiler preloads
+// those into SGPRs at launch (built with -amdgpu-kernarg-preload-count), so
+// neither the first loads nor the LDS waits before the matrix-core work sit
+// behind a kernel-argument fetch (a scalar load shares the LDS wait counter);
+// the rest are read from the struct.  The wavefront count is the gblock count.
 template <int K, int T, bool A8, bool IX>
 __global__ void __launch_bounds__(1024) gemv_b1_kernel(const uint4 *planes_, const uint16_t *coeffs_,
                                                        const uint16_t *x_, int I_, int n_tiles_, int n_gblocks_,
-                                                       GemvArgs a_rest)
+                                                       uint16_t *y_, int O_, GemvArgs a_rest)
 {
     GemvArgs a = a_rest;
     a.planes = planes_;
@@ -58,11 +63,13 @@ __global__ void __launch_bounds__(1024) gemv_b1_kernel(const uint4 *planes_, con
     a.I = I_;
     a.n_tiles = n_tiles_;
     a.n_gblocks = n_gblocks_;
+    a.y = y_;
+    a.O = O_;
 
     extern __shared__ __align__(16) unsigned char smem[];
     const int lane = threadIdx.x & 63;
     const int wv = wave_id();
-    const int nw = blockDim.x >> 6;
+    const int nw = a.n_gblocks;  // one wavefront per gblock
     unsigned char *lds = smem + wv * B1_WAVE_LDS;
     float *red = (float *)(smem + nw * B1_WAVE_LDS);
 
@@ -128,7 +135,7 @@ __global__ void __launch_bounds__(1024) gemv_b1_kernel(const uint4 *planes_, con
     // limbs 2 and 3 of the SBVR-8 codes are zero: those columns read zeros
     const bool act = (!A8 || l < 2) && ((kb >> 1) == (s & 1));
     const int data_off = (s * 4 + l) * 32 + 16 * (kb & 1);
-    const int zero_off = 2048;
+    const int zero_off = 2048 + 16 * (lane & 15);
     // the k-block half a lane does not cover reads the zero chunk for every q
     const int lo_off = (act && s < 2) ? data_off : zero_off;
     const int hi_off = (act && s >= 2) ? data_off : zero_off;
@@ -183,9 +190,8 @@ __global__ void __launch_bounds__(1024) gemv_b1_kernel(const uint4 *planes_, con
         }
     };
 
-    // the zero chunk read by the columns of the other k-blocks
-    if (lane < 2)
-        *(uint4 *)(lds + zero_off + 16 * lane) = make_uint4(0u, 0u, 0u, 0u);
+    // the zero region read by the columns of the other k-blocks
+    *(uint32_t *)(lds + 2048 + 4 * lane) = 0u;
 
     {
         B1Regs<K, T> R;
@@ -234,7 +240,7 @@ __global__ void __launch_bounds__(1024) gemv_b1_kernel(const uint4 *planes_, con
                 red[(wv * T + t) * TR + lrow + p] = acc[t][p];
     }
     __syncthreads();
-    for (int idx = threadIdx.x; idx < T * TR; idx += blockDim.x) {
+    for (int idx = threadIdx.x; idx < T * TR; idx += 64 * nw) {
         const int o = row_base + idx;
         if (o < a.O) {
             float v = 0.f;
@@ -307,7 +313,7 @@ int launch_gemv_b1(const Dims &d, const WeightRef &w, const uint16_t *x, uint16_
                      : d.k == 3 ? b1_kernel_for<3>(T, a8, ix)
                      : d.k == 2 ? b1_kernel_for<2>(T, a8, ix)
                                 : b1_kernel_for<1>(T, a8, ix);
-    void *args[] = {&a.planes, &a.coeffs, &a.x, &a.I, &a.n_tiles, &a.n_gblocks, &a};
+    void *args[] = {&a.planes, &a.coeffs, &a.x, &a.I, &a.n_tiles, &a.n_gblocks, &a.y, &a.O, &a};
     return launch_kernel(fn, dim3(grid), dim3(64 * waves), lds, stream, args);
 }
 

@@ -34,8 +34,11 @@
 
 namespace sbvr {
 
-// per wavefront: [q][s][l][32 B] limb chunks, then 32 zero bytes
-constexpr int B1S_WAVE_LDS = 2048 + 32;
+// per wavefront: [q][s][l][32 B] limb chunks, then 256 zero bytes (the
+// operand halves a lane does not cover read 16 of them, a different 16 for
+// each lane of a 16-lane group: reading one shared chunk from most lanes
+// serialised the LDS reads, about 0.3 us on the latency-bound launches)
+constexpr int B1S_WAVE_LDS = 2048 + 256;
 // Ring depth: one gblock per wavefront keeps 64 VGPRs (8 wavefronts per
 // SIMD) at depth 2; with several gblocks the workgroups are fewer and a
 // deeper ring keeps enough bytes in flight.
@@ -81,14 +84,16 @@ constexpr int B1S_WAVE_LDS = 2048 + 32;
 // item m is consumed, and the sets of item m+D are gathered then from the
 // index block loaded D items earlier, so neither the index load nor the gather
 // waits on anything issued less than D items before.
-// The fields every wavefront needs before its first loads come again as
-// leading scalar arguments: the compiler preloads those into SGPRs at launch
-// (built with -amdgpu-kernarg-preload-count), so the first loads do not wait
-// for a kernel-argument fetch; the rest are read from the struct.
+// The fields every wavefront needs (its first loads' addresses and sizes, the
+// output and the wavefront count) come again as leading scalar arguments: the
+// compiler preloads those into SGPRs at launch (built with
+// -amdgpu-kernarg-preload-count), so neither the first loads nor the LDS
+// waits before the matrix-core work sit behind a kernel-argument fetch (a
+// scalar load shares the LDS wait counter); the rest are read from the struct.
 template <int K, int D, bool MULTI, bool A8, bool IX>
 __global__ void __launch_bounds__(1024) gemv_b1s_kernel(const uint4 *planes_, const uint16_t *coeffs_,
                                                         const uint16_t *x_, int I_, int n_tiles_, int n_gblocks_, int tpw_,
-                                                        GemvArgs a_rest)
+                                                        uint16_t *y_, int O_, int nw_, GemvArgs a_rest)
 {
     GemvArgs a = a_rest;
     a.planes = planes_;
@@ -98,11 +103,13 @@ __global__ void __launch_bounds__(1024) gemv_b1s_kernel(const uint4 *planes_, co
     a.n_tiles = n_tiles_;
     a.n_gblocks = n_gblocks_;
     a.tpw = tpw_;
+    a.y = y_;
+    a.O = O_;
 
     extern __shared__ __align__(16) unsigned char smem[];
     const int lane = threadIdx.x & 63;
     const int wv = wave_id();
-    const int nw = blockDim.x >> 6;
+    const int nw = nw_;  // wavefronts in the workgroup
     unsigned char *lds = smem + wv * B1S_WAVE_LDS;
     constexpr int TR = tile_rows(K), NP = partials_per_lane<K>();
     float *red = (float *)(smem + nw * B1S_WAVE_LDS);  // [tpw][nw][TR]
@@ -236,15 +243,14 @@ __global__ void __launch_bounds__(1024) gemv_b1s_kernel(const uint4 *planes_, co
     // limbs 2 and 3 of the SBVR-8 codes are zero: those columns read zeros
     const bool act = (!A8 || l < 2) && ((kb >> 1) == (s & 1));
     const int data_off = (s * 4 + l) * 32 + 16 * (kb & 1);
-    const int zero_off = 2048;
+    const int zero_off = 2048 + 16 * (lane & 15);
     // the k-block half a lane does not cover reads the zero chunk for every q
     const int lo_off = (act && s < 2) ? data_off : zero_off;
     const int hi_off = (act && s >= 2) ? data_off : zero_off;
     const int lo_step = (act && s < 2) ? 512 : 0;
     const int hi_step = (act && s >= 2) ? 512 : 0;
     const int inv_alpha = inv_alpha_exp(lane & 3);
-    if (lane < 2)
-        *(uint4 *)(lds + zero_off + 16 * lane) = make_uint4(0u, 0u, 0u, 0u);
+    *(uint32_t *)(lds + 2048 + 4 * lane) = 0u;  // the zero region
 
     v8i Bq[4];
     float inv_scale;
@@ -315,7 +321,7 @@ __global__ void __launch_bounds__(1024) gemv_b1s_kernel(const uint4 *planes_, co
 
     __syncthreads();
     const int row_base = tile0 * TR;
-    for (int idx = threadIdx.x; idx < ntl * TR; idx += blockDim.x) {
+    for (int idx = threadIdx.x; idx < ntl * TR; idx += 64 * nw) {
         const int o = row_base + idx;
         if (o < a.O) {
             const float *r = red + (idx / TR) * nw * TR + (idx % TR);
@@ -380,7 +386,8 @@ int launch_gemv_b1s(const Dims &d, const WeightRef &w, const uint16_t *x, uint16
                      : d.k == 3 ? b1s_kernel_for<3>(multi, short_run, wide, a8, ix)
                      : d.k == 2 ? b1s_kernel_for<2>(multi, short_run, wide, a8, ix)
                                 : b1s_kernel_for<1>(multi, short_run, wide, a8, ix);
-    void *args[] = {&a.planes, &a.coeffs, &a.x, &a.I, &a.n_tiles, &a.n_gblocks, &a.tpw, &a};
+    int nw = waves;
+    void *args[] = {&a.planes, &a.coeffs, &a.x, &a.I, &a.n_tiles, &a.n_gblocks, &a.tpw, &a.y, &a.O, &nw, &a};
     return launch_kernel(fn, dim3(grid), dim3(64 * waves), lds, stream, args);
 }
 

@@ -3,9 +3,10 @@ activations, checked against the error bound the kernels' documentation
 states (no GPU needed).
 
 The kernels scale a 512-element block by 2^(sigma + inv_alpha) in binary16
-(sigma = 14 - e for a block maximum in [2^(e-1), 2^e); inv_alpha in
-{1, 0, -1}), cut the result three times to two mantissa bits (mask 0xFF00)
-and keep the top byte of each piece, which is read as an E5M2 number.  This
+(sigma = min(14 - e, 29) for a block maximum in [2^(e-1), 2^e); inv_alpha in
+{1, 0, -1}; two exact power-of-two products), cut the result three times to
+two mantissa bits (mask 0xFF00) and keep the top byte of each piece, which is
+read as an E5M2 number.  This
 model does the same steps with numpy's binary16 arithmetic (each operation
 rounded to nearest, the IEEE rule the GPU's binary16 instructions follow) and
 checks, over every finite binary16 value below a block maximum:
@@ -24,7 +25,7 @@ def scale_exponent(amax):
     if amax == 0:
         return 0
     _, e = np.frexp(np.float64(amax))
-    return 14 - int(e)
+    return min(14 - int(e), 29)
 
 
 def pow2_h(e):
@@ -36,10 +37,7 @@ def split_model(x, sigma, inv_alpha):
     """x: float16 array -> (x', four uint8 limb arrays) as the kernels do it."""
     s0 = min(sigma, 14)
     w = (x * pow2_h(s0 + inv_alpha)).astype(np.float16)
-    rem = sigma - s0
-    while rem > 0:
-        w = (w * pow2_h(min(rem, 15))).astype(np.float16)
-        rem -= 15
+    w = (w * pow2_h(sigma - s0)).astype(np.float16)
     pieces = []
     r = w
     for _ in range(3):
@@ -62,7 +60,7 @@ def e5m2_value(byte):
     return sign * val
 
 
-@pytest.mark.parametrize("amax", [65504.0, 3.75, 1.0, 0.4, 2.0 ** -14, 1e-6, 2.0 ** -24])
+@pytest.mark.parametrize("amax", [65504.0, 3.75, 1.0, 0.4, 2.0 ** -14, 3e-5, 1e-6, 2.0 ** -24])
 @pytest.mark.parametrize("inv_alpha", [1, 0, -1])
 def test_split_is_exact_above_the_stated_floor(amax, inv_alpha):
     amax = float(np.float16(amax))
