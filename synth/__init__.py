@@ -31,6 +31,9 @@ def seed_for(config: int, layer: int = 0, proj: int = 0) -> int:
     return 1000 * config + 16 * layer + proj
 
 
+CHUNK = 1 << 20  # Box-Muller pairs per chunk
+
+
 class Stream:
     """Counter-free stream of raw 64-bit words from PCG64(seed)."""
 
@@ -40,20 +43,40 @@ class Stream:
     def raw(self, n: int) -> np.ndarray:
         return np.asarray(self._bg.random_raw(int(n)), dtype=np.uint64)
 
+    @staticmethod
+    def _unit(r: np.ndarray) -> np.ndarray:
+        """Doubles in [0, 1) from the top 53 bits of raw words."""
+        return (r >> np.uint64(11)).astype(np.float64) * (1.0 / 9007199254740992.0)
+
     def uniform01(self, n: int) -> np.ndarray:
         """Doubles in [0, 1) from the top 53 bits of each raw word."""
-        r = self.raw(n) >> np.uint64(11)
-        return r.astype(np.float64) * (1.0 / 9007199254740992.0)
+        return self._unit(self.raw(n))
+
+    def _pairs(self, m: int, chunk: int = CHUNK):
+        """Box-Muller over the next 2m raw words: pair i takes u1 = 1 - unit
+        of word i and u2 = unit of word m + i.  Yields (first pair, rad*cos,
+        rad*sin) chunk by chunk (bounded temporaries) and leaves the stream
+        after the 2m words."""
+        g1 = self._bg
+        g2 = np.random.PCG64()
+        g2.state = g1.state
+        g2.advance(m)
+        for a in range(0, m, chunk):
+            c = min(chunk, m - a)
+            u1 = 1.0 - self._unit(np.asarray(g1.random_raw(c), dtype=np.uint64))  # (0, 1]
+            u2 = self._unit(np.asarray(g2.random_raw(c), dtype=np.uint64))
+            rad = np.sqrt(-2.0 * np.log(u1))
+            yield a, rad * np.cos(2.0 * np.pi * u2), rad * np.sin(2.0 * np.pi * u2)
+        g1.advance(m)
 
     def normal(self, n: int) -> np.ndarray:
-        """Standard normals by Box-Muller, two per pair of uniforms."""
+        """Standard normals by Box-Muller, two per pair of uniforms: z[2i] and
+        z[2i+1] from words i and m + i of the next 2m = 2 ceil(n/2) words."""
         m = (int(n) + 1) // 2
-        u1 = 1.0 - self.uniform01(m)  # (0, 1]
-        u2 = self.uniform01(m)
-        rad = np.sqrt(-2.0 * np.log(u1))
         z = np.empty(2 * m)
-        z[0::2] = rad * np.cos(2.0 * np.pi * u2)
-        z[1::2] = rad * np.sin(2.0 * np.pi * u2)
+        for a, zc, zs in self._pairs(m):
+            z[2 * a:2 * (a + zc.size):2] = zc
+            z[2 * a + 1:2 * (a + zc.size):2] = zs
         return z[:n]
 
     def below(self, bound: int) -> int:
@@ -65,7 +88,12 @@ class Stream:
 def weights(O: int, I: int, sigma: float, seed: int, outlier_frac: float = 0.0) -> np.ndarray:
     """fp32 [O][I] weights: fp32(sigma * z), plus round(frac*O*I) outliers at +-8 sigma."""
     st = Stream(seed)
-    W = (sigma * st.normal(O * I)).astype(np.float32)
+    n = O * I
+    W = np.empty(n + (n & 1), dtype=np.float32)  # fp32(sigma * z), z = st.normal(n)
+    for a, zc, zs in st._pairs((n + 1) // 2):
+        W[2 * a:2 * (a + zc.size):2] = (sigma * zc).astype(np.float32)
+        W[2 * a + 1:2 * (a + zc.size):2] = (sigma * zs).astype(np.float32)
+    W = W[:n]
     n_out = int(round(outlier_frac * O * I))
     if n_out:
         total = O * I
