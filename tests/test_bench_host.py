@@ -67,3 +67,28 @@ def test_more_than_one_gpu_is_refused():
                        capture_output=True, text=True, timeout=60)
     assert r.returncode == 2
     assert "one GPU" in r.stderr
+
+
+def test_kernel_summary_groups_dispatches(tmp_path):
+    """--kernel-summary: per (instance, workgroup, grid) mean and median of
+    end - start, and the machine-readable record the bench reads back."""
+    cols = ["Kind", "Kernel_Name", "Start_Timestamp", "End_Timestamp", "Workgroup_Size_X", "Grid_Size_X"]
+    gate = "void sbvr::gemv_b1s_kernel<4, 4, false, false, false>(HIP_vector_type<unsigned int, 4u> const*)"
+    kv = "void sbvr::gemv_b1_kernel<4, 1, false, false>(HIP_vector_type<unsigned int, 4u> const*)"
+    rows = [(gate, 1000, 8000, 512, 131072), (gate, 9000, 16200, 512, 131072), (gate, 20000, 27400, 512, 131072),
+            (kv, 30000, 32600, 512, 131072), ("other_kernel(int)", 0, 5, 64, 64)]
+    path = tmp_path / "trace.csv"
+    with open(path, "w", newline="") as fh:
+        w = csv.writer(fh)
+        w.writerow(cols)
+        for name, a, b, wg, grid in rows:
+            w.writerow(["KERNEL_DISPATCH", name, a, b, wg, grid])
+    text = bench.kernel_summary(str(path))
+    assert "| `gemv_b1s_kernel<4, 4, false, false, false>` | 512 | 131072 | 3 | 7200 | 7200 | 7000 | 7400 |" in text
+    assert "other_kernel" not in text
+    rec = [line for line in text.splitlines() if line.startswith("rocprof-record:")]
+    import json
+    r = json.loads(rec[0].split(":", 1)[1])
+    assert r["kernels"]["gemv_b1s_kernel<4, 4, false, false, false>"] == {
+        "workgroup": 512, "grid": 131072, "calls": 3, "mean_ns": 7200.0, "median_ns": 7200.0}
+    assert r["source_sha256"] == bench.kernel_source_digest()
