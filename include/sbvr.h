@@ -78,15 +78,19 @@ int sbvr_version(void);
 /*
  * Size queries (pure host functions, no HIP calls).  Bytes the caller must
  * provide for the device planes / device coefficients of an O x I matrix
- * with k planes; 0 if the arguments are invalid.
+ * with k planes (the k bitvectors and k coefficients per 128-weight group of
+ * Sec. 4.1, stored as in Sec. 4.4, plus the device layout's zero padding of
+ * the last row tile and the last 512-element block); 0 if the arguments are
+ * invalid.
  */
 size_t sbvr_packed_plane_bytes(int O, int I, int k);
 size_t sbvr_packed_coeff_bytes(int O, int I, int k);
 
 /*
  * Workspace a GEMV call needs, in bytes (0 means none: pass workspace = NULL
- * and ws_bytes = 0).  The current kernels reduce split-K partial sums inside
- * one workgroup and need no global workspace.
+ * and ws_bytes = 0).  The inner-product sum of Sec. 4.4 is split over the
+ * wavefronts of one workgroup and reduced there, so the current kernels need
+ * no global workspace.
  */
 size_t sbvr_workspace_bytes(int O, int I, int k, int B);
 
@@ -103,9 +107,10 @@ int sbvr_pack(int O, int I, int k, const uint32_t *planes_canon, const uint16_t 
               void *planes_dev, void *coeffs_dev, hipStream_t stream);
 
 /*
- * Inverse of sbvr_pack: recover the canonical tensors, bit for bit, from the
- * device format.  Same shapes and ownership as sbvr_pack with the roles of
- * input and output exchanged.
+ * Inverse of sbvr_pack: recover the canonical tensors (the bitvectors and
+ * coefficients of Sec. 4.1 in the storage order of Sec. 4.4), bit for bit,
+ * from the device format.  Same shapes and ownership as sbvr_pack with the
+ * roles of input and output exchanged.
  */
 int sbvr_unpack(int O, int I, int k, const void *planes_dev, const void *coeffs_dev,
                 uint32_t *planes_canon, uint16_t *coeffs_canon, hipStream_t stream);
@@ -123,10 +128,14 @@ int sbvr_gemv(int O, int I, int k, const void *planes_dev, const void *coeffs_de
               hipStream_t stream);
 
 /*
- * Small-batch SBVR GEMM: Y[b][o] as sbvr_gemv for each of the B activation
- * vectors X[b][0..I), with the weights read from memory once for all B.
- *   X  binary16 [B][I] row-major (input);  Y  binary16 [B][O] row-major (output).
- *   1 <= B <= 8.
+ * Small-batch SBVR GEMM: the GEMV of Sec. 4.4 applied to each of the B
+ * activation vectors X[b][0..I) (the paper's kernel handles one token per
+ * decode step; a batch of B tokens multiplies the same SBVR weights B times),
+ *     Y[b][o] = fp16_rne( sum_g sum_i c[o][g][i] * sum_j b[o][g][i][j] X[b][128 g + j] ),
+ * with the weights read from memory once for all B.
+ *   X  binary16 [B][I] row-major (input);  Y  binary16 [B][O] row-major
+ *   (output, every element written).  1 <= B <= 8.  workspace / ws_bytes as
+ *   sbvr_gemv.  X must not overlap Y.
  */
 int sbvr_gemm_small_batch(int O, int I, int k, const void *planes_dev, const void *coeffs_dev,
                           const uint16_t *X, uint16_t *Y, int B, void *workspace,
@@ -215,6 +224,17 @@ int sbvr_decompress(int O, int I, int k, const void *planes_dev, const void *coe
                     hipStream_t stream);
 
 /*
+ * Prefill decompression of the coefficient-cache format: as sbvr_decompress
+ * with c[o][g][i] = table[index[o][g]][i] (zero for an index >= n_sets).
+ * planes_dev, index_dev, table_dev from sbvr_pack_indexed; W as for
+ * sbvr_decompress.
+ */
+int sbvr_decompress_indexed(int O, int I, int k, int n_sets, const void *planes_dev, const void *index_dev,
+                            const void *table_dev, uint16_t *W, hipStream_t stream);
+
+#define SBVR_ENCODE_MAX_ENTRIES 65536
+
+/*
  * SBVR encoding on the GPU (Algorithm 1 and the bitvector assignment of
  * Sec. 4.2): every 128-weight group of W takes, from the (r, s, b) grid of
  * Eqs. 4-11 with |R1| = n_ratio1, |R2| = n_ratio2, N_scale = n_scale and
@@ -234,16 +254,6 @@ int sbvr_decompress(int O, int I, int k, const void *planes_dev, const void *coe
  * At most SBVR_ENCODE_MAX_ENTRIES grid entries ((n_ratio1 + n_ratio2) *
  * n_scale * n_bias); more is SBVR_E_UNSUPPORTED.
  */
-/*
- * Prefill decompression of the coefficient-cache format: as sbvr_decompress
- * with c[o][g][i] = table[index[o][g]][i] (zero for an index >= n_sets).
- * planes_dev, index_dev, table_dev from sbvr_pack_indexed; W as for
- * sbvr_decompress.
- */
-int sbvr_decompress_indexed(int O, int I, int k, int n_sets, const void *planes_dev, const void *index_dev,
-                            const void *table_dev, uint16_t *W, hipStream_t stream);
-
-#define SBVR_ENCODE_MAX_ENTRIES 65536
 int sbvr_encode(int O, int I, int k, const float *W, int n_ratio1, int n_ratio2, int n_scale, int n_bias,
                 int normalise, uint32_t *planes_canon, uint16_t *coeffs_canon, double *mse,
                 hipStream_t stream);

@@ -41,10 +41,13 @@
  *       s = absmax / (2^(l-1) - 1).
  *   R12 Activation vectors are the 128-element groups of the inner dimension,
  *       the ones that meet a weight group in the inner product (Sec. 4.4).
- *   R13 The grid point is the conventional integer-grid rounding the section
- *       adopts: t = x / s in binary32, q = t rounded to nearest even, within
- *       +-(2^(l-1) - 1); s and t are binary32 (the precision the GPU kernel
- *       takes this decision in); an all-zero vector has s = 0 and q = 0.
+ *   R13 The grid point is the conventional integer-grid rounding Sec. 4.3
+ *       adopts (round to nearest, as the RTN of Sec. 3.1): t = x / s, q = t
+ *       rounded to nearest even, within +-(2^(l-1) - 1); an all-zero vector
+ *       has s = 0 and q = 0.  The paper names no precision for s and t; they
+ *       are binary32, the default floating-point type of the PyTorch and
+ *       CUDA implementation Sec. 5.1 describes (binary16 activations
+ *       promoted to it), with correctly rounded division.
  */
 #include <math.h>
 #include <pthread.h>

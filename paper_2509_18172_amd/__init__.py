@@ -222,6 +222,26 @@ class PackedWeight:
                             torch.empty(cb, dtype=torch.uint8, device=device))
 
 
+def _out(out, shape, x):
+    """The output tensor: a new fp16 tensor on x's device, or the caller's,
+    which must be fp16, contiguous, of exactly `shape` and on x's device (the
+    kernels write every element of it)."""
+    torch = _torch()
+    if out is None:
+        return torch.empty(shape, dtype=torch.float16, device=x.device)
+    assert out.dtype == torch.float16 and out.is_contiguous() and tuple(out.shape) == tuple(shape), \
+        f"out must be a contiguous fp16 tensor of shape {tuple(shape)}"
+    assert out.device == x.device, "out must be on the activations' device"
+    return out
+
+
+def _check_input(W, x, shape):
+    torch = _torch()
+    assert x.dtype == torch.float16 and x.is_contiguous() and tuple(x.shape) == tuple(shape), \
+        f"activations must be a contiguous fp16 tensor of shape {tuple(shape)}"
+    assert x.is_cuda and x.device == W.planes.device, "activations must be on the weights' device"
+
+
 def pack(planes_canon, coeffs_canon, stream=None) -> PackedWeight:
     """Repack canonical device tensors (int32/uint32 [O][G][k][4], int16/uint16
     [O][G][k]) into a PackedWeight."""
@@ -229,6 +249,7 @@ def pack(planes_canon, coeffs_canon, stream=None) -> PackedWeight:
     assert four == 4 and tuple(coeffs_canon.shape) == (O, G, k)
     assert planes_canon.is_contiguous() and coeffs_canon.is_contiguous()
     assert planes_canon.element_size() == 4 and coeffs_canon.element_size() == 2
+    assert planes_canon.is_cuda and coeffs_canon.device == planes_canon.device, "canonical tensors must be on the GPU"
     W = PackedWeight.alloc(O, G * GROUP, k, device=planes_canon.device)
     _check(sbvr_pack(O, G * GROUP, k, planes_canon.data_ptr(), coeffs_canon.data_ptr(),
                      W.planes.data_ptr(), W.coeffs.data_ptr(), _stream(stream)), "sbvr_pack")
@@ -248,9 +269,8 @@ def unpack(W: PackedWeight, stream=None):
 
 def gemv(W: PackedWeight, x, out=None, stream=None):
     """y = SBVR(W) x for x fp16 [I]; returns fp16 [O]."""
-    torch = _torch()
-    assert x.dtype == torch.float16 and x.is_contiguous() and x.shape == (W.I,)
-    y = torch.empty(W.O, dtype=torch.float16, device=x.device) if out is None else out
+    _check_input(W, x, (W.I,))
+    y = _out(out, (W.O,), x)
     _check(sbvr_gemv(W.O, W.I, W.k, W.planes.data_ptr(), W.coeffs.data_ptr(), x.data_ptr(),
                      y.data_ptr(), None, 0, _stream(stream)), "sbvr_gemv")
     return y
@@ -258,10 +278,10 @@ def gemv(W: PackedWeight, x, out=None, stream=None):
 
 def gemm_small_batch(W: PackedWeight, X, out=None, stream=None):
     """Y = X SBVR(W)^T for X fp16 [B][I], 1 <= B <= 8; returns fp16 [B][O]."""
-    torch = _torch()
-    assert X.dtype == torch.float16 and X.is_contiguous() and X.dim() == 2 and X.shape[1] == W.I
+    assert X.dim() == 2
     B = X.shape[0]
-    Y = torch.empty((B, W.O), dtype=torch.float16, device=X.device) if out is None else out
+    _check_input(W, X, (B, W.I))
+    Y = _out(out, (B, W.O), X)
     _check(sbvr_gemm_small_batch(W.O, W.I, W.k, W.planes.data_ptr(), W.coeffs.data_ptr(),
                                  X.data_ptr(), Y.data_ptr(), B, None, 0, _stream(stream)),
            "sbvr_gemm_small_batch")
@@ -271,9 +291,8 @@ def gemm_small_batch(W: PackedWeight, X, out=None, stream=None):
 def gemv_a8(W: PackedWeight, x, out=None, stream=None):
     """The W4A8 decode GEMV: x fp16 [I] converted online to SBVR-8 activations
     (per-128-group scale, 8-bit two's-complement codes); returns fp16 [O]."""
-    torch = _torch()
-    assert x.dtype == torch.float16 and x.is_contiguous() and x.shape == (W.I,)
-    y = torch.empty(W.O, dtype=torch.float16, device=x.device) if out is None else out
+    _check_input(W, x, (W.I,))
+    y = _out(out, (W.O,), x)
     _check(sbvr_gemv_a8(W.O, W.I, W.k, W.planes.data_ptr(), W.coeffs.data_ptr(), x.data_ptr(),
                         y.data_ptr(), None, 0, _stream(stream)), "sbvr_gemv_a8")
     return y
@@ -301,7 +320,8 @@ def pack_indexed(planes_canon, index_canon, table_canon, stream=None) -> Indexed
     n_sets = table_canon.shape[0]
     assert four == 4 and tuple(index_canon.shape) == (O, G) and tuple(table_canon.shape) == (n_sets, k)
     for t in (planes_canon, index_canon, table_canon):
-        assert t.is_contiguous()
+        assert t.is_contiguous() and t.is_cuda and t.device == planes_canon.device, \
+            "canonical tensors must be contiguous and on one GPU"
     assert planes_canon.element_size() == 4 and index_canon.element_size() == 2 and table_canon.element_size() == 2
     I = G * GROUP
     pb, ib, tb = sbvr_packed_plane_bytes(O, I, k), sbvr_packed_index_bytes(O, I, k), sbvr_packed_table_bytes(n_sets, k)
@@ -334,9 +354,8 @@ def unpack_indexed(W: IndexedWeight, stream=None):
 def gemv_indexed(W: IndexedWeight, x, out=None, a8: bool = False, stream=None):
     """y = SBVR(W) x on the coefficient-cache format, x fp16 [I]; with
     a8=True the activations are converted online to SBVR-8 (W4A8)."""
-    torch = _torch()
-    assert x.dtype == torch.float16 and x.is_contiguous() and x.shape == (W.I,)
-    y = torch.empty(W.O, dtype=torch.float16, device=x.device) if out is None else out
+    _check_input(W, x, (W.I,))
+    y = _out(out, (W.O,), x)
     fn, name = (sbvr_gemv_indexed_a8, "sbvr_gemv_indexed_a8") if a8 else (sbvr_gemv_indexed, "sbvr_gemv_indexed")
     _check(fn(W.O, W.I, W.k, W.n_sets, W.planes.data_ptr(), W.index.data_ptr(), W.table.data_ptr(),
               x.data_ptr(), y.data_ptr(), None, 0, _stream(stream)), name)
@@ -349,7 +368,7 @@ def encode(W, k: int, n_ratio1: int = 8, n_ratio2: int = 8, n_scale: int = 16, n
     returns (planes int32 [O][G][k][4], coeffs int16 [O][G][k][, mse float64
     [O][G]]) device tensors.  Defaults: the 1024-entry search grid."""
     torch = _torch()
-    assert W.dtype == torch.float32 and W.is_contiguous() and W.dim() == 2
+    assert W.dtype == torch.float32 and W.is_contiguous() and W.dim() == 2 and W.is_cuda
     O, I = W.shape
     G = I // GROUP
     planes = torch.empty((O, G, k, 4), dtype=torch.int32, device=W.device)
@@ -366,6 +385,7 @@ def decompress(W, out=None, stream=None):
     torch = _torch()
     M = torch.empty((W.O, W.I), dtype=torch.float16, device=W.planes.device) if out is None else out
     assert M.dtype == torch.float16 and M.is_contiguous() and tuple(M.shape) == (W.O, W.I)
+    assert M.device == W.planes.device, "out must be on the weights' device"
     if isinstance(W, IndexedWeight):
         _check(sbvr_decompress_indexed(W.O, W.I, W.k, W.n_sets, W.planes.data_ptr(), W.index.data_ptr(),
                                        W.table.data_ptr(), M.data_ptr(), _stream(stream)), "sbvr_decompress_indexed")

@@ -21,6 +21,13 @@ int check_shape(int O, int I, int k)
     // element offsets inside the kernels are 32-bit
     if ((long long)O * I > (1ll << 31) - 1)
         return SBVR_E_UNSUPPORTED;
+    // byte offsets within a workgroup's range of tiles are 32-bit and must stay
+    // below the per-lane "read zero" offset (2^30): one tile's plane bytes over
+    // all gblocks (n_gblocks * GB * TR * k * 16) are capped at 2^26, i.e.
+    // I <= 2^25 at k = 4 (the activation offsets of a row then fit an int too)
+    const Dims d = make_dims(O, I, k);
+    if ((long long)d.n_gblocks * GB * d.tr * k * 16 > (1ll << 26))
+        return SBVR_E_UNSUPPORTED;
     return SBVR_OK;
 }
 

@@ -382,7 +382,7 @@ typedef __amdgpu_buffer_rsrc_t buf_rsrc;
 constexpr unsigned BUF_DWORD3 = 0x00020000u;  // raw (untyped) buffer, gfx9 family
 constexpr int BUF_NT = 2;                     // non-temporal cache policy
 constexpr unsigned BUF_OOB = 0x80000000u;     // an offset beyond every range used here
-constexpr unsigned LANE_OOB = 0x40000000u;    // per-lane offset that reads zero (ranges stay below 2^30)
+constexpr unsigned LANE_OOB = 0x40000000u;    // per-lane offset that reads zero (the host caps ranges below 2^30)
 
 __device__ __forceinline__ buf_rsrc make_rsrc(const void *base, unsigned bytes)
 {

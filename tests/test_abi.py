@@ -113,6 +113,21 @@ def test_algorithmic_bytes_formula():
     assert sb.algorithmic_bytes(4096, 4096, 4, B=8) == 9_568_256
 
 
+def test_row_length_limit():
+    """One tile's plane bytes over a whole row are capped at 2^26 (32-bit
+    byte offsets inside a workgroup stay below the read-zero offset 2^30):
+    a single row of 2^31 - 128 elements, or of 2^25 + 512 at k = 4, is
+    refused before any pointer is touched; 2^25 at k = 4 and k = 2 (1 KiB
+    plane blocks) is accepted by the size queries."""
+    for O, I, k in [(1, (1 << 31) - 128, 4), (1, (1 << 25) + 512, 4), (3, (1 << 25) + 512, 2)]:
+        assert sb.sbvr_packed_plane_bytes(O, I, k) == 0, (O, I, k)
+        assert gemv(O=O, I=I, k=k) == sb.SBVR_E_UNSUPPORTED
+        assert sb.sbvr_gemv_a8(O, I, k, FAKE, FAKE, FAKE, FAKE, None, 0, 0) == sb.SBVR_E_UNSUPPORTED
+        assert sb.sbvr_decompress(O, I, k, FAKE, FAKE, FAKE, 0) == sb.SBVR_E_UNSUPPORTED
+    assert sb.sbvr_packed_plane_bytes(1, 1 << 25, 4) == (1 << 26)
+    assert sb.sbvr_packed_plane_bytes(2, 1 << 25, 2) == (1 << 26)  # one 8-row tile
+
+
 def test_element_count_limit():
     """O * I must stay below 2^31 (the kernels' element offsets are 32-bit):
     the size queries return 0 and every entry point rejects the shape before

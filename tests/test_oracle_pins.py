@@ -538,3 +538,22 @@ def test_indexed_generator_shapes_and_range():
     assert planes.shape == (7, 3, 2, 4) and index.shape == (7, 3) and table.shape == (65536, 2)
     _, index1, _ = synth.random_indexed_sbvr(7, 384, 2, 1, seed=1)
     assert np.all(index1 == 0)
+
+
+def test_rtn_comparators_hand_values():
+    """The RTN comparators (Sec. 3.1, Eq. 2 with the step read as
+    max|w| / (2^(b-1) - 1), reading R7; asymmetric min-max RTN with 2^b
+    levels) on D = {-3, ..., 4} * 2^-6, every quotient exact in binary64:
+      symmetric 2 bits: delta = 2^-4, q = (-1, 0, 0, 0, 0, 0, 1, 1) (the
+        ties -0.5 and 0.5 go to even), errors (1, -2, -1, 0, 1, 2, -1, 0) *
+        2^-6, MSE = 12 / 8 * 2^-12;
+      asymmetric 2 bits: delta = 7/3 * 2^-6, q = (0, 0, 1, 1, 2, 2, 3, 3),
+        errors (0, 1, -1/3, 2/3, -2/3, 1/3, -1, 0) * 2^-6, MSE = 7/18 * 2^-12;
+      asymmetric 3 bits: delta = 2^-6, every point on the grid, MSE = 0."""
+    D = np.arange(-3, 5, dtype=np.float64) * 2.0 ** -6
+    assert oracle.rtn_sym_mse(D, 2) == 1.5 * 2.0 ** -12
+    np.testing.assert_allclose(oracle.rtn_asym_mse(D, 2), 7.0 / 18.0 * 2.0 ** -12, rtol=1e-12)
+    assert oracle.rtn_asym_mse(D, 3) == 0.0
+    # a constant group and an all-zero group have nothing to round away
+    assert oracle.rtn_asym_mse(np.full(8, 0.3), 2) == 0.0
+    assert oracle.rtn_sym_mse(np.zeros(8), 3) == 0.0
