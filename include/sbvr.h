@@ -72,7 +72,7 @@ const char *sbvr_status_string(int status);
 
 /* Library ABI version (major * 100 + minor); 1.01 adds sbvr_decompress,
  * 1.02 sbvr_gemv_a8, 1.03 the coefficient-cache format entry points,
- * 1.04 sbvr_encode and sbvr_decompress_indexed. */
+ * 1.04 sbvr_encode and sbvr_decompress_indexed, 1.05 sbvr_gemm_prefill. */
 int sbvr_version(void);
 
 /*
@@ -154,6 +154,22 @@ int sbvr_gemm_small_batch(int O, int I, int k, const void *planes_dev, const voi
 int sbvr_gemv_a8(int O, int I, int k, const void *planes_dev, const void *coeffs_dev,
                  const uint16_t *x, uint16_t *y, void *workspace, size_t ws_bytes,
                  hipStream_t stream);
+
+/*
+ * Prefill GEMM on SBVR weights (the prefill design of Sec. 5.1: the weights
+ * are decompressed to binary16 and multiplied on the matrix cores), for a
+ * prompt of T tokens, without writing the decompressed matrix to memory:
+ *     Y[t][o] = fp16_rne( sum_j X[t][j] * fp16_rne(w_hat[o][j]) ),
+ * where fp16_rne(w_hat[o][j]) is the correctly rounded subset sum of
+ * Sec. 4.1 (the value sbvr_decompress writes); binary32 accumulation.
+ *   planes_dev, coeffs_dev  device-format weights from sbvr_pack.
+ *   X  binary16 [T][I] row-major (input, 16-byte aligned);
+ *   Y  binary16 [T][O] row-major (output, every element written).
+ *   T >= 1.  X must not overlap Y.  The result does not depend on how the
+ *   work is split (fixed reduction order).
+ */
+int sbvr_gemm_prefill(int O, int I, int k, const void *planes_dev, const void *coeffs_dev, const uint16_t *X,
+                      uint16_t *Y, int T, hipStream_t stream);
 
 /*
  * COEFFICIENT-CACHE FORMAT (Sec. 4.4): the coefficients are stored once per

@@ -31,7 +31,7 @@ EXPORTED = (
     "sbvr_workspace_bytes", "sbvr_pack", "sbvr_unpack", "sbvr_gemv", "sbvr_gemm_small_batch",
     "sbvr_decompress", "sbvr_gemv_a8", "sbvr_packed_index_bytes", "sbvr_packed_table_bytes",
     "sbvr_pack_indexed", "sbvr_unpack_indexed", "sbvr_gemv_indexed", "sbvr_gemv_indexed_a8", "sbvr_encode",
-    "sbvr_decompress_indexed",
+    "sbvr_decompress_indexed", "sbvr_gemm_prefill",
 )
 
 
@@ -76,6 +76,7 @@ def _load():
         "sbvr_gemv_indexed_a8": (i32, [i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, sz, vp]),
         "sbvr_encode": (i32, [i32, i32, i32, vp, i32, i32, i32, i32, i32, vp, vp, vp, vp]),
         "sbvr_decompress_indexed": (i32, [i32, i32, i32, i32, vp, vp, vp, vp, vp]),
+        "sbvr_gemm_prefill": (i32, [i32, i32, i32, vp, vp, vp, vp, i32, vp]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -177,6 +178,10 @@ def sbvr_decompress(O, I, k, planes_dev, coeffs_dev, W, stream=0) -> int:
 
 def sbvr_decompress_indexed(O, I, k, n_sets, planes_dev, index_dev, table_dev, W, stream=0) -> int:
     return _lib.sbvr_decompress_indexed(O, I, k, n_sets, planes_dev, index_dev, table_dev, W, stream)
+
+
+def sbvr_gemm_prefill(O, I, k, planes_dev, coeffs_dev, X, Y, T, stream=0) -> int:
+    return _lib.sbvr_gemm_prefill(O, I, k, planes_dev, coeffs_dev, X, Y, T, stream)
 
 
 # --------------------------------------------------------------------------
@@ -377,6 +382,18 @@ def encode(W, k: int, n_ratio1: int = 8, n_ratio2: int = 8, n_scale: int = 16, n
     _check(sbvr_encode(O, I, k, W.data_ptr(), n_ratio1, n_ratio2, n_scale, n_bias, int(normalise), planes.data_ptr(),
                        coeffs.data_ptr(), mse.data_ptr() if want_mse else None, _stream(stream)), "sbvr_encode")
     return (planes, coeffs, mse) if want_mse else (planes, coeffs)
+
+
+def gemm_prefill(W: PackedWeight, X, out=None, stream=None):
+    """Y = X fp16(W_hat)^T for a prompt X fp16 [T][I] (prefill GEMM on the
+    SBVR weights, decoded on the fly); returns fp16 [T][O]."""
+    assert X.dim() == 2
+    T = X.shape[0]
+    _check_input(W, X, (T, W.I))
+    Y = _out(out, (T, W.O), X)
+    _check(sbvr_gemm_prefill(W.O, W.I, W.k, W.planes.data_ptr(), W.coeffs.data_ptr(), X.data_ptr(), Y.data_ptr(), T,
+                             _stream(stream)), "sbvr_gemm_prefill")
+    return Y
 
 
 def decompress(W, out=None, stream=None):

@@ -9,7 +9,7 @@ import subprocess
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 SOURCES = [os.path.join(HERE, "csrc", f) for f in ("api.hip", "pack.hip", "gemv_b1.hip", "gemv_b1s.hip", "gemm_sbs.hip",
-                                                  "decompress.hip", "encode.hip")]
+                                                  "decompress.hip", "encode.hip", "prefill.hip")]
 # The encoder's binary64 arithmetic is its definition: no fused multiply-add.
 SOURCE_FLAGS = {
     "encode.hip": ["-ffp-contract=off"],

@@ -121,7 +121,7 @@ const char *sbvr_status_string(int status)
     }
 }
 
-int sbvr_version(void) { return 104; }
+int sbvr_version(void) { return 105; }
 
 size_t sbvr_packed_plane_bytes(int O, int I, int k)
 {
@@ -281,6 +281,19 @@ int sbvr_decompress(int O, int I, int k, const void *planes_dev, const void *coe
     if (!aligned(planes_dev, 16) || !aligned(coeffs_dev, 16) || !aligned(W, 16))
         return SBVR_E_ALIGNMENT;
     return launch_decompress(make_dims(O, I, k), per_group_weights(planes_dev, coeffs_dev), W, stream);
+}
+
+int sbvr_gemm_prefill(int O, int I, int k, const void *planes_dev, const void *coeffs_dev, const uint16_t *X,
+                      uint16_t *Y, int T, hipStream_t stream)
+{
+    int st = check_shape(O, I, k);
+    if (st != SBVR_OK)
+        return st;
+    if (T < 1 || !planes_dev || !coeffs_dev || !X || !Y)
+        return SBVR_E_INVALID_ARG;
+    if (!aligned(planes_dev, 16) || !aligned(coeffs_dev, 16) || !aligned(X, 16) || !aligned(Y, 2))
+        return SBVR_E_ALIGNMENT;
+    return launch_prefill(make_dims(O, I, k), planes_dev, coeffs_dev, X, Y, T, stream);
 }
 
 int sbvr_decompress_indexed(int O, int I, int k, int n_sets, const void *planes_dev, const void *index_dev,

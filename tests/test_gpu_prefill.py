@@ -1,0 +1,163 @@
+"""The prefill GEMM on SBVR weights (sbvr_gemm_prefill) against the oracle.
+
+  * Per token, the oracle's exact result y_ref = W_hat x (binary64, exactly
+    decoded weights) with the gate max|y - y_ref| / max|y_ref| <= 1e-3.
+  * The weights the kernel multiplies are pinned bit for bit: with unit
+    vectors as tokens, Y[t][o] is one product 1 * w, exact, so it must equal
+    the correctly rounded binary16 weight (numpy's rounding of the oracle's
+    exact decoding -- the matrix sbvr_decompress writes).
+"""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-3
+
+
+@pytest.fixture(scope="module")
+def sb():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2509_18172_amd as m
+    return m
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def log(msg):
+    print(msg, flush=True)
+
+
+def packed(sb, planes, coeffs):
+    W = sb.pack(dev(planes.view(np.int32)), dev(coeffs.view(np.int16)))
+    torch.cuda.synchronize()
+    return W
+
+
+def run(sb, W, X):
+    Y = sb.gemm_prefill(W, dev(X))
+    torch.cuda.synchronize()
+    return Y.cpu().numpy().astype(np.float64)
+
+
+def rel_err(y, y_ref):
+    den = np.abs(y_ref).max()
+    return float(np.abs(y - y_ref).max() / den) if den > 0 else float(np.abs(y).max())
+
+
+def fp16_weights(planes, coeffs, rows=None):
+    with np.errstate(over="ignore"):
+        Wh = oracle.decompress(planes if rows is None else planes[rows], coeffs if rows is None else coeffs[rows])
+        return Wh.astype(np.float16).astype(np.float64)
+
+
+def check(Y, X, planes, coeffs, rows=None, what=""):
+    """Per token: the exact-weight gate."""
+    y_ref = oracle.sbvr_gemv(planes, coeffs, X, rows=rows)
+    Yr = Y if rows is None else Y[:, rows]
+    worst = max(rel_err(Yr[t], y_ref[t]) for t in range(X.shape[0]))
+    log(f"prefill {what}: worst per-token err vs exact weights {worst:.3e}")
+    assert worst <= TOL, (what, worst)
+
+
+def check_unit_tokens(sb, W, planes, coeffs, cols, what=""):
+    """Tokens e_j for the columns `cols`: Y[t][o] must be fp16(w_hat[o][j_t])."""
+    I = planes.shape[1] * 128
+    X = np.zeros((len(cols), I), dtype=np.float16)
+    X[np.arange(len(cols)), cols] = 1.0
+    Y = sb.gemm_prefill(W, dev(X))
+    torch.cuda.synchronize()
+    want = fp16_weights(planes, coeffs)[:, cols].T
+    got = Y.cpu().numpy().astype(np.float64)
+    assert np.array_equal(got, want), (what, int((got != want).sum()))
+
+
+@pytest.mark.parametrize("T", [1, 16, 64, 512])
+def test_prefill_oracle_encoded(sb, T):
+    """An oracle-encoded 1024 x 4096 matrix (N(0, 0.02^2) with outliers,
+    Algorithm 1, k = 4), prompts of 1, 16, 64 and 512 tokens."""
+    O, I = 1024, 4096
+    W = synth.weights(O, I, 0.02, seed=synth.seed_for(1, 0, 1), outlier_frac=0.001)
+    planes, coeffs = oracle.encode_matrix(W, 4)
+    X = synth.activations(I, seed=700 + T, batch=T)
+    check(run(sb, packed(sb, planes, coeffs), X), X, planes, coeffs, what=f"encoded {O}x{I} T={T}")
+
+
+@pytest.mark.parametrize("O,I,k,T", [(1, 128, 4, 1), (1001, 640, 3, 37), (70, 896, 2, 130), (33, 2560, 1, 17),
+                                     (257, 4096, 4, 65), (64, 256, 4, 16), (129, 1152, 2, 3)])
+def test_prefill_ragged(sb, O, I, k, T):
+    """Row counts that are not a multiple of the 64-row workgroup (nor of the
+    device tile), token counts that are not a multiple of 16, ragged last
+    gblocks, k = 1..4, one group per K-slice and more."""
+    planes, coeffs = synth.random_sbvr(O, I, k, seed=O + 3 * I + k)
+    W = packed(sb, planes, coeffs)
+    X = synth.activations(I, seed=O + T, batch=T)
+    check(run(sb, W, X), X, planes, coeffs, what=f"ragged {O}x{I} k={k} T={T}")
+    # every column of the first and the last group, as unit tokens
+    cols = np.r_[np.arange(128), np.arange(I - 128, I)] if I > 128 else np.arange(128)
+    check_unit_tokens(sb, W, planes, coeffs, cols, what=f"ragged {O}x{I} k={k}")
+
+
+@pytest.mark.parametrize("O,I", [(14336, 4096), (4096, 14336), (1024, 4096)])
+@pytest.mark.parametrize("T", [64, 512])
+def test_prefill_full_size_sampled(sb, O, I, T):
+    """Llama-3-8B projection shapes at the benchmark's prompt lengths, on
+    sampled rows (first and last included) and every token."""
+    planes, coeffs = synth.random_sbvr(O, I, 4, seed=O + 7 * I)
+    X = synth.activations(I, seed=T + O, batch=T)
+    rows = np.unique(np.r_[0, O - 1, np.random.default_rng(T).integers(0, O, 62)])
+    check(run(sb, packed(sb, planes, coeffs), X), X, planes, coeffs, rows=rows, what=f"full {O}x{I} T={T}")
+
+
+def test_prefill_wide_coefficient_span(sb):
+    """Coefficient sets spanning more than 12 binades (their subset sums are
+    not exact in binary32, so the table falls back to binary64 sums), next to
+    ordinary ones; the weights must still be the correctly rounded ones."""
+    O, I, k, T = 96, 512, 4, 20
+    planes, coeffs = synth.random_sbvr(O, I, k, seed=41)
+    c = coeffs.view(np.float16).copy()
+    c[::2, :, 3] = np.float16(3e-6) * np.sign(c[::2, :, 3]).astype(np.float16)  # a subnormal term beside ~1e-2
+    c[1::4, :, 0] = np.float16(1500.0)
+    coeffs = c.view(np.uint16)
+    X = synth.activations(I, seed=43, batch=T, scale=0.05)
+    W = packed(sb, planes, coeffs)
+    check(run(sb, W, X), X, planes, coeffs, what="wide coefficient span")
+    check_unit_tokens(sb, W, planes, coeffs, np.arange(I), what="wide coefficient span")
+
+
+def test_prefill_matches_decompress_and_is_deterministic(sb):
+    """The fused kernel multiplies the same binary16 weights sbvr_decompress
+    writes (compared with a binary64 GEMM on the decompressed matrix), and
+    repeated calls give identical bits."""
+    O, I, T = 300, 1024, 48
+    planes, coeffs = synth.random_sbvr(O, I, 4, seed=12)
+    W = packed(sb, planes, coeffs)
+    X = synth.activations(I, seed=13, batch=T)
+    M = sb.decompress(W).cpu().numpy().astype(np.float64)
+    assert np.array_equal(M, fp16_weights(planes, coeffs))
+    Y1 = sb.gemm_prefill(W, dev(X))
+    Y2 = sb.gemm_prefill(W, dev(X))
+    torch.cuda.synchronize()
+    assert torch.equal(Y1.view(torch.int16), Y2.view(torch.int16))
+    check(Y1.cpu().numpy().astype(np.float64), X, planes, coeffs, what="vs decompress")
+
+
+def test_prefill_error_paths(sb):
+    O, I = 64, 256
+    planes, coeffs = synth.random_sbvr(O, I, 4, seed=5)
+    W = packed(sb, planes, coeffs)
+    X = dev(synth.activations(I, seed=6, batch=4))
+    Y = torch.full((4, O), 7.0, dtype=torch.float16, device="cuda")
+    p, c = W.planes.data_ptr(), W.coeffs.data_ptr()
+    assert sb.sbvr_gemm_prefill(O, I, 4, p, c, X.data_ptr(), Y.data_ptr(), 0, 0) == sb.SBVR_E_INVALID_ARG
+    assert sb.sbvr_gemm_prefill(O, I, 4, p, c, X.data_ptr() + 8, Y.data_ptr(), 4, 0) == sb.SBVR_E_ALIGNMENT
+    assert sb.sbvr_gemm_prefill(O, 100, 4, p, c, X.data_ptr(), Y.data_ptr(), 4, 0) == sb.SBVR_E_INVALID_ARG
+    assert sb.sbvr_gemm_prefill(O, I, 5, p, c, X.data_ptr(), Y.data_ptr(), 4, 0) == sb.SBVR_E_UNSUPPORTED
+    torch.cuda.synchronize()
+    assert bool((Y == 7.0).all())  # nothing was written
