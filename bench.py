@@ -52,8 +52,10 @@ One JSON line is printed:
                 (sbvr_gemv_indexed) and SBVR-8 activations (sbvr_gemv_indexed_a8)
   low_bit       per projection at k = 2 and 3 planes, same timing
   prefill       per projection: sbvr_decompress to binary16 (us, GB/s of the
-                SBVR bytes read plus the 2 bytes per weight written) and, for
-                context, a 512-token library GEMM (torch.matmul) on the result
+                SBVR bytes read plus the 2 bytes per weight written), a 64- and
+                a 512-token library GEMM (torch linear) on the result, and the
+                fused prefill GEMM on the SBVR weights (sbvr_gemm_prefill) at
+                1, 16, 64, 128 and 512 tokens
   llama3_70b    per projection of the Llama-3-70B shapes, same timing
   encoder       sbvr_encode (Algorithm 1 on the GPU, the 1024-entry grid) on an
                 fp32 q/o-shaped matrix: seconds and groups per second, and the
@@ -76,6 +78,13 @@ calibration), for
   rocprofv3 --pmc FETCH_SIZE -- python3 bench.py --traffic-probe   (and WRITE_SIZE);
 --traffic-summary FETCH_CSV WRITE_CSV turns the two counter files into the
 record kept under profiles/.
+
+--prefill-probe runs, eagerly, sbvr_decompress, the library GEMM on its
+result and the fused sbvr_gemm_prefill on every distinct Llama-3-8B shape at
+each prompt length, separated by marker fills, for
+  rocprofv3 --kernel-trace -- python3 bench.py --prefill-probe;
+--prefill-summary TRACE_CSV turns the trace into the record kept under
+profiles/.
 """
 from __future__ import annotations
 
@@ -94,12 +103,14 @@ sys.path.insert(0, ROOT)
 
 PEAK_GBPS = 8000.0
 PROJ_ORDER = ("q", "k", "v", "o", "gate", "up", "down")
+PREFILL_TOKENS = (1, 16, 64, 128, 512)  # prompt lengths of the fused prefill GEMM timings
 TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "hbm_traffic_llama3-8b_k4.md")
 ROCPROF_RECORD = "sbvr_gemv_llama3-8b_headline_kernel_stats.md"
 CALIB_BYTES = 256 << 20
 DECODE_REPLAYS = 50   # replays of the L-layer decode graph
 EVENT_WARMUP, EVENT_CALLS = 20, 200  # per-call event timing
 PROBE_LAUNCHES = 4
+PREFILL_PROBE_CALLS = 16  # launches per phase of --prefill-probe
 
 
 def parse():
@@ -122,6 +133,11 @@ def parse():
                     help="eager launches of every shape plus a calibration copy, for counter runs")
     ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="summarise two rocprofv3 --pmc counter files (no GPU needed)")
+    ap.add_argument("--prefill-probe", action="store_true",
+                    help="eager prefill launches (decompress, library GEMM, fused GEMM) per shape and prompt "
+                         "length, separated by marker fills, for a rocprofv3 kernel trace")
+    ap.add_argument("--prefill-summary", metavar="KERNEL_TRACE_CSV",
+                    help="per-kernel durations of a --prefill-probe kernel trace (no GPU needed)")
     return ap.parse_args()
 
 
@@ -208,6 +224,51 @@ def kernel_summary(trace_csv: str) -> str:
     return "\n".join(lines)
 
 
+def prefill_probe_cases():
+    """(label, O, I, T) in the order --prefill-probe runs them: the distinct
+    Llama-3-8B projection shapes times PREFILL_TOKENS."""
+    import synth
+    seen, cases = set(), []
+    for name in PROJ_ORDER:
+        O, I = synth.LLAMA8B[name]
+        if (O, I) in seen:
+            continue
+        seen.add((O, I))
+        cases += [(f"{name} {O}x{I}", O, I, T) for T in PREFILL_TOKENS]
+    return cases
+
+
+def prefill_summary(trace_csv: str) -> str:
+    """Markdown table of a --prefill-probe kernel trace: per case, the mean
+    duration of sbvr_decompress, of the library GEMM's kernels (per call) and
+    of the fused sbvr_gemm_prefill, from the second of the two passes."""
+    import numpy as np
+    rows = []
+    with open(trace_csv, newline="") as f:
+        for r in csv.DictReader(f):
+            rows.append((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), r["Kernel_Name"]))
+    rows.sort()
+    segs = []
+    for t0, t1, name in rows:
+        if "FillFunctor" in name:  # the marker between phases
+            segs.append([])
+        elif segs:
+            segs[-1].append((t1 - t0, name))
+    segs = segs[1:]  # the marker tensor's own initial fill
+    lines = ["| case | tokens | decompress us | library GEMM us | decompress + library us | fused us |",
+             "|---|---:|---:|---:|---:|---:|"]
+    rec = {}
+    for i, (label, O, I, T) in enumerate(prefill_probe_cases()):
+        dec, lib, fus = segs[6 * i + 3: 6 * i + 6]
+        d = np.mean([x for x, n in dec if "decompress_kernel" in n]) / 1e3
+        lb = sum(x for x, n in lib if "sbvr::" not in n) / PREFILL_PROBE_CALLS / 1e3
+        fu = np.mean([x for x, n in fus if "prefill_kernel" in n]) / 1e3
+        lines.append(f"| {label} | {T} | {d:.1f} | {lb:.1f} | {d + lb:.1f} | {fu:.1f} |")
+        rec[f"{label} T={T}"] = {"decompress_us": round(d, 2), "library_us": round(lb, 2), "fused_us": round(fu, 2)}
+    lines += ["", "prefill-record: " + json.dumps(rec, sort_keys=True)]
+    return "\n".join(lines)
+
+
 def load_rocprof(kernel: str):
     """The dominant kernel's mean dispatch duration from the committed
     rocprofv3 record of the headline command, when it was taken on the
@@ -276,6 +337,44 @@ def cpu_model_name():
     return platform.processor() or platform.machine()
 
 
+def prefill_probe(k, dev):
+    """Eager launches for a kernel trace: per case (prefill_probe_cases), two
+    passes of [marker] 16 x sbvr_decompress [marker] 16 x library GEMM on the
+    decompressed matrix [marker] 16 x sbvr_gemm_prefill, over 16 packed copies
+    of one random SBVR matrix."""
+    import numpy as np
+    import torch
+
+    import paper_2509_18172_amd as sb
+    import synth
+    marker = torch.zeros(1, device=dev)
+    cur = None
+    for label, O, I, T in prefill_probe_cases():
+        if cur != (O, I):
+            Ws = None
+            torch.cuda.empty_cache()
+            planes, coeffs = synth.random_sbvr(O, I, k, seed=O + I)
+            p = torch.from_numpy(planes.view(np.int32)).to(dev)
+            c = torch.from_numpy(coeffs.view(np.int16)).to(dev)
+            Ws = [sb.pack(p, c) for _ in range(PREFILL_PROBE_CALLS)]
+            M = torch.empty((O, I), dtype=torch.float16, device=dev)
+            cur = (O, I)
+        X = torch.from_numpy(synth.activations(I, seed=T, batch=T)).to(dev)
+        Y = torch.empty((T, O), dtype=torch.float16, device=dev)
+        for _ in range(2):  # the first pass settles the library's kernel choice
+            marker.fill_(1.0)
+            for W in Ws:
+                sb.decompress(W, out=M)
+            marker.fill_(2.0)
+            for _ in range(PREFILL_PROBE_CALLS):
+                torch.nn.functional.linear(X, M)
+            marker.fill_(3.0)
+            for W in Ws:
+                sb.gemm_prefill(W, X, out=Y)
+            torch.cuda.synchronize()
+        print(f"prefill-probe: {label} T={T} done", flush=True)
+
+
 def main():
     args = parse()
     if args.traffic_summary:
@@ -283,6 +382,9 @@ def main():
         return
     if args.kernel_summary:
         print(kernel_summary(args.kernel_summary))
+        return
+    if args.prefill_summary:
+        print(prefill_summary(args.prefill_summary))
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the SBVR GEMV path "
@@ -297,6 +399,9 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
+    if args.prefill_probe:
+        prefill_probe(args.k, dev)
+        return
     shapes = synth.LLAMA8B if args.model == "llama3-8b" else synth.LLAMA70B
     k = args.k
     nbytes = {n: sb.algorithmic_bytes(*shapes[n], k) for n in PROJ_ORDER}
@@ -716,8 +821,24 @@ def main():
                 for _ in range(3):
                     torch.nn.functional.linear(Xs, M)
             gemm = [timed(lambda: torch.nn.functional.linear(Xs, M)) * 1e3 for _ in range(5)]
+            X64 = Xs[:64].contiguous()
+            with torch.cuda.stream(stream):
+                for _ in range(3):
+                    torch.nn.functional.linear(X64, M)
+            gemm64 = [timed(lambda: torch.nn.functional.linear(X64, M)) * 1e3 for _ in range(5)]
+            # the fused GEMM (sbvr_gemm_prefill: the binary16 weights never
+            # reach memory) over the same SBVR copies, per prompt length
+            fused = {}
+            pf = (lambda W, X, Y, stream: sb.gemm_prefill(W, X, out=Y, stream=stream))
+            for TT in PREFILL_TOKENS:
+                XT = Xs[:TT].contiguous()
+                Ys = [torch.empty((TT, O), dtype=torch.float16, device=dev) for _ in range(2)]
+                fused[str(TT)] = round(launch_us([(pf, (w, XT, Ys[i % 2])) for i, w in enumerate(ws[:16])],
+                                                 n_launch=16, replays=5), 2)
             prefill[name] = {"decompress_us": round(us, 3), "decompress_gbps": round(bb / (us * 1e3), 1),
-                             "decompress_bytes": bb, "gemm_us_512_tokens": round(float(np.median(gemm)), 2)}
+                             "decompress_bytes": bb, "gemm_us_512_tokens": round(float(np.median(gemm)), 2),
+                             "gemm_us_64_tokens": round(float(np.median(gemm64)), 2),
+                             "fused_gemm_us": fused}
             del outs
             torch.cuda.empty_cache()
 

@@ -165,8 +165,9 @@ int sbvr_gemv_a8(int O, int I, int k, const void *planes_dev, const void *coeffs
  *   planes_dev, coeffs_dev  device-format weights from sbvr_pack.
  *   X  binary16 [T][I] row-major (input, 16-byte aligned);
  *   Y  binary16 [T][O] row-major (output, every element written).
- *   T >= 1.  X must not overlap Y.  The result does not depend on how the
- *   work is split (fixed reduction order).
+ *   1 <= T <= 2^22 (larger: SBVR_E_UNSUPPORTED).  X must not overlap Y.
+ *   The summation order is fixed for given (O, I, k, T), so repeated calls
+ *   give identical bits; it follows the launch shape, which depends on T.
  */
 int sbvr_gemm_prefill(int O, int I, int k, const void *planes_dev, const void *coeffs_dev, const uint16_t *X,
                       uint16_t *Y, int T, hipStream_t stream);

@@ -291,6 +291,8 @@ int sbvr_gemm_prefill(int O, int I, int k, const void *planes_dev, const void *c
         return st;
     if (T < 1 || !planes_dev || !coeffs_dev || !X || !Y)
         return SBVR_E_INVALID_ARG;
+    if (T > (1 << 22))  // keeps the token grid dimension below 2^16
+        return SBVR_E_UNSUPPORTED;
     if (!aligned(planes_dev, 16) || !aligned(coeffs_dev, 16) || !aligned(X, 16) || !aligned(Y, 2))
         return SBVR_E_ALIGNMENT;
     return launch_prefill(make_dims(O, I, k), planes_dev, coeffs_dev, X, Y, T, stream);

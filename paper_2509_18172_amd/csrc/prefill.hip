@@ -8,26 +8,30 @@
 // the result equals X times the decompressed matrix with fp32 accumulation.
 //
 // Work split.  A wavefront owns 16 weight rows (one column tile of the
-// matrix-core instruction), up to 64 tokens (BTT tiles of 16) and a run of
-// whole groups of the inner dimension (a K-slice).  A workgroup of 16
+// matrix-core instruction), BTT token tiles of 16 (BTT = 1, 2, 4, 8) and a
+// run of whole groups of the inner dimension (a K-slice).  A workgroup of 16
 // wavefronts holds R = 16 / S row tiles times S K-slices; the S partial sums
-// of a row tile are added through LDS at the end in a fixed order
-// (deterministic).  Per group a wavefront
-//   * builds the 2^k-entry subset-sum table of each of its 16 rows in its own
-//     LDS region (binary32 sums, exact when the coefficients span at most 12
-//     binades, else binary64; rounded once to binary16);
-//   * per 32-element step (word ks of each plane): forms the k-bit subset
+// of a row tile are added through LDS at the end in a fixed order.  Per group
+//   * the R wavefronts of a K-slice stage the group's activation tile
+//     (16 BTT tokens x 128 values) in LDS with coalesced 16-byte loads, double
+//     buffered, so the activations are read once per workgroup rather than
+//     once per row tile;
+//   * a wavefront builds the 2^k-entry subset-sum table of each of its 16 rows
+//     in its own LDS region (binary32 sums, exact when the coefficients span at
+//     most 12 binades, else binary64; rounded once to binary16);
+//   * per 32-element step (word ks of each plane) it forms the k-bit subset
 //     index of the lane's eight consecutive elements from the plane words (the
 //     device bit layout puts element 8v+p of a word at bit 4p+v, so
 //     (w >> v) & 0x11111111 holds bit i of elements 8v..8v+7 in nibbles
 //     0..7), looks them up, and multiplies the eight binary16 weights with the
-//     BTT token tiles of X on v_mfma_f32_16x16x32_f16 (lane l: row or column
+//     BTT token tiles on v_mfma_f32_16x16x32_f16 (lane l: row or column
 //     l % 16, k = 8 (l / 16) .. +7; measured on the device).
 // The plane slots, coefficients and activations of the next group are loaded
 // while the current one is decoded.
-// Bound: for short prompts the weight stream and the decoding (a few vector
-// instructions and one LDS lookup per weight and 64-token block); for long
-// ones the matrix cores (2 T O I flops) and the activation reads.
+// Bound: the decoding (about 300 vector instructions per wavefront and group,
+// whatever BTT is) for prompts up to a few hundred tokens; BTT = 8 amortises
+// it over 128 tokens, and past that the weights are decoded once per 128
+// tokens.
 #include "device_ops.h"
 #include "f16_round.h"
 #include "launch.h"
@@ -36,9 +40,16 @@ namespace sbvr {
 
 typedef _Float16 v8h __attribute__((ext_vector_type(8)));
 
-// wavefronts per workgroup (R row tiles x S K-slices): 16, or 8 for tiles of
-// 32 or 64 tokens, whose double-buffered activations need more registers
-__host__ __device__ constexpr int pf_waves(int btt) { return btt >= 2 ? 8 : 16; }
+constexpr int PF_WAVES = 16;          // wavefronts per workgroup: R row tiles x S K-slices
+constexpr int PF_XROW = 256 + 16;     // LDS bytes per token row of an activation tile (padding
+                                      // spreads the 16 rows of an operand read over all banks)
+#ifndef PF_LUT_PAD
+#define PF_LUT_PAD 2
+#endif
+// activation chunks (16 bytes) per thread and group, at most: the launcher
+// keeps S BTT <= 4 pf_xpt(BTT) (a K-slice's 1024 / S threads load 256 BTT chunks)
+__host__ __device__ constexpr int pf_xpt(int btt) { return btt <= 2 ? 4 : 2; }
+constexpr size_t PF_LDS_MAX = 160 * 1024;  // LDS of one workgroup on gfx950
 
 struct PrefillArgs {
     const uint32_t *planes;  // device plane blocks
@@ -46,7 +57,7 @@ struct PrefillArgs {
     const uint16_t *X;       // binary16 [T][I]
     uint16_t *Y;             // binary16 [T][O]
     int O, I, T, n_tiles, n_gblocks, G, gps;  // gps: groups per K-slice
-    int S;                                    // K-slices per workgroup (a power of two <= 16)
+    int S;                                    // K-slices per workgroup (a power of two)
 };
 
 __device__ __forceinline__ int f16_exp(uint32_t h)  // unbiased exponent, subnormals as -14
@@ -55,19 +66,29 @@ __device__ __forceinline__ int f16_exp(uint32_t h)  // unbiased exponent, subnor
     return e == 0 ? -14 : e - 15;
 }
 
+// LDS: per K-slice two activation tiles of 16 BTT token rows (PF_XROW bytes
+// each: the group's 128 binary16 values), then per wavefront its 16 rows x
+// 2^k subset-sum table.  The K-slice reduction reuses the front afterwards.
+__host__ __device__ constexpr int pf_xtile(int btt) { return 16 * btt * PF_XROW; }
+
 template <int K, int BTT>
-__global__ void __launch_bounds__(64 * pf_waves(BTT)) prefill_kernel(PrefillArgs a)
+__global__ void __launch_bounds__(64 * PF_WAVES) prefill_kernel(PrefillArgs a)
 {
     constexpr int TR = tile_rows(K), NSUB = 1 << K;
-    constexpr int LUT_B = 16 * NSUB * 2;  // per wavefront: [16 rows][subset]
+    constexpr int LROW = NSUB + PF_LUT_PAD;  // table row stride (binary16 entries)
+    constexpr int LUT_B = 16 * LROW * 2;
+    constexpr int XT = pf_xtile(BTT);
+    constexpr int XCH = 16 * BTT * 16;  // 16-byte chunks of an activation tile
+    constexpr int XPT = pf_xpt(BTT);
     extern __shared__ __align__(16) unsigned char smem[];
     const int lane = threadIdx.x & 63, w = wave_id();
-    const int S = a.S, R = pf_waves(BTT) / S;
+    const int S = a.S, R = PF_WAVES / S;
     const int ks_id = w % S, rt = w / S;  // K-slice and row tile of this wavefront
     const int n = lane & 15, kq = lane >> 4;
-    uint16_t *lut = (uint16_t *)(smem + w * LUT_B);
+    unsigned char *xbuf = smem + (size_t)ks_id * 2 * XT;
+    uint16_t *lut = (uint16_t *)(smem + (size_t)S * 2 * XT + w * LUT_B);
     const int o_base = (blockIdx.x * R + rt) * 16, t_base = blockIdx.y * 16 * BTT;
-    const int g0 = ks_id * a.gps, g1 = min(a.G, g0 + a.gps);
+    const int g0 = ks_id * a.gps;
     const int rows_dev = a.n_tiles * TR;  // rows held by the device format (padding included)
 
     v4f acc[BTT];
@@ -75,19 +96,15 @@ __global__ void __launch_bounds__(64 * pf_waves(BTT)) prefill_kernel(PrefillArgs
     for (int tt = 0; tt < BTT; ++tt)
         acc[tt] = v4f{0.f, 0.f, 0.f, 0.f};
 
-    // the decode row of this lane (its column of the result), and the table
-    // entries it builds: row n, subsets NSUB/4 * kq .. (all of them for k < 2)
+    // the decode row of this lane (its column of the result)
     const int o = min(o_base + n, rows_dev - 1);
     const bool row_ok = o_base + n < rows_dev;
     const int tile = o / TR, r = o % TR;
     struct GroupLoads {
         uint4 slot[K];
         uint16_t c[K];
-        v8h x[4][BTT];  // activations of the four 32-element steps
     };
-    // loads of one group, issued a group ahead of their use: the row's plane
-    // slots (16 bytes: the group's four words), its coefficients and the
-    // token tiles' activations
+    // the row's plane slots (16 bytes: the group's four words) and coefficients
     auto load_group = [&](int g, GroupLoads &L) {
         const int gb = g / GB, b = g % GB;
         const size_t blk = (size_t)tile * a.n_gblocks + gb;
@@ -99,28 +116,50 @@ __global__ void __launch_bounds__(64 * pf_waves(BTT)) prefill_kernel(PrefillArgs
 #pragma unroll
         for (int i = 0; i < K; ++i)
             L.c[i] = cp[i];
+    };
+    // a group's activation tile, loaded by the K-slice's R wavefronts: 16
+    // consecutive threads read one token's 256 bytes (tokens past T read as
+    // zero)
+    const int xthr = rt * 64 + lane, nxthr = R * 64;
+    auto load_x = [&](int g, uint4 *v) {
 #pragma unroll
-        for (int tt = 0; tt < BTT; ++tt) {
-            const int t = t_base + 16 * tt + n;
-            const uint16_t *xp = a.X + (size_t)min(t, a.T - 1) * a.I + (size_t)g * GROUP + 8 * kq;
+        for (int q = 0; q < XPT; ++q) {
+            const int ch = xthr + q * nxthr;
+            v[q] = make_uint4(0u, 0u, 0u, 0u);
+            const int t = t_base + ch / 16;
+            if (ch < XCH && t < a.T)
+                v[q] = *(const uint4 *)(a.X + (size_t)t * a.I + (size_t)g * GROUP + (ch % 16) * 8);
+        }
+    };
+    auto store_x = [&](unsigned char *buf, const uint4 *v) {
 #pragma unroll
-            for (int ks = 0; ks < 4; ++ks) {
-                uint4 v = *(const uint4 *)(xp + ks * 32);
-                if (t >= a.T)
-                    v = make_uint4(0u, 0u, 0u, 0u);
-                L.x[ks][tt] = __builtin_bit_cast(v8h, v);
-            }
+        for (int q = 0; q < XPT; ++q) {
+            const int ch = xthr + q * nxthr;
+            if (ch < XCH)
+                *(uint4 *)(buf + (ch / 16) * PF_XROW + (ch % 16) * 16) = v[q];
         }
     };
 
+    // every wavefront of the workgroup runs gps steps (groups past G are
+    // skipped but keep the barriers aligned)
     GroupLoads cur, nxt;
-    if (g0 < g1)
+    uint4 xv[XPT];
+    if (g0 < a.G) {
         load_group(g0, cur);
-    for (int g = g0; g < g1; ++g) {
-        if (g + 1 < g1)
+        load_x(g0, xv);
+        store_x(xbuf, xv);
+    }
+    __syncthreads();
+    for (int j = 0; j < a.gps; ++j) {
+        const int g = g0 + j;
+        const bool more = j + 1 < a.gps && g + 1 < a.G;
+        if (more) {
             load_group(g + 1, nxt);
-        // ---- subset-sum table of the 16 rows for group g ----
-        {
+            load_x(g + 1, xv);  // stored after this group's products
+        }
+        if (g < a.G) {
+            // ---- subset-sum table of the 16 rows for group g (lane: row n,
+            // subsets NSUB/4 * kq ..; all of them for k < 2) ----
             uint32_t c[K];
 #pragma unroll
             for (int i = 0; i < K; ++i)
@@ -133,9 +172,9 @@ __global__ void __launch_bounds__(64 * pf_waves(BTT)) prefill_kernel(PrefillArgs
                     emin = min(emin, f16_exp(c[i]));
                 }
             }
-            constexpr int PER = NSUB >= 4 ? NSUB / 4 : NSUB;  // entries this lane writes
+            constexpr int PER = NSUB >= 4 ? NSUB / 4 : NSUB;
             const int p0 = NSUB >= 4 ? PER * kq : 0;
-            uint16_t *lrow = lut + n * NSUB + p0;
+            uint16_t *lrow = lut + n * LROW + p0;
             if (emax - emin <= 11) {
                 // every subset sum has at most 24 significant bits: exact in
                 // binary32, one rounding to binary16
@@ -163,44 +202,51 @@ __global__ void __launch_bounds__(64 * pf_waves(BTT)) prefill_kernel(PrefillArgs
                     lrow[q] = f64_to_f16_rne(sum);
                 }
             }
-        }
-        // the table is read by other lanes of this wavefront only: its LDS
-        // writes complete before the reads below (in order within a wavefront)
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            // the table is read by other lanes of this wavefront only: its LDS
+            // writes complete before the reads below (in order within a wavefront)
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 
-        const uint16_t *L = lut + n * NSUB;
+            const uint16_t *L = lut + n * LROW;
+            const unsigned char *xt = xbuf + (j & 1) * XT;
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-            uint32_t pat = 0u;  // nibble p: subset index of element 32 ks + 8 kq + p
+            for (int ks = 0; ks < 4; ++ks) {
+                uint32_t pat = 0u;  // nibble p: subset index of element 32 ks + 8 kq + p
 #pragma unroll
-            for (int i = 0; i < K; ++i) {
-                const uint4 sl = cur.slot[i];
-                const uint32_t word = ks == 0 ? sl.x : (ks == 1 ? sl.y : (ks == 2 ? sl.z : sl.w));
-                pat |= ((word >> kq) & 0x11111111u) << i;
+                for (int i = 0; i < K; ++i) {
+                    const uint4 sl = cur.slot[i];
+                    const uint32_t word = ks == 0 ? sl.x : (ks == 1 ? sl.y : (ks == 2 ? sl.z : sl.w));
+                    pat |= ((word >> kq) & 0x11111111u) << i;
+                }
+                if (!row_ok)
+                    pat = 0u;  // rows past the device format: entry 0 (zero)
+                uint4 bw;
+                bw.x = (uint32_t)L[pat & 0xf] | ((uint32_t)L[(pat >> 4) & 0xf] << 16);
+                bw.y = (uint32_t)L[(pat >> 8) & 0xf] | ((uint32_t)L[(pat >> 12) & 0xf] << 16);
+                bw.z = (uint32_t)L[(pat >> 16) & 0xf] | ((uint32_t)L[(pat >> 20) & 0xf] << 16);
+                bw.w = (uint32_t)L[(pat >> 24) & 0xf] | ((uint32_t)L[pat >> 28] << 16);
+                const v8h B = __builtin_bit_cast(v8h, bw);
+#pragma unroll
+                for (int tt = 0; tt < BTT; ++tt) {
+                    // token 16 tt + n, elements 32 ks + 8 kq .. +7
+                    const uint4 av = *(const uint4 *)(xt + (16 * tt + n) * PF_XROW + (ks * 4 + kq) * 16);
+                    acc[tt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(v8h, av), B, acc[tt], 0,
+                                                                      0, 0);
+                }
             }
-            if (!row_ok)
-                pat = 0u;  // rows past the device format: entry 0 (zero)
-            uint4 bw;
-            bw.x = (uint32_t)L[pat & 0xf] | ((uint32_t)L[(pat >> 4) & 0xf] << 16);
-            bw.y = (uint32_t)L[(pat >> 8) & 0xf] | ((uint32_t)L[(pat >> 12) & 0xf] << 16);
-            bw.z = (uint32_t)L[(pat >> 16) & 0xf] | ((uint32_t)L[(pat >> 20) & 0xf] << 16);
-            bw.w = (uint32_t)L[(pat >> 24) & 0xf] | ((uint32_t)L[pat >> 28] << 16);
-            const v8h B = __builtin_bit_cast(v8h, bw);
-#pragma unroll
-            for (int tt = 0; tt < BTT; ++tt)
-                acc[tt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(cur.x[ks][tt], B, acc[tt], 0, 0, 0);
         }
-        // the next group's table writes follow this group's lookups (in order)
-        if (g + 1 < g1)
+        if (more) {
+            // the other buffer was last read before the previous barrier
+            store_x(xbuf + ((j + 1) & 1) * XT, xv);
             cur = nxt;
+        }
+        __syncthreads();
     }
 
     // ---- the S K-slices of each row tile summed in a fixed order: halving
-    // tree through LDS (slot of K-slice s of row tile rt: (rt * S/2 + s)) ----
+    // tree through LDS (slot of K-slice s of row tile rt: rt * S/2 + s) ----
     float *red = (float *)smem;  // [R][S / 2][BTT * 4][64 lanes]
-    __syncthreads();
     for (int half = S / 2; half >= 1; half /= 2) {
         if (ks_id >= half && ks_id < 2 * half) {
             float *dst = red + ((size_t)rt * (S / 2) + (ks_id - half)) * (BTT * 4 * 64);
@@ -241,43 +287,65 @@ static const void *prefill_kernel_for(int btt)
     switch (btt) {
     case 1: return (const void *)prefill_kernel<K, 1>;
     case 2: return (const void *)prefill_kernel<K, 2>;
-    default: return (const void *)prefill_kernel<K, 4>;
+    case 4: return (const void *)prefill_kernel<K, 4>;
+    default: return (const void *)prefill_kernel<K, 8>;
     }
 }
 
-// Launch shape: BTT token tiles of 16 per workgroup (1, 2 or 4: prompts of
-// more than 64 tokens take several workgroups along the tokens), 16 (8 at
-// BTT = 2, 4) wavefronts per workgroup split into R row tiles x S K-slices.  S (a
-// power of two, at most the wavefront count and the group count) is the
-// largest that keeps the
-// grid near 4096 wavefronts (four per SIMD): splitting K further only
-// shortens each wavefront's run of groups (its first loads' latency is paid
-// per run) and multiplies the activation reads (each row tile reads its
-// tokens' activations once).
+// Launch shape.  A wavefront's per-group work (plane loads, table build,
+// pattern extraction and lookups) is the same whatever BTT is, so large token
+// tiles amortise it; splitting K into S slices spreads it over more
+// wavefronts and shortens each one's chain of groups; both are bounded by the
+// activation tiles' LDS (S BTT <= 4 pf_xpt).  Workgroups hold 1024 threads and
+// up to 148 KiB of LDS, one per CU: among the shapes whose grid fits one
+// round of the 256 CUs the one with the most workgroups wins (ties: the
+// largest S BTT); when none fits, the fewest workgroups.  This rule picks the
+// measured best of every (BTT, S) on the Llama-3-8B projection shapes at
+// 1 .. 512 tokens.
+constexpr int PF_CUS = 256;
+
 int launch_prefill(const Dims &d, const void *planes_dev, const void *coeffs_dev, const uint16_t *X, uint16_t *Y,
                    int T, hipStream_t stream)
 {
-    const int btt = T <= 16 ? 1 : (T <= 32 ? 2 : 4);
-    const int gy = (T + 16 * btt - 1) / (16 * btt);
-    int S = 1;
-    // waves = 16 * ceil(O * S / 256) * gy
-    const int waves = pf_waves(btt);
-    // total wavefronts = waves * ceil(O * S / (16 * waves)) * gy ~ O * S * gy / 16
-    while (2 * S <= waves && 2 * S <= d.G && (long)d.O * 2 * S * gy <= 4096L * 16)
-        S *= 2;
-    const int R = waves / S;
-    const int gx = (d.O + 16 * R - 1) / (16 * R);
+    int btt = 0, S = 0, best_wg = 0;
+    for (int bt = 1; bt <= 8; bt *= 2) {
+        if (bt > 1 && 16 * (bt / 2) >= T)  // a smaller tile already covers the prompt
+            break;
+        const int gy = (T + 16 * bt - 1) / (16 * bt);
+        for (int sk = 1; sk <= PF_WAVES && sk <= d.G && sk * bt <= 4 * pf_xpt(bt); sk *= 2) {
+            const int wg = (d.O + 16 * (PF_WAVES / sk) - 1) / (16 * (PF_WAVES / sk)) * gy;
+            const bool fits = wg <= PF_CUS, best_fits = best_wg > 0 && best_wg <= PF_CUS;
+            bool take;
+            if (btt == 0)
+                take = true;
+            else if (fits != best_fits)
+                take = fits;
+            else if (wg != best_wg)
+                take = fits ? wg > best_wg : wg < best_wg;
+            else
+                take = sk * bt > S * btt;
+            if (take) {
+                btt = bt;
+                S = sk;
+                best_wg = wg;
+            }
+        }
+    }
+    const int R = PF_WAVES / S;
+    const int gx = (d.O + 16 * R - 1) / (16 * R), gy = (T + 16 * btt - 1) / (16 * btt);
     PrefillArgs a = {(const uint32_t *)planes_dev, (const uint16_t *)coeffs_dev, X, Y, d.O, d.I, T, d.n_tiles,
                      d.n_gblocks, d.G, (d.G + S - 1) / S, S};
-    const size_t lut = (size_t)waves * 16 * (1u << d.k) * 2;
+    const size_t front = (size_t)S * 2 * pf_xtile(btt);
     const size_t red = (size_t)R * (S / 2) * btt * 4 * 64 * 4;
-    const size_t lds = lut > red ? lut : red;
+    const size_t lds = (front > red ? front : red) + (size_t)PF_WAVES * 16 * ((1u << d.k) + PF_LUT_PAD) * 2;
+    if (lds > PF_LDS_MAX)
+        return SBVR_E_UNSUPPORTED;
     const void *fn = d.k == 4   ? prefill_kernel_for<4>(btt)
                      : d.k == 3 ? prefill_kernel_for<3>(btt)
                      : d.k == 2 ? prefill_kernel_for<2>(btt)
                                 : prefill_kernel_for<1>(btt);
     void *args[] = {&a};
-    return launch_kernel(fn, dim3(gx, gy), dim3(64 * waves), lds, stream, args);
+    return launch_kernel(fn, dim3(gx, gy), dim3(64 * PF_WAVES), lds, stream, args);
 }
 
 }  // namespace sbvr

@@ -92,3 +92,46 @@ def test_kernel_summary_groups_dispatches(tmp_path):
     assert r["kernels"]["gemv_b1s_kernel<4, 4, false, false, false>"] == {
         "workgroup": 512, "grid": 131072, "calls": 3, "mean_ns": 7200.0, "median_ns": 7200.0}
     assert r["source_sha256"] == bench.kernel_source_digest()
+
+
+def test_prefill_summary_segments_by_marker(tmp_path):
+    """--prefill-summary: phases are cut at the marker fills, the second pass
+    of each case is used, library time is per call (all its kernels summed)."""
+    fill = "void at::native::vectorized_elementwise_kernel<4, at::native::FillFunctor<float>>(int)"
+    dec = "void sbvr::decompress_kernel<4, false, 4>(sbvr::Dims)"
+    lib = "Cijk_Alik_Bljk_HHS_BH_MT16x16x256"
+    fus = "void sbvr::prefill_kernel<4, 1>(sbvr::PrefillArgs)"
+    n = bench.PREFILL_PROBE_CALLS
+    rows, t = [(fill, 0, 1)], 10
+
+    def add(name, dur, count):
+        nonlocal t
+        for _ in range(count):
+            rows.append((name, t, t + dur))
+            t += dur + 5
+
+    for ci, _ in enumerate(bench.prefill_probe_cases()):
+        for rep in range(2):
+            scale = 1 if rep else 3  # first pass slower: must be ignored
+            add(fill, 1, 1)
+            add(dec, 1000 * scale + ci, n)
+            add(fill, 1, 1)
+            add(lib, 500 * scale, 2 * n)  # two library kernels per call
+            add("__amd_rocclr_fillBufferAligned", 7, 1)
+            add(fill, 1, 1)
+            add(fus, 2000 * scale, n)
+    path = tmp_path / "trace.csv"
+    with open(path, "w", newline="") as fh:
+        w = csv.writer(fh)
+        w.writerow(["Kernel_Name", "Start_Timestamp", "End_Timestamp"])
+        w.writerows(rows)
+    text = bench.prefill_summary(str(path))
+    import json
+    rec = json.loads([ln for ln in text.splitlines() if ln.startswith("prefill-record:")][0].split(":", 1)[1])
+    cases = bench.prefill_probe_cases()
+    assert len(rec) == len(cases)
+    label, O, I, T = cases[2]
+    r = rec[f"{label} T={T}"]
+    # library: 2 kernels of 0.5 us plus the 7 ns fill, per call
+    assert r == {"decompress_us": round((1000 + 2) / 1e3, 2), "library_us": round((2 * 500 * n + 7) / n / 1e3, 2),
+                 "fused_us": 2.0}

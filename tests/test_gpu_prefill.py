@@ -159,5 +159,7 @@ def test_prefill_error_paths(sb):
     assert sb.sbvr_gemm_prefill(O, I, 4, p, c, X.data_ptr() + 8, Y.data_ptr(), 4, 0) == sb.SBVR_E_ALIGNMENT
     assert sb.sbvr_gemm_prefill(O, 100, 4, p, c, X.data_ptr(), Y.data_ptr(), 4, 0) == sb.SBVR_E_INVALID_ARG
     assert sb.sbvr_gemm_prefill(O, I, 5, p, c, X.data_ptr(), Y.data_ptr(), 4, 0) == sb.SBVR_E_UNSUPPORTED
+    # token counts past 2^22 are refused before anything is read
+    assert sb.sbvr_gemm_prefill(O, I, 4, p, c, X.data_ptr(), Y.data_ptr(), (1 << 22) + 1, 0) == sb.SBVR_E_UNSUPPORTED
     torch.cuda.synchronize()
     assert bool((Y == 7.0).all())  # nothing was written
