@@ -51,6 +51,9 @@ namespace sbvr {
 // bytes per lane of a 16-lane group (a set of four vectors is staged in two
 // phases, which keeps eight wavefronts' staging within 35 KB)
 constexpr int SBS_VPS = 4;
+// LDS a small-batch workgroup may use (of the 160 KiB of a gfx950 CU; one
+// workgroup per CU runs anyway at this kernel's register use)
+constexpr size_t SBS_LDS_MAX = 160 * 1024;
 __host__ __device__ constexpr int sbs_sets(int nb) { return (nb + SBS_VPS - 1) / SBS_VPS; }
 __host__ __device__ constexpr int sbs_vps(int nb) { return nb < SBS_VPS ? nb : SBS_VPS; }
 __host__ __device__ constexpr int sbs_stage_bytes(int) { return GB * 2 * 4 * GROUP + 256; }
@@ -133,6 +136,35 @@ __device__ __forceinline__ uint2 coef_group(const CoefGroups<K> &c, int g)
     }
 }
 
+// acc[p] += the coefficients times the lane's four D values of their rows
+// (rows grouped by output row as in apply_coefs), one fused multiply-add per
+// value with the binary16 coefficient converted on the way in
+template <int K>
+__device__ __forceinline__ void fma_coefs(uint2 c, const v4f &d, float *acc)
+{
+    const _Float16 c0 = __builtin_bit_cast(_Float16, (uint16_t)(c.x & 0xffffu));
+    const _Float16 c1 = __builtin_bit_cast(_Float16, (uint16_t)(c.x >> 16));
+    const _Float16 c2 = __builtin_bit_cast(_Float16, (uint16_t)(c.y & 0xffffu));
+    const _Float16 c3 = __builtin_bit_cast(_Float16, (uint16_t)(c.y >> 16));
+    constexpr int RS = row_slots(K);
+    if constexpr (RS == 4) {
+        acc[0] = fmaf((float)c0, d[0], acc[0]);
+        acc[0] = fmaf((float)c1, d[1], acc[0]);
+        acc[0] = fmaf((float)c2, d[2], acc[0]);
+        acc[0] = fmaf((float)c3, d[3], acc[0]);
+    } else if constexpr (RS == 2) {
+        acc[0] = fmaf((float)c0, d[0], acc[0]);
+        acc[0] = fmaf((float)c1, d[1], acc[0]);
+        acc[1] = fmaf((float)c2, d[2], acc[1]);
+        acc[1] = fmaf((float)c3, d[3], acc[1]);
+    } else {
+        acc[0] = fmaf((float)c0, d[0], acc[0]);
+        acc[1] = fmaf((float)c1, d[1], acc[1]);
+        acc[2] = fmaf((float)c2, d[2], acc[2]);
+        acc[3] = fmaf((float)c3, d[3], acc[3]);
+    }
+}
+
 template <int K, int NB, int D, bool MULTI>
 __global__ void __launch_bounds__(512) gemm_sbs_kernel(GemvArgs a)
 {
@@ -147,7 +179,7 @@ __global__ void __launch_bounds__(512) gemm_sbs_kernel(GemvArgs a)
     const int B = a.B;  // vectors actually present (<= NB)
     unsigned char *stage = smem + wv * STAGE;
     constexpr int TR = tile_rows(K), NP = partials_per_lane<K>();
-    float *red = (float *)(smem + nw * STAGE);  // [tpw][nw][NS][TR rows][4 vectors]
+    float *red = (float *)(smem + nw * STAGE);  // [tpw][nw][NS][TR rows][16 columns]
 
     const int tile0 = blockIdx.x * a.tpw;
     const int ntl = min(a.tpw, a.n_tiles - tile0);
@@ -288,9 +320,10 @@ __global__ void __launch_bounds__(512) gemm_sbs_kernel(GemvArgs a)
         load_x(Xn, wv + nw);
     __builtin_amdgcn_sched_barrier(0);
 
-    // red offset of this lane's (row, vector) partials; written by limb-0 lanes
-    float *red_w = red + (wv * NS * TR + (lane >> 4) * NP) * SBS_VPS + vb;
-    const int red_tile = nw * NS * TR * SBS_VPS;
+    // red offset of this lane's (row, column) partials: column n = (vector,
+    // limb) of its set; the four limbs of a vector are added in the final sum
+    float *red_w = red + (wv * NS * TR + (lane >> 4) * NP) * 16 + n;
+    const int red_tile = nw * NS * TR * 16;
     int cur_i = 0, cur_gb = wv;
     for (int m0 = 0; m0 < n_items; m0 += D) {
 #pragma unroll
@@ -320,33 +353,23 @@ __global__ void __launch_bounds__(512) gemm_sbs_kernel(GemvArgs a)
             issue(j);
 #pragma unroll
             for (int st = 0; st < NS; ++st) {
+                // the lane's (tile row, vector, limb) partials of the item:
+                // every group's coefficients chained into one accumulator
                 float acc[NP];
 #pragma unroll
                 for (int p = 0; p < NP; ++p)
                     acc[p] = 0.f;
 #pragma unroll
-                for (int g = 0; g < GB; ++g) {
-                    float part[NP];
-                    apply_coefs<K>(coef_group<K>(cr, g), d[g][st], part);
-#pragma unroll
-                    for (int p = 0; p < NP; ++p)
-                        acc[p] += part[p];
-                }
-#pragma unroll
-                for (int p = 0; p < NP; ++p) {
-                    float v = acc[p] * oscale[st];
-                    v += dpp_f32<DPP_QUAD_XOR1>(v);
-                    v += dpp_f32<DPP_QUAD_XOR2>(v);
-                    acc[p] = v;
-                }
-                if (valid && limb == 0) {
-                    float *r = red_w + cur_i * red_tile + st * TR * SBS_VPS;
+                for (int g = 0; g < GB; ++g)
+                    fma_coefs<K>(coef_group<K>(cr, g), d[g][st], acc);
+                if (valid) {
+                    float *r = red_w + cur_i * red_tile + st * TR * 16;
 #pragma unroll
                     for (int p = 0; p < NP; ++p) {
                         if (!MULTI || cur_gb == wv)
-                            r[p * SBS_VPS] = acc[p];
+                            r[p * 16] = acc[p] * oscale[st];
                         else
-                            r[p * SBS_VPS] += acc[p];
+                            r[p * 16] += acc[p] * oscale[st];
                     }
                 }
             }
@@ -367,10 +390,12 @@ __global__ void __launch_bounds__(512) gemm_sbs_kernel(GemvArgs a)
         const int o = row_base + lr;
         if (o < a.O) {
             const int st = b / SBS_VPS, v = b % SBS_VPS;
-            const float *r = red + (lr / TR) * red_tile + (st * TR + lr % TR) * SBS_VPS + v;
+            const float *r = red + (lr / TR) * red_tile + (st * TR + lr % TR) * 16 + 4 * v;
             float s = 0.f;
-            for (int w = 0; w < nw; ++w)
-                s += r[w * NS * TR * SBS_VPS];
+            for (int w = 0; w < nw; ++w) {
+                const float4 q = *(const float4 *)(r + w * NS * TR * 16);  // the vector's four limbs
+                s += (q.x + q.y) + (q.z + q.w);
+            }
             a.y[(size_t)b * a.O + o] = __half_as_ushort(__float2half_rn(s));
         }
     }
@@ -405,10 +430,10 @@ int launch_gemm_sbs(const Dims &d, const void *planes_dev, const void *coeffs_de
     const int nb = B <= 2 ? 2 : (B <= 4 ? 4 : 8);
     const int gpw = (d.n_gblocks + SBVR_SBS_MAX_WAVES - 1) / SBVR_SBS_MAX_WAVES;
     const int waves = (d.n_gblocks + gpw - 1) / gpw;
-    // tiles per workgroup, capped so that dynamic LDS stays within 64 KiB
+    // tiles per workgroup, capped so that dynamic LDS stays within SBS_LDS_MAX
     const size_t fixed = (size_t)waves * sbs_stage_bytes(nb);
-    const size_t per_tile = (size_t)waves * sbs_sets(nb) * d.tr * SBS_VPS * 4;
-    const int max_tpw = (int)((SBVR_MAX_DYN_LDS - fixed) / per_tile);
+    const size_t per_tile = (size_t)waves * sbs_sets(nb) * d.tr * 16 * 4;
+    const int max_tpw = (int)((SBS_LDS_MAX - fixed) / per_tile);
     const int tpw = min((d.n_tiles + SBVR_SBS_GROUPS - 1) / SBVR_SBS_GROUPS, max_tpw);
     const int grid = (d.n_tiles + tpw - 1) / tpw;
     const bool multi = gpw > 1;
