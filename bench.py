@@ -71,13 +71,15 @@ roofline.mean_launch_us); --kernel-summary TRACE_CSV prints per-kernel
 duration statistics of a rocprofv3 kernel trace.
 
 --traffic-probe runs, eagerly, four launches of every projection shape (fp16
-and W4A8 activations, the coefficient-cache format, and the prefill
-decompression to binary16) and an elementwise
+and W4A8 activations, small batch B = 8, the coefficient-cache format, and
+the prefill decompression to binary16) and an elementwise
 negation over 256 MiB of float32 (reads and writes 256 MiB: the counter
 calibration), for
   rocprofv3 --pmc FETCH_SIZE -- python3 bench.py --traffic-probe   (and WRITE_SIZE);
 --traffic-summary FETCH_CSV WRITE_CSV turns the two counter files into the
-record kept under profiles/.
+record kept under profiles/; --counter-summary A_CSV B_CSV does the same for
+two instruction/cycle counter passes over the probe (the pass lists are in
+counter_summary's docstring).
 
 --prefill-probe runs, eagerly, sbvr_decompress, the library GEMM on its
 result and the fused sbvr_gemm_prefill on every distinct Llama-3-8B shape at
@@ -133,6 +135,9 @@ def parse():
                     help="eager launches of every shape plus a calibration copy, for counter runs")
     ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="summarise two rocprofv3 --pmc counter files (no GPU needed)")
+    ap.add_argument("--counter-summary", nargs=2, metavar=("PASS_A_CSV", "PASS_B_CSV"),
+                    help="instruction and cycle counters per SBVR kernel from two rocprofv3 --pmc passes over "
+                         "--traffic-probe (no GPU needed)")
     ap.add_argument("--prefill-probe", action="store_true",
                     help="eager prefill launches (decompress, library GEMM, fused GEMM) per shape and prompt "
                          "length, separated by marker fills, for a rocprofv3 kernel trace")
@@ -187,13 +192,67 @@ def traffic_summary(fetch_csv: str, write_csv: str) -> str:
         "write_kib": float(np.median(write[copy])), "fetch_scale": f_scale, "write_scale": w_scale},
         "kernels": {}}
     for name in fetch:
-        if "gemv_b1" not in name:
+        if "gemv_b1" not in name and "gemm_sbs" not in name:
             continue
         short = short_kernel_name(name)
         fk, wk = float(np.median(fetch[name])), float(np.median(write.get(name, [0.0])))
         rec["kernels"][short] = {"dispatches": len(fetch[name]), "fetch_kib": fk, "write_kib": wk,
                                  "bytes_per_launch": round(fk * 1024 * f_scale + wk * 1024 * w_scale)}
     lines = ["traffic-record: " + json.dumps(rec, sort_keys=True)]
+    return "\n".join(lines)
+
+
+def read_counters(path: str):
+    """{(kernel instance, grid): {"counters": {name: [per-dispatch values]},
+    "vgpr", "agpr", "lds"}} for the SBVR kernels of a rocprofv3 counter CSV."""
+    out = {}
+    with open(path) as fh:
+        for r in csv.DictReader(fh):
+            if "sbvr::" not in r["Kernel_Name"]:
+                continue
+            key = (short_kernel_name(r["Kernel_Name"]), int(r["Grid_Size"]))
+            e = out.setdefault(key, {"counters": {}, "vgpr": int(r["VGPR_Count"]),
+                                     "agpr": int(r["Accum_VGPR_Count"]), "lds": int(r["LDS_Block_Size"])})
+            e["counters"].setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+    return out
+
+
+def counter_summary(a_csv: str, b_csv: str) -> str:
+    """Markdown table of two rocprofv3 --pmc passes over --traffic-probe:
+    pass A with SQ_WAVES SQ_INSTS_VALU SQ_INSTS_MFMA SQ_INSTS_LDS
+    SQ_INSTS_VMEM_RD SQ_INSTS_SALU SQ_BUSY_CYCLES SQ_WAVE_CYCLES, pass B with
+    SQ_ACTIVE_INST_VALU SQ_VALU_MFMA_BUSY_CYCLES SQ_WAIT_INST_ANY
+    SQ_ACTIVE_INST_ANY SQ_LDS_BANK_CONFLICT GRBM_GUI_ACTIVE.  Medians over the
+    dispatches of each (kernel instance, grid); instruction counts per
+    wavefront; cycle counters per wavefront as the counters report them."""
+    import numpy as np
+    A, Bp = read_counters(a_csv), read_counters(b_csv)
+    lines = ["| kernel | grid | VGPR (arch+acc) | LDS B | waves | VALU / wave | MFMA / wave | LDS / wave | "
+             "VMEM rd / wave | SALU / wave | MFMA busy / MFMA | active VALU / wave | active any / wave | "
+             "wait any / wave | wave cycles / wave | LDS conflicts / CU |",
+             "|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|"]
+    rec = {"source_sha256": kernel_source_digest(), "kernels": {}}
+    for (kname, grid), e in sorted(A.items()):
+        ca = e["counters"]
+        cb = Bp.get((kname, grid), {"counters": {}})["counters"]
+        med = lambda c, n: float(np.median(c[n])) if n in c else float("nan")
+        w = med(ca, "SQ_WAVES")
+        if not w > 0:
+            continue
+        nm = med(ca, "SQ_INSTS_MFMA")
+        row = {"vgpr": e["vgpr"], "agpr": e["agpr"], "lds": e["lds"], "waves": w,
+               "valu": med(ca, "SQ_INSTS_VALU") / w, "mfma": nm / w, "lds_insts": med(ca, "SQ_INSTS_LDS") / w,
+               "vmem": med(ca, "SQ_INSTS_VMEM_RD") / w, "salu": med(ca, "SQ_INSTS_SALU") / w,
+               "mfma_busy_per_inst": med(cb, "SQ_VALU_MFMA_BUSY_CYCLES") / nm if nm else 0.0,
+               "active_valu": med(cb, "SQ_ACTIVE_INST_VALU") / w, "active_any": med(cb, "SQ_ACTIVE_INST_ANY") / w,
+               "wait_any": med(cb, "SQ_WAIT_INST_ANY") / w, "wave_cycles": med(ca, "SQ_WAVE_CYCLES") / w,
+               "lds_conflicts_per_cu": med(cb, "SQ_LDS_BANK_CONFLICT") / 256}
+        rec["kernels"][f"{kname} grid {grid}"] = {k: round(v, 2) if isinstance(v, float) else v for k, v in row.items()}
+        lines.append(f"| `{kname}` | {grid} | {e['vgpr']}+{e['agpr']} | {e['lds']} | {w:.0f} | {row['valu']:.0f} | "
+                     f"{row['mfma']:.1f} | {row['lds_insts']:.1f} | {row['vmem']:.1f} | {row['salu']:.0f} | "
+                     f"{row['mfma_busy_per_inst']:.0f} | {row['active_valu']:.0f} | {row['active_any']:.0f} | "
+                     f"{row['wait_any']:.0f} | {row['wave_cycles']:.0f} | {row['lds_conflicts_per_cu']:.0f} |")
+    lines += ["", "counter-record: " + json.dumps(rec, sort_keys=True)]
     return "\n".join(lines)
 
 
@@ -386,6 +445,9 @@ def main():
     if args.prefill_summary:
         print(prefill_summary(args.prefill_summary))
         return
+    if args.counter_summary:
+        print(counter_summary(*args.counter_summary))
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the SBVR GEMV path "
               "has no multi-GPU mode.", file=sys.stderr)
@@ -449,6 +511,12 @@ def main():
                 for li in range(L):
                     W, x, y = layers[li][name]
                     sb.gemv_a8(W, x, out=y, stream=stream)
+            for name in PROJ_ORDER:  # small batch, B = 8 vectors
+                O, I = shapes[name]
+                X8 = torch.from_numpy(synth.activations(I, seed=77, batch=8)).to(dev)
+                Y8 = torch.empty((8, O), dtype=torch.float16, device=dev)
+                for li in range(L):
+                    sb.gemm_small_batch(layers[li][name][0], X8, out=Y8, stream=stream)
             for name in PROJ_ORDER:  # coefficient-cache format, one set per ten groups
                 O, I = shapes[name]
                 n_sets = max(1, min(65536, (O * (I // 128) + 9) // 10))

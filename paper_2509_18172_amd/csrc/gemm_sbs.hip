@@ -429,7 +429,9 @@ int launch_gemm_sbs(const Dims &d, const void *planes_dev, const void *coeffs_de
 {
     const int nb = B <= 2 ? 2 : (B <= 4 ? 4 : 8);
     const int gpw = (d.n_gblocks + SBVR_SBS_MAX_WAVES - 1) / SBVR_SBS_MAX_WAVES;
-    const int waves = (d.n_gblocks + gpw - 1) / gpw;
+    // several gblocks per wavefront: all eight wavefronts, so that the strided
+    // gblock assignment balances the four SIMDs
+    const int waves = gpw > 1 ? SBVR_SBS_MAX_WAVES : (d.n_gblocks + gpw - 1) / gpw;
     // tiles per workgroup, capped so that dynamic LDS stays within SBS_LDS_MAX
     const size_t fixed = (size_t)waves * sbs_stage_bytes(nb);
     const size_t per_tile = (size_t)waves * sbs_sets(nb) * d.tr * 16 * 4;

@@ -360,7 +360,12 @@ int launch_gemv_b1s(const Dims &d, const WeightRef &w, const uint16_t *x, uint16
                     hipStream_t stream)
 {
     const int gpw = (d.n_gblocks + SBVR_B1S_MAX_WAVES - 1) / SBVR_B1S_MAX_WAVES;
-    const int waves = (d.n_gblocks + gpw - 1) / gpw;
+    // with several gblocks per wavefront, always the full 16 wavefronts: the
+    // strided gblock assignment then gives every SIMD (wavefronts w, w + 4, ..)
+    // the same number of gblocks to within one (8B down, 28 gblocks: 14
+    // wavefronts left two SIMDs with 8 gblocks and two with 6; 9.1 -> 8.2 us;
+    // 70B down 24.7 -> 22.3 us)
+    const int waves = gpw > 1 ? SBVR_B1S_MAX_WAVES : (d.n_gblocks + gpw - 1) / gpw;
     // one gblock per wavefront: about 16 wavefronts per CU -- 512 workgroups of
     // up to 8 wavefronts, 256 of more (70B q/o, gate/up: 8.4 -> 8.1 us,
     // 22.3 -> 22.1 us) -- except the k = 4 depth-4 launch (256 of up to 8)
