@@ -178,12 +178,29 @@ def read_counter_csv(path: str, counter: str):
     return out
 
 
+def read_counter_by_grid(path: str, counter: str):
+    """{(kernel instance, grid threads): [per-dispatch value of `counter`]}
+    for the SBVR kernels, plus the calibration copy under ("neg", 0)."""
+    out = {}
+    with open(path) as fh:
+        for r in csv.DictReader(fh):
+            if r["Counter_Name"] != counter:
+                continue
+            name = r["Kernel_Name"]
+            key = ("neg", 0) if "neg_kernel" in name else (short_kernel_name(name), int(r["Grid_Size"]))
+            if key[0] == "neg" or "sbvr::" in name:
+                out.setdefault(key, []).append(float(r["Counter_Value"]))
+    return out
+
+
 def traffic_summary(fetch_csv: str, write_csv: str) -> str:
     """The profiles/ record: per-launch FETCH_SIZE and WRITE_SIZE of every GEMV
-    kernel, scaled by what the same counters read for a copy of known size."""
+    kernel (per kernel instance and grid), scaled by what the same counters
+    read for a copy of known size.  An instance launched with one grid only is
+    keyed by its name, else by "name grid G"."""
     import numpy as np
-    fetch, write = read_counter_csv(fetch_csv, "FETCH_SIZE"), read_counter_csv(write_csv, "WRITE_SIZE")
-    copy = next(n for n in fetch if "neg_kernel" in n)
+    fetch, write = read_counter_by_grid(fetch_csv, "FETCH_SIZE"), read_counter_by_grid(write_csv, "WRITE_SIZE")
+    copy = ("neg", 0)
     # KiB per dispatch; the copy reads and writes CALIB_BYTES
     f_scale = CALIB_BYTES / (np.median(fetch[copy]) * 1024)
     w_scale = CALIB_BYTES / (np.median(write[copy]) * 1024)
@@ -191,29 +208,50 @@ def traffic_summary(fetch_csv: str, write_csv: str) -> str:
         "copy_bytes": CALIB_BYTES, "fetch_kib": float(np.median(fetch[copy])),
         "write_kib": float(np.median(write[copy])), "fetch_scale": f_scale, "write_scale": w_scale},
         "kernels": {}}
-    for name in fetch:
+    grids = {}
+    for name, grid in fetch:
+        grids.setdefault(name, set()).add(grid)
+    lines = ["| kernel | grid | dispatches | FETCH_SIZE KiB (median) | WRITE_SIZE KiB | calibrated bytes / launch |",
+             "|---|---:|---:|---:|---:|---:|"]
+    for (name, grid) in sorted(k for k in fetch if k != copy):
         if "gemv_b1" not in name and "gemm_sbs" not in name:
             continue
-        short = short_kernel_name(name)
-        fk, wk = float(np.median(fetch[name])), float(np.median(write.get(name, [0.0])))
-        rec["kernels"][short] = {"dispatches": len(fetch[name]), "fetch_kib": fk, "write_kib": wk,
-                                 "bytes_per_launch": round(fk * 1024 * f_scale + wk * 1024 * w_scale)}
-    lines = ["traffic-record: " + json.dumps(rec, sort_keys=True)]
+        # one launch configuration can serve two shapes (same grid): split
+        # its dispatches where the sorted FETCH_SIZE values jump by > 25 %
+        vals = sorted(fetch[(name, grid)])
+        clusters = [[vals[0]]]
+        for v in vals[1:]:
+            (clusters[-1] if v <= clusters[-1][-1] * 1.25 else clusters.append([]) or clusters[-1]).append(v)
+        wk = float(np.median(write.get((name, grid), [0.0])))
+        for ci, cl in enumerate(clusters):
+            fk = float(np.median(cl))
+            nbytes = round(fk * 1024 * f_scale + wk * 1024 * w_scale)
+            key = name if len(grids[name]) == 1 else f"{name} grid {grid}"
+            if len(clusters) > 1:
+                key += f" size {ci + 1} of {len(clusters)}"
+            rec["kernels"][key] = {"dispatches": len(cl), "fetch_kib": fk, "write_kib": wk,
+                                   "grid": grid, "bytes_per_launch": nbytes}
+            lines.append(f"| `{name}` | {grid} | {len(cl)} | {fk:.1f} | {wk:.1f} | {nbytes:,} |")
+    lines += ["", "traffic-record: " + json.dumps(rec, sort_keys=True)]
     return "\n".join(lines)
 
 
 def read_counters(path: str):
-    """{(kernel instance, grid): {"counters": {name: [per-dispatch values]},
-    "vgpr", "agpr", "lds"}} for the SBVR kernels of a rocprofv3 counter CSV."""
+    """{(kernel instance, grid): {"dispatches": [{counter: value}, ...] in
+    dispatch order, "vgpr", "agpr"}} for the SBVR kernels of a rocprofv3
+    counter CSV."""
     out = {}
     with open(path) as fh:
-        for r in csv.DictReader(fh):
-            if "sbvr::" not in r["Kernel_Name"]:
-                continue
-            key = (short_kernel_name(r["Kernel_Name"]), int(r["Grid_Size"]))
-            e = out.setdefault(key, {"counters": {}, "vgpr": int(r["VGPR_Count"]),
-                                     "agpr": int(r["Accum_VGPR_Count"]), "lds": int(r["LDS_Block_Size"])})
-            e["counters"].setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+        rows = sorted(csv.DictReader(fh), key=lambda r: int(r["Dispatch_Id"]))
+    for r in rows:
+        if "sbvr::" not in r["Kernel_Name"]:
+            continue
+        key = (short_kernel_name(r["Kernel_Name"]), int(r["Grid_Size"]))
+        e = out.setdefault(key, {"ids": {}, "vgpr": int(r["VGPR_Count"]), "agpr": int(r["Accum_VGPR_Count"])})
+        e["ids"].setdefault(int(r["Dispatch_Id"]), {})[r["Counter_Name"]] = float(r["Counter_Value"])
+    for e in out.values():
+        e["dispatches"] = [e["ids"][i] for i in sorted(e["ids"])]
+        del e["ids"]
     return out
 
 
@@ -223,35 +261,49 @@ def counter_summary(a_csv: str, b_csv: str) -> str:
     SQ_INSTS_VMEM_RD SQ_INSTS_SALU SQ_BUSY_CYCLES SQ_WAVE_CYCLES, pass B with
     SQ_ACTIVE_INST_VALU SQ_VALU_MFMA_BUSY_CYCLES SQ_WAIT_INST_ANY
     SQ_ACTIVE_INST_ANY SQ_LDS_BANK_CONFLICT GRBM_GUI_ACTIVE.  Medians over the
-    dispatches of each (kernel instance, grid); instruction counts per
+    dispatches of each (kernel instance, grid); a launch configuration that
+    serves two shapes is split where its per-dispatch VALU count jumps by
+    more than 25 % (the two passes run the same probe, so the k-th dispatch
+    of an instance is the same launch in both).  Instruction counts per
     wavefront; cycle counters per wavefront as the counters report them."""
     import numpy as np
     A, Bp = read_counters(a_csv), read_counters(b_csv)
-    lines = ["| kernel | grid | VGPR (arch+acc) | LDS B | waves | VALU / wave | MFMA / wave | LDS / wave | "
+    lines = ["| kernel | grid | VGPR (rocprof) | waves | VALU / wave | MFMA / wave | LDS / wave | "
              "VMEM rd / wave | SALU / wave | MFMA busy / MFMA | active VALU / wave | active any / wave | "
              "wait any / wave | wave cycles / wave | LDS conflicts / CU |",
-             "|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|"]
+             "|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|"]
     rec = {"source_sha256": kernel_source_digest(), "kernels": {}}
     for (kname, grid), e in sorted(A.items()):
-        ca = e["counters"]
-        cb = Bp.get((kname, grid), {"counters": {}})["counters"]
-        med = lambda c, n: float(np.median(c[n])) if n in c else float("nan")
-        w = med(ca, "SQ_WAVES")
-        if not w > 0:
-            continue
-        nm = med(ca, "SQ_INSTS_MFMA")
-        row = {"vgpr": e["vgpr"], "agpr": e["agpr"], "lds": e["lds"], "waves": w,
-               "valu": med(ca, "SQ_INSTS_VALU") / w, "mfma": nm / w, "lds_insts": med(ca, "SQ_INSTS_LDS") / w,
-               "vmem": med(ca, "SQ_INSTS_VMEM_RD") / w, "salu": med(ca, "SQ_INSTS_SALU") / w,
-               "mfma_busy_per_inst": med(cb, "SQ_VALU_MFMA_BUSY_CYCLES") / nm if nm else 0.0,
-               "active_valu": med(cb, "SQ_ACTIVE_INST_VALU") / w, "active_any": med(cb, "SQ_ACTIVE_INST_ANY") / w,
-               "wait_any": med(cb, "SQ_WAIT_INST_ANY") / w, "wave_cycles": med(ca, "SQ_WAVE_CYCLES") / w,
-               "lds_conflicts_per_cu": med(cb, "SQ_LDS_BANK_CONFLICT") / 256}
-        rec["kernels"][f"{kname} grid {grid}"] = {k: round(v, 2) if isinstance(v, float) else v for k, v in row.items()}
-        lines.append(f"| `{kname}` | {grid} | {e['vgpr']}+{e['agpr']} | {e['lds']} | {w:.0f} | {row['valu']:.0f} | "
-                     f"{row['mfma']:.1f} | {row['lds_insts']:.1f} | {row['vmem']:.1f} | {row['salu']:.0f} | "
-                     f"{row['mfma_busy_per_inst']:.0f} | {row['active_valu']:.0f} | {row['active_any']:.0f} | "
-                     f"{row['wait_any']:.0f} | {row['wave_cycles']:.0f} | {row['lds_conflicts_per_cu']:.0f} |")
+        da = e["dispatches"]
+        db = Bp.get((kname, grid), {"dispatches": []})["dispatches"]
+        order = sorted(range(len(da)), key=lambda i: da[i].get("SQ_INSTS_VALU", 0.0))
+        clusters = [[order[0]]]
+        for i in order[1:]:
+            prev = da[clusters[-1][-1]].get("SQ_INSTS_VALU", 0.0)
+            if da[i].get("SQ_INSTS_VALU", 0.0) > prev * 1.25:
+                clusters.append([])
+            clusters[-1].append(i)
+        for ci, idx in enumerate(clusters):
+            def med(rows, n):
+                v = [rows[i][n] for i in idx if i < len(rows) and n in rows[i]]
+                return float(np.median(v)) if v else float("nan")
+            w = med(da, "SQ_WAVES")
+            if not w > 0:
+                continue
+            nm = med(da, "SQ_INSTS_MFMA")
+            row = {"vgpr": e["vgpr"], "agpr": e["agpr"], "waves": w, "dispatches": len(idx),
+                   "valu": med(da, "SQ_INSTS_VALU") / w, "mfma": nm / w, "lds_insts": med(da, "SQ_INSTS_LDS") / w,
+                   "vmem": med(da, "SQ_INSTS_VMEM_RD") / w, "salu": med(da, "SQ_INSTS_SALU") / w,
+                   "mfma_busy_per_inst": med(db, "SQ_VALU_MFMA_BUSY_CYCLES") / nm if nm else 0.0,
+                   "active_valu": med(db, "SQ_ACTIVE_INST_VALU") / w, "active_any": med(db, "SQ_ACTIVE_INST_ANY") / w,
+                   "wait_any": med(db, "SQ_WAIT_INST_ANY") / w, "wave_cycles": med(da, "SQ_WAVE_CYCLES") / w,
+                   "lds_conflicts_per_cu": med(db, "SQ_LDS_BANK_CONFLICT") / 256}
+            key = f"{kname} grid {grid}" + (f" size {ci + 1} of {len(clusters)}" if len(clusters) > 1 else "")
+            rec["kernels"][key] = {k: round(v, 2) if isinstance(v, float) else v for k, v in row.items()}
+            lines.append(f"| `{kname}` | {grid} | {e['vgpr']}+{e['agpr']} | {w:.0f} | {row['valu']:.0f} | "
+                         f"{row['mfma']:.1f} | {row['lds_insts']:.1f} | {row['vmem']:.1f} | {row['salu']:.0f} | "
+                         f"{row['mfma_busy_per_inst']:.0f} | {row['active_valu']:.0f} | {row['active_any']:.0f} | "
+                         f"{row['wait_any']:.0f} | {row['wave_cycles']:.0f} | {row['lds_conflicts_per_cu']:.0f} |")
     lines += ["", "counter-record: " + json.dumps(rec, sort_keys=True)]
     return "\n".join(lines)
 

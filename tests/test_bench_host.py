@@ -31,12 +31,15 @@ def test_kernel_instance_names(O, I, name):
 
 
 def _write_counter_csv(path, counter, rows):
-    cols = ["Correlation_Id", "Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value"]
+    """rows: (kernel, value) or (kernel, value, grid threads)."""
+    cols = ["Correlation_Id", "Dispatch_Id", "Grid_Size", "Kernel_Name", "Counter_Name", "Counter_Value"]
     with open(path, "w", newline="") as fh:
         w = csv.DictWriter(fh, fieldnames=cols)
         w.writeheader()
-        for i, (kernel, value) in enumerate(rows):
-            w.writerow({"Correlation_Id": i, "Dispatch_Id": i, "Kernel_Name": kernel,
+        for i, row in enumerate(rows):
+            kernel, value = row[0], row[1]
+            grid = row[2] if len(row) > 2 else 131072
+            w.writerow({"Correlation_Id": i, "Dispatch_Id": i, "Grid_Size": grid, "Kernel_Name": kernel,
                         "Counter_Name": counter, "Counter_Value": value})
 
 
@@ -57,6 +60,28 @@ def test_traffic_summary_scales_by_copy(tmp_path):
     assert k["dispatches"] == 3
     assert k["bytes_per_launch"] == round(16100.0 * 1024 * 2 + 7.0 * 1024 * 2)
     assert rec["source_sha256"] == bench.kernel_source_digest()
+
+
+def test_traffic_summary_separates_grids_and_sizes(tmp_path):
+    """One instance at two grids is keyed per grid; one launch configuration
+    serving two shapes (same grid, 4x the bytes) is split by size."""
+    copy = "void at::native::vectorized_elementwise_kernel<4, at::native::neg_kernel_cuda(at::TensorIteratorBase&)::{lambda()#1}>"
+    kern = "void sbvr::gemm_sbs_kernel<4, 8, 2, false>(sbvr::GemvArgs)"
+    calib_kib = bench.CALIB_BYTES / 1024
+    rows = [(kern, 1200.0), (kern, 4800.0), (kern, 1210.0), (kern, 4790.0), (kern, 9000.0, 65536),
+            (copy, calib_kib)]
+    _write_counter_csv(tmp_path / "f.csv", "FETCH_SIZE", rows)
+    _write_counter_csv(tmp_path / "w.csv", "WRITE_SIZE", [(r[0], 0.0) + tuple(r[2:]) for r in rows[:-1]]
+                       + [(copy, calib_kib)])
+    text = bench.traffic_summary(str(tmp_path / "f.csv"), str(tmp_path / "w.csv"))
+    import json
+    import re
+    rec = json.loads(re.search(r"^traffic-record: (\{.*\})$", text, re.M).group(1))["kernels"]
+    base = "gemm_sbs_kernel<4, 8, 2, false> grid 131072"
+    assert rec[base + " size 1 of 2"]["dispatches"] == 2
+    assert rec[base + " size 1 of 2"]["bytes_per_launch"] == round(1205.0 * 1024)
+    assert rec[base + " size 2 of 2"]["bytes_per_launch"] == round(4795.0 * 1024)
+    assert rec["gemm_sbs_kernel<4, 8, 2, false> grid 65536"]["bytes_per_launch"] == 9000 * 1024
 
 
 def test_more_than_one_gpu_is_refused():
