@@ -304,6 +304,34 @@ def test_ragged_shapes(sb, O, I, k):
     assert max(rel_err(Y[b], Y_ref[b]) for b in range(3)) <= TOL
 
 
+@pytest.mark.parametrize("O,I,k", [
+    # 18 gblocks per row (the last with 3 groups): the streaming kernel's 16
+    # wavefronts take 2 or 1 gblocks, the small-batch kernel's 8 take 3 or 2
+    (1000, 9088, 4),
+    # 17 gblocks: one wavefront takes 2, fifteen take 1 (most uneven)
+    (300, 8320, 2),
+    # 29 gblocks, the last holding one group, k = 3
+    (517, 14464, 3)])
+def test_long_rows_uneven_gblock_assignment(sb, O, I, k):
+    """Rows longer than 16 gblocks, whose gblock count does not divide over
+    the wavefronts: batch 1, W4A8 (k = 4) and small batch B = 2, 5, 8 against
+    the oracle, repeated calls bit-identical."""
+    planes, coeffs = synth.random_sbvr(O, I, k, seed=O * 7 + I + k)
+    W = packed(sb, planes, coeffs)
+    x = synth.activations(I, seed=O + 11)
+    y = run_gemv(sb, W, x)
+    assert rel_err(y, oracle.sbvr_gemv(planes, coeffs, x)) <= TOL
+    assert np.array_equal(y, run_gemv(sb, W, x))
+    if k == 4:
+        assert rel_err(run_gemv_a8(sb, W, x), oracle.sbvr_gemv_w4a8(planes, coeffs, x)) <= TOL
+    for B in (2, 5, 8):
+        X = synth.activations(I, seed=O + B, batch=B)
+        Y = run_gemm(sb, W, X)
+        Y_ref = oracle.sbvr_gemv(planes, coeffs, X)
+        assert max(rel_err(Y[b], Y_ref[b]) for b in range(B)) <= TOL, B
+        assert np.array_equal(Y, run_gemm(sb, W, X))
+
+
 def test_activation_dynamic_range(sb):
     O, I = 128, 2048
     planes, coeffs = synth.random_sbvr(O, I, 4, seed=90, coeff_sigma=1e-4)
