@@ -456,9 +456,10 @@ def test_output_canary_and_error_paths(sb):
 
 @pytest.mark.parametrize("O,I", [(4096, 4096), (14336, 4096)])
 def test_graph_capture_replays_match_eager(sb, O, I):
-    """Every GEMV-type entry point (one-shot and streaming kernels) and the
-    decompression and encoding kernels, captured in one graph: each replay
-    reproduces the eager results bit for bit."""
+    """Every GEMV-type entry point (one-shot and streaming kernels), the
+    decompression, the prefill GEMM (two launch shapes) and the encoding
+    kernels, captured in one graph: each replay reproduces the eager results
+    bit for bit."""
     planes, coeffs = synth.random_sbvr(O, I, 4, seed=123)
     W = packed(sb, planes, coeffs)
     n_sets = (O * (I // 128) + 9) // 10
@@ -467,6 +468,7 @@ def test_graph_capture_replays_match_eager(sb, O, I):
     x = dev(synth.activations(I, seed=124))
     X = dev(synth.activations(I, seed=125, batch=4))
     Wf = dev(synth.weights(64, I, 0.02, seed=127))
+    X16, X80 = dev(synth.activations(I, seed=128, batch=16)), dev(synth.activations(I, seed=129, batch=80))
     calls = {
         "gemv": lambda out=None: sb.gemv(W, x, out=out),
         "small_batch": lambda out=None: sb.gemm_small_batch(W, X, out=out),
@@ -475,6 +477,8 @@ def test_graph_capture_replays_match_eager(sb, O, I):
         "indexed_a8": lambda out=None: sb.gemv_indexed(Wi, x, out=out, a8=True),
         "decompress": lambda out=None: sb.decompress(W, out=out),
         "decompress_indexed": lambda out=None: sb.decompress(Wi, out=out),
+        "prefill_16": lambda out=None: sb.gemm_prefill(W, X16, out=out),
+        "prefill_80": lambda out=None: sb.gemm_prefill(W, X80, out=out),
     }
     eager = {n: f().clone() for n, f in calls.items()}
     ep, ec = sb.encode(Wf, 4)
