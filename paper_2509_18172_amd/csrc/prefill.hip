@@ -43,9 +43,9 @@ typedef _Float16 v8h __attribute__((ext_vector_type(8)));
 constexpr int PF_WAVES = 16;          // wavefronts per workgroup: R row tiles x S K-slices
 constexpr int PF_XROW = 256 + 16;     // LDS bytes per token row of an activation tile (padding
                                       // spreads the 16 rows of an operand read over all banks)
-#ifndef PF_LUT_PAD
-#define PF_LUT_PAD 2
-#endif
+// subset-sum table rows padded by two entries (consecutive rows start one
+// LDS bank apart; 0, 2 and 4 measured the same)
+constexpr int PF_LUT_PAD = 2;
 // activation chunks (16 bytes) per thread and group, at most: the launcher
 // keeps S BTT <= 4 pf_xpt(BTT) (a K-slice's 1024 / S threads load 256 BTT chunks)
 __host__ __device__ constexpr int pf_xpt(int btt) { return btt <= 2 ? 4 : 2; }
