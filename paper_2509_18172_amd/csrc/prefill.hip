@@ -175,22 +175,35 @@ __global__ void __launch_bounds__(64 * PF_WAVES) prefill_kernel(PrefillArgs a)
             constexpr int PER = NSUB >= 4 ? NSUB / 4 : NSUB;
             const int p0 = NSUB >= 4 ? PER * kq : 0;
             uint16_t *lrow = lut + n * LROW + p0;
-            if (emax - emin <= 11) {
-                // every subset sum has at most 24 significant bits: exact in
-                // binary32, one rounding to binary16
+            // binary32 path: every subset sum has at most 24 significant bits
+            // (exact whatever the order of the additions), one rounding to
+            // binary16.  The entry index is p0 + q: its bits above LOGPER come
+            // from the lane (p0), the ones below from q (compile time).
+            constexpr int LOGPER = PER == 4 ? 2 : (PER == 2 ? 1 : 0);
+            auto table32 = [&]() {
                 float cf[K];
 #pragma unroll
                 for (int i = 0; i < K; ++i)
                     cf[i] = half_bits_to_float(c[i]);
+                float hi = 0.f;
+#pragma unroll
+                for (int i = LOGPER; i < K; ++i)
+                    hi += ((p0 >> i) & 1) ? cf[i] : 0.f;
 #pragma unroll
                 for (int q = 0; q < PER; ++q) {
-                    const int p = p0 + q;
-                    float sum = 0.f;
+                    float sum = hi;
 #pragma unroll
-                    for (int i = 0; i < K; ++i)
-                        sum += ((p >> i) & 1) ? cf[i] : 0.f;
+                    for (int i = 0; i < LOGPER && i < K; ++i)
+                        if ((q >> i) & 1)
+                            sum += cf[i];
                     lrow[q] = __half_as_ushort(__float2half_rn(sum));
                 }
+            };
+            const bool wide = emax - emin > 11;
+            if (__builtin_amdgcn_ballot_w64(wide) == 0) {
+                table32();  // no lane of the wavefront needs binary64 (wavefront-uniform branch)
+            } else if (!wide) {
+                table32();
             } else {
 #pragma unroll
                 for (int q = 0; q < PER; ++q) {
