@@ -60,6 +60,33 @@ struct PrefillArgs {
     int S;                                    // K-slices per workgroup (a power of two)
 };
 
+// LDS address of a pointer into the workgroup's LDS
+__device__ __forceinline__ uint32_t lds_addr(const void *p)
+{
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p;
+}
+
+// base + byte B of v, one SDWA add (the compiler forms a shift, a mask and an
+// add for the same expression)
+template <int B>
+__device__ __forceinline__ uint32_t add_byte(uint32_t base, uint32_t v)
+{
+    uint32_t r;
+    if constexpr (B == 0)
+        asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_0"
+            : "=v"(r) : "v"(base), "v"(v));
+    else if constexpr (B == 1)
+        asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_1"
+            : "=v"(r) : "v"(base), "v"(v));
+    else if constexpr (B == 2)
+        asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_2"
+            : "=v"(r) : "v"(base), "v"(v));
+    else
+        asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_3"
+            : "=v"(r) : "v"(base), "v"(v));
+    return r;
+}
+
 __device__ __forceinline__ int f16_exp(uint32_t h)  // unbiased exponent, subnormals as -14
 {
     const int e = (int)((h >> 10) & 0x1f);
@@ -232,14 +259,17 @@ __global__ void __launch_bounds__(64 * PF_WAVES) prefill_kernel(PrefillArgs a)
                     const uint32_t word = ks == 0 ? sl.x : (ks == 1 ? sl.y : (ks == 2 ? sl.z : sl.w));
                     pat |= ((word >> kq) & 0x11111111u) << i;
                 }
-                if (!row_ok)
-                    pat = 0u;  // rows past the device format: entry 0 (zero)
-                uint4 bw;
-                bw.x = (uint32_t)L[pat & 0xf] | ((uint32_t)L[(pat >> 4) & 0xf] << 16);
-                bw.y = (uint32_t)L[(pat >> 8) & 0xf] | ((uint32_t)L[(pat >> 12) & 0xf] << 16);
-                bw.z = (uint32_t)L[(pat >> 16) & 0xf] | ((uint32_t)L[(pat >> 20) & 0xf] << 16);
-                bw.w = (uint32_t)L[(pat >> 24) & 0xf] | ((uint32_t)L[pat >> 28] << 16);
-                const v8h B = __builtin_bit_cast(v8h, bw);
+                // (rows past the device format have all-zero tables.)  Byte b
+                // of e2 / o2 is the byte offset of nibble 2b / 2b+1's entry,
+                // so each lookup's address is one byte-select add; the entries
+                // load straight into the halves of the operand registers.
+                const uint32_t e2 = (pat & 0x0F0F0F0Fu) << 1, o2 = (pat >> 3) & 0x1E1E1E1Eu;
+                const uint32_t Lbase = lds_addr(L);  // the row's table
+                const uint32_t a[8] = {add_byte<0>(Lbase, e2), add_byte<0>(Lbase, o2), add_byte<1>(Lbase, e2),
+                                       add_byte<1>(Lbase, o2), add_byte<2>(Lbase, e2), add_byte<2>(Lbase, o2),
+                                       add_byte<3>(Lbase, e2), add_byte<3>(Lbase, o2)};
+                auto at = [&](int i) { return *(const __attribute__((address_space(3))) _Float16 *)(uintptr_t)a[i]; };
+                const v8h B = {at(0), at(1), at(2), at(3), at(4), at(5), at(6), at(7)};
 #pragma unroll
                 for (int tt = 0; tt < BTT; ++tt) {
                     // token 16 tt + n, elements 32 ks + 8 kq .. +7
