@@ -13,6 +13,7 @@
 // 0..7), forms the subset index of each element, looks it up and writes 16
 // bytes.  HBM-bound: per weight it reads k/8 + 2k/128 bytes and writes 2.
 #include "device_ops.h"
+#include "lds_lookup.h"
 #include "f16_round.h"
 #include "launch.h"
 
@@ -128,10 +129,16 @@ __global__ void __launch_bounds__(1024) decompress_kernel(Dims d, const uint32_t
         for (int i = 0; i < K; ++i)
             sub |= ((w[u][i] >> v) & 0x11111111u) << i;
         const uint16_t *L = lut[u] + r * ROW_E + b * NSUB;
+        // byte h of e2 / o2: byte offset of nibble 2h / 2h+1's entry; one
+        // byte-select add per lookup address
+        const uint32_t e2 = (sub & 0x0F0F0F0Fu) << 1, o2 = (sub >> 3) & 0x1E1E1E1Eu, Lb = lds_addr(L);
+        const uint32_t a[8] = {add_byte<0>(Lb, e2), add_byte<0>(Lb, o2), add_byte<1>(Lb, e2), add_byte<1>(Lb, o2),
+                               add_byte<2>(Lb, e2), add_byte<2>(Lb, o2), add_byte<3>(Lb, e2), add_byte<3>(Lb, o2)};
+        auto at = [&](int i) { return (uint32_t)*(const __attribute__((address_space(3))) uint16_t *)(uintptr_t)a[i]; };
         v4u_t out;
 #pragma unroll
         for (int h = 0; h < 4; ++h)
-            out[h] = (uint32_t)L[(sub >> (8 * h)) & 0xf] | ((uint32_t)L[(sub >> (8 * h + 4)) & 0xf] << 16);
+            out[h] = at(2 * h) | (at(2 * h + 1) << 16);
         __builtin_nontemporal_store(out, (v4u_t *)(W + (size_t)o * d.I + (size_t)g * GROUP + wq * 32 + 8 * v));
     }
 }

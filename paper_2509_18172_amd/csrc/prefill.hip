@@ -33,6 +33,7 @@
 // it over 128 tokens, and past that the weights are decoded once per 128
 // tokens.
 #include "device_ops.h"
+#include "lds_lookup.h"
 #include "f16_round.h"
 #include "launch.h"
 
@@ -59,33 +60,6 @@ struct PrefillArgs {
     int O, I, T, n_tiles, n_gblocks, G, gps;  // gps: groups per K-slice
     int S;                                    // K-slices per workgroup (a power of two)
 };
-
-// LDS address of a pointer into the workgroup's LDS
-__device__ __forceinline__ uint32_t lds_addr(const void *p)
-{
-    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p;
-}
-
-// base + byte B of v, one SDWA add (the compiler forms a shift, a mask and an
-// add for the same expression)
-template <int B>
-__device__ __forceinline__ uint32_t add_byte(uint32_t base, uint32_t v)
-{
-    uint32_t r;
-    if constexpr (B == 0)
-        asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_0"
-            : "=v"(r) : "v"(base), "v"(v));
-    else if constexpr (B == 1)
-        asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_1"
-            : "=v"(r) : "v"(base), "v"(v));
-    else if constexpr (B == 2)
-        asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_2"
-            : "=v"(r) : "v"(base), "v"(v));
-    else
-        asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_3"
-            : "=v"(r) : "v"(base), "v"(v));
-    return r;
-}
 
 __device__ __forceinline__ int f16_exp(uint32_t h)  // unbiased exponent, subnormals as -14
 {
