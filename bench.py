@@ -25,6 +25,9 @@ One JSON line is printed:
   decode_step_w4a8  the same graph with SBVR-8 activations (sbvr_gemv_a8)
   decode_step_fused the same weights with q|k|v and gate|up packed as one
                 matrix each (rows concatenated), 4 GEMVs per layer
+  decode_step_grouped the 224 GEMVs on the separate weights, q, k, v and
+                gate, up each enqueued as one grouped launch
+                (sbvr_gemv_grouped): 4 launches per layer
   per_call_us   mean duration of each projection's launch, from HIP events
                 around a graph of 64 back-to-back launches of that shape
                 cycling through >= 1 GB of distinct weight copies (median
@@ -792,6 +795,30 @@ def main():
         del fused_graph, fused_layers
         torch.cuda.empty_cache()
 
+    # the same 224 GEMVs on the separate weights, the projections that share
+    # an input (q, k, v; gate, up) each enqueued as one grouped launch
+    # (sbvr_gemv_grouped): 4 launches per layer, no repacking
+    decode_step_grouped = None
+    if not args.quick:
+        def grouped_call(names, lay):
+            Ws, ys = [lay[n][0] for n in names], [lay[n][2] for n in names]
+            x = lay[names[0]][1]
+            return (lambda Ws, x, ys, stream: sb.gemv_grouped(Ws, [x] * len(Ws), outs=ys, stream=stream)), (Ws, x, ys)
+
+        grouped_calls = []
+        for li in range(L):
+            lay = layers[li]
+            grouped_calls += [grouped_call(("q", "k", "v"), lay), gemv_call(*lay["o"]),
+                              grouped_call(("gate", "up"), lay), gemv_call(*lay["down"])]
+        grouped_graph = capture(grouped_calls)
+        timed(grouped_graph.replay)
+        reps = [timed(grouped_graph.replay) * 1e3 for _ in range(DECODE_REPLAYS)]
+        us = float(np.median(reps))
+        decode_step_grouped = {"launches": len(grouped_calls), "gemvs": 7 * L, "us_per_token": round(us, 2),
+                               "mean_us_per_token": round(float(np.mean(reps)), 2),
+                               "gbps": round(layer_bytes * L / (us * 1e3), 1), "replays": len(reps)}
+        del grouped_graph
+
     # ---- per-launch durations: >= 64 back-to-back launches per graph, cycling
     # through distinct weight copies totalling >= ROTATE_BYTES ----
     def launch_us(calls, n_launch=64, replays=11):
@@ -1094,6 +1121,7 @@ def main():
         "per_call_events": per_call_events,
         "decode_step_w4a8": decode_step_a8,
         "decode_step_fused": decode_step_fused,
+        "decode_step_grouped": decode_step_grouped,
         "small_batch": small_batch or None,
         "w4a8": w4a8 or None,
         "indexed": indexed,

@@ -72,7 +72,8 @@ const char *sbvr_status_string(int status);
 
 /* Library ABI version (major * 100 + minor); 1.01 adds sbvr_decompress,
  * 1.02 sbvr_gemv_a8, 1.03 the coefficient-cache format entry points,
- * 1.04 sbvr_encode and sbvr_decompress_indexed, 1.05 sbvr_gemm_prefill. */
+ * 1.04 sbvr_encode and sbvr_decompress_indexed, 1.05 sbvr_gemm_prefill,
+ * 1.06 sbvr_gemv_grouped. */
 int sbvr_version(void);
 
 /*
@@ -154,6 +155,34 @@ int sbvr_gemm_small_batch(int O, int I, int k, const void *planes_dev, const voi
 int sbvr_gemv_a8(int O, int I, int k, const void *planes_dev, const void *coeffs_dev,
                  const uint16_t *x, uint16_t *y, void *workspace, size_t ws_bytes,
                  hipStream_t stream);
+
+/* Most GEMVs one sbvr_gemv_grouped call takes. */
+#define SBVR_GEMV_GROUP_MAX 4
+
+/*
+ * Grouped batch-1 GEMV: n independent GEMVs of Sec. 4.4 (each exactly the
+ * sbvr_gemv of its arguments, bit for bit) enqueued as ONE kernel launch, for
+ * the projections of a decode step that run back to back -- e.g. q, k and v,
+ * or gate and up, each with its own packed weights -- so that a captured
+ * decode step (the paper runs it under a CUDA graph, Sec. 5.2) pays one
+ * launch instead of n.
+ *   n                 1 <= n <= SBVR_GEMV_GROUP_MAX.
+ *   O                 host array [n]: out_features of member i.
+ *   I, k              shared by every member.
+ *   planes_dev, coeffs_dev, x, y
+ *                     host arrays [n] of device pointers, member i's
+ *                     device-format weights (sbvr_pack of O[i] x I, k),
+ *                     binary16 x[i] [I] (input) and y[i] [O[i]] (output,
+ *                     every element written).  Same alignment as sbvr_gemv.
+ *   workspace / ws_bytes  as sbvr_gemv (may be NULL / 0).
+ * The host arrays are read during the call only.  Members may share an x;
+ * no y may overlap another member's y or any x.  Every member is validated
+ * as sbvr_gemv would validate it before anything is enqueued; the first
+ * failing member's status is returned.
+ */
+int sbvr_gemv_grouped(int n, const int *O, int I, int k, const void *const *planes_dev,
+                      const void *const *coeffs_dev, const uint16_t *const *x, uint16_t *const *y,
+                      void *workspace, size_t ws_bytes, hipStream_t stream);
 
 /*
  * Prefill GEMM on SBVR weights (the prefill design of Sec. 5.1: the weights

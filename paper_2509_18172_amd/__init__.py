@@ -31,7 +31,7 @@ EXPORTED = (
     "sbvr_workspace_bytes", "sbvr_pack", "sbvr_unpack", "sbvr_gemv", "sbvr_gemm_small_batch",
     "sbvr_decompress", "sbvr_gemv_a8", "sbvr_packed_index_bytes", "sbvr_packed_table_bytes",
     "sbvr_pack_indexed", "sbvr_unpack_indexed", "sbvr_gemv_indexed", "sbvr_gemv_indexed_a8", "sbvr_encode",
-    "sbvr_decompress_indexed", "sbvr_gemm_prefill",
+    "sbvr_decompress_indexed", "sbvr_gemm_prefill", "sbvr_gemv_grouped",
 )
 
 
@@ -77,6 +77,7 @@ def _load():
         "sbvr_encode": (i32, [i32, i32, i32, vp, i32, i32, i32, i32, i32, vp, vp, vp, vp]),
         "sbvr_decompress_indexed": (i32, [i32, i32, i32, i32, vp, vp, vp, vp, vp]),
         "sbvr_gemm_prefill": (i32, [i32, i32, i32, vp, vp, vp, vp, i32, vp]),
+        "sbvr_gemv_grouped": (i32, [i32, vp, i32, i32, vp, vp, vp, vp, vp, sz, vp]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -132,6 +133,21 @@ def sbvr_gemm_small_batch(O, I, k, planes_dev, coeffs_dev, X, Y, B, workspace=No
 
 def sbvr_gemv_a8(O, I, k, planes_dev, coeffs_dev, x, y, workspace=None, ws_bytes=0, stream=0) -> int:
     return _lib.sbvr_gemv_a8(O, I, k, planes_dev, coeffs_dev, x, y, workspace, ws_bytes, stream)
+
+
+GEMV_GROUP_MAX = 4
+
+
+def sbvr_gemv_grouped(n, O, I, k, planes_dev, coeffs_dev, x, y, workspace=None, ws_bytes=0, stream=0) -> int:
+    """O, planes_dev, coeffs_dev, x, y: sequences of n ints (out_features and
+    device pointers), marshalled into the host arrays the C call reads."""
+    seq = (O, planes_dev, coeffs_dev, x, y)
+    if any(len(v) < n for v in seq):
+        return SBVR_E_INVALID_ARG
+    m = max(n, 1)
+    arr_O = (C.c_int * m)(*[int(v) for v in list(O)[:n]])
+    ptrs = [(C.c_void_p * m)(*[int(p) for p in list(v)[:n]]) for v in seq[1:]]
+    return _lib.sbvr_gemv_grouped(n, arr_O, I, k, *ptrs, workspace, ws_bytes, stream)
 
 
 def sbvr_packed_index_bytes(O: int, I: int, k: int) -> int:
@@ -279,6 +295,22 @@ def gemv(W: PackedWeight, x, out=None, stream=None):
     _check(sbvr_gemv(W.O, W.I, W.k, W.planes.data_ptr(), W.coeffs.data_ptr(), x.data_ptr(),
                      y.data_ptr(), None, 0, _stream(stream)), "sbvr_gemv")
     return y
+
+
+def gemv_grouped(Ws, xs, outs=None, stream=None):
+    """y_i = SBVR(W_i) x_i for up to GEMV_GROUP_MAX matrices with the same I
+    and k, as one kernel launch; returns the list of fp16 [O_i] outputs."""
+    Ws, xs = list(Ws), list(xs)
+    assert 1 <= len(Ws) <= GEMV_GROUP_MAX and len(xs) == len(Ws)
+    I, k = Ws[0].I, Ws[0].k
+    assert all(W.I == I and W.k == k for W in Ws), "members must share I and k"
+    for W, x in zip(Ws, xs):
+        _check_input(W, x, (W.I,))
+    ys = [_out(None if outs is None else outs[i], (W.O,), xs[i]) for i, W in enumerate(Ws)]
+    _check(sbvr_gemv_grouped(len(Ws), [W.O for W in Ws], I, k, [W.planes.data_ptr() for W in Ws],
+                             [W.coeffs.data_ptr() for W in Ws], [x.data_ptr() for x in xs],
+                             [y.data_ptr() for y in ys], None, 0, _stream(stream)), "sbvr_gemv_grouped")
+    return ys
 
 
 def gemm_small_batch(W: PackedWeight, X, out=None, stream=None):

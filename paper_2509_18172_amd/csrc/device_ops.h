@@ -465,4 +465,39 @@ struct GemvArgs {
     int n_sets;
 };
 
+// Grouped launch: several GEMVs with the same inner dimension and plane count
+// (each with its own weights, activations and output) in one dispatch.
+// Member m owns the workgroups [wg0[m], wg0[m + 1]); entries past the last
+// member hold wg0 = INT_MAX.
+constexpr int GROUP_MAX = 4;
+struct GemvGroup {
+    const uint4 *planes[GROUP_MAX];
+    const uint16_t *coeffs[GROUP_MAX];
+    const uint16_t *x[GROUP_MAX];
+    uint16_t *y[GROUP_MAX];
+    int O[GROUP_MAX];
+    int n_tiles[GROUP_MAX];
+    int wg0[GROUP_MAX];
+};
+
+template <class T>
+__device__ __forceinline__ T group_pick(const T (&v)[GROUP_MAX], int m)
+{
+    return m == 0 ? v[0] : (m == 1 ? v[1] : (m == 2 ? v[2] : v[3]));
+}
+
+// Binds `a` to the member that owns workgroup `bid` of a grouped launch and
+// returns the workgroup's index within that member (all wavefront-uniform).
+__device__ __forceinline__ int bind_group_member(const GemvGroup &g, GemvArgs &a, int bid)
+{
+    const int m = (bid >= g.wg0[1]) + (bid >= g.wg0[2]) + (bid >= g.wg0[3]);
+    a.planes = group_pick(g.planes, m);
+    a.coeffs = group_pick(g.coeffs, m);
+    a.x = group_pick(g.x, m);
+    a.y = group_pick(g.y, m);
+    a.O = group_pick(g.O, m);
+    a.n_tiles = group_pick(g.n_tiles, m);
+    return bid - group_pick(g.wg0, m);
+}
+
 }  // namespace sbvr

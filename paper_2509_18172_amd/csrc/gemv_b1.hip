@@ -24,6 +24,8 @@
 // arithmetic, and scheduling barriers keep the compiler from sinking weight
 // loads below the activation work (left alone it does, to save registers,
 // which serialises DRAM latency behind arithmetic).
+#include <climits>
+
 #include "device_ops.h"
 #include "launch.h"
 
@@ -51,21 +53,10 @@ struct B1Regs {
 // neither the first loads nor the LDS waits before the matrix-core work sit
 // behind a kernel-argument fetch (a scalar load shares the LDS wait counter);
 // the rest are read from the struct.  The wavefront count is the gblock count.
+// The kernel body for workgroup `bid` of the matrix in `a`.
 template <int K, int T, bool A8, bool IX>
-__global__ void __launch_bounds__(1024) gemv_b1_kernel(const uint4 *planes_, const uint16_t *coeffs_,
-                                                       const uint16_t *x_, int I_, int n_tiles_, int n_gblocks_,
-                                                       uint16_t *y_, int O_, GemvArgs a_rest)
+__device__ __forceinline__ void gemv_b1_body(const GemvArgs &a, unsigned bid)
 {
-    GemvArgs a = a_rest;
-    a.planes = planes_;
-    a.coeffs = coeffs_;
-    a.x = x_;
-    a.I = I_;
-    a.n_tiles = n_tiles_;
-    a.n_gblocks = n_gblocks_;
-    a.y = y_;
-    a.O = O_;
-
     extern __shared__ __align__(16) unsigned char smem[];
     const int lane = threadIdx.x & 63;
     const int wv = wave_id();
@@ -73,7 +64,7 @@ __global__ void __launch_bounds__(1024) gemv_b1_kernel(const uint4 *planes_, con
     unsigned char *lds = smem + wv * B1_WAVE_LDS;
     float *red = (float *)(smem + nw * B1_WAVE_LDS);
 
-    const int tile0 = blockIdx.x * T;
+    const int tile0 = bid * T;
     const int gb = wv;
 
     constexpr int TR = tile_rows(K), NP = partials_per_lane<K>();
@@ -251,6 +242,33 @@ __global__ void __launch_bounds__(1024) gemv_b1_kernel(const uint4 *planes_, con
     }
 }
 
+template <int K, int T, bool A8, bool IX>
+__global__ void __launch_bounds__(1024) gemv_b1_kernel(const uint4 *planes_, const uint16_t *coeffs_,
+                                                       const uint16_t *x_, int I_, int n_tiles_, int n_gblocks_,
+                                                       uint16_t *y_, int O_, GemvArgs a_rest)
+{
+    GemvArgs a = a_rest;
+    a.planes = planes_;
+    a.coeffs = coeffs_;
+    a.x = x_;
+    a.I = I_;
+    a.n_tiles = n_tiles_;
+    a.n_gblocks = n_gblocks_;
+    a.y = y_;
+    a.O = O_;
+    gemv_b1_body<K, T, A8, IX>(a, blockIdx.x);
+}
+
+// Grouped launch (binary16 activations, per-group coefficients): the
+// workgroups of every member in one grid, each bound to its member's matrix.
+template <int K, int T>
+__global__ void __launch_bounds__(1024) gemv_b1_group_kernel(GemvArgs a_rest, GemvGroup g)
+{
+    GemvArgs a = a_rest;
+    const unsigned bid = (unsigned)bind_group_member(g, a, (int)blockIdx.x);
+    gemv_b1_body<K, T, false, false>(a, bid);
+}
+
 // Launch shape.  T tiles (T * TR rows) per workgroup: the most (<= 8) that still
 // leaves >= 256 workgroups for 256 CUs and >= 2048 wavefronts in all; one
 // wavefront per gblock.  (Measured T = 1 / 2 / 4 / 8: 4096 x 4096 4.30 / 4.01 /
@@ -314,6 +332,63 @@ int launch_gemv_b1(const Dims &d, const WeightRef &w, const uint16_t *x, uint16_
                      : d.k == 2 ? b1_kernel_for<2>(T, a8, ix)
                                 : b1_kernel_for<1>(T, a8, ix);
     void *args[] = {&a.planes, &a.coeffs, &a.x, &a.I, &a.n_tiles, &a.n_gblocks, &a.y, &a.O, &a};
+    return launch_kernel(fn, dim3(grid), dim3(64 * waves), lds, stream, args);
+}
+
+// the C ABI's bound, and the three comparisons of bind_group_member
+static_assert(GROUP_MAX == SBVR_GEMV_GROUP_MAX && GROUP_MAX == 4, "group table size");
+
+int fill_group(GemvGroup &g, int n, const GemvMember *mem, const Dims &d, int tiles_per_group)
+{
+    int wg = 0;
+    for (int i = 0; i < GROUP_MAX; ++i) {
+        const GemvMember &m = mem[i < n ? i : 0];
+        g.planes[i] = (const uint4 *)m.planes;
+        g.coeffs[i] = (const uint16_t *)m.coeffs;
+        g.x[i] = m.x;
+        g.y[i] = m.y;
+        g.O[i] = m.O;
+        g.n_tiles[i] = make_dims(m.O, d.I, d.k).n_tiles;
+        g.wg0[i] = i < n ? wg : INT_MAX;
+        if (i < n)
+            wg += (g.n_tiles[i] + tiles_per_group - 1) / tiles_per_group;
+    }
+    return wg;
+}
+
+template <int K>
+static const void *b1_group_kernel_for(int T)
+{
+    switch (T) {
+    case 8: return (const void *)gemv_b1_group_kernel<K, 8>;
+    case 4: return (const void *)gemv_b1_group_kernel<K, 4>;
+    case 2: return (const void *)gemv_b1_group_kernel<K, 2>;
+    default: return (const void *)gemv_b1_group_kernel<K, 1>;
+    }
+}
+
+int launch_gemv_group(int n, const GemvMember *mem, int I, int k, hipStream_t stream)
+{
+    // the combined shape (every member's row tiles) selects kernel and shape
+    Dims d = make_dims(mem[0].O, I, k);
+    int tiles = 0;
+    for (int i = 0; i < n; ++i)
+        tiles += make_dims(mem[i].O, I, k).n_tiles;
+    d.n_tiles = tiles;
+    d.O = tiles * d.tr;
+    if (d.n_gblocks > B1_MAX_WAVES || (long)d.n_tiles * d.n_gblocks >= SBVR_B1S_MIN_BLOCKS)
+        return launch_gemv_b1s_group(d, n, mem, stream);
+    const int T = choose_b1_tiles(d);
+    const int waves = d.n_gblocks;
+    GemvGroup g;
+    const int grid = fill_group(g, n, mem, d, T);
+    GemvArgs a = {nullptr, nullptr, nullptr, nullptr, 0, d.I, d.k, 0, d.n_gblocks, 1, 1, 0, nullptr, nullptr, 0};
+    const size_t lds = (size_t)waves * B1_WAVE_LDS + (size_t)waves * T * d.tr * 4;
+    const void *fn = d.k == 4   ? b1_group_kernel_for<4>(T)
+                     : d.k == 3 ? b1_group_kernel_for<3>(T)
+                     : d.k == 2 ? b1_group_kernel_for<2>(T)
+                                : b1_group_kernel_for<1>(T);
+    void *args[] = {&a, &g};
     return launch_kernel(fn, dim3(grid), dim3(64 * waves), lds, stream, args);
 }
 

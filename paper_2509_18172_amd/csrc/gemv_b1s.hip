@@ -90,31 +90,18 @@ constexpr int B1S_WAVE_LDS = 2048 + 256;
 // -amdgpu-kernarg-preload-count), so neither the first loads nor the LDS
 // waits before the matrix-core work sit behind a kernel-argument fetch (a
 // scalar load shares the LDS wait counter); the rest are read from the struct.
+// The kernel body for workgroup `bid` (of nw wavefronts) of the matrix in `a`.
 template <int K, int D, bool MULTI, bool A8, bool IX>
-__global__ void __launch_bounds__(1024) gemv_b1s_kernel(const uint4 *planes_, const uint16_t *coeffs_,
-                                                        const uint16_t *x_, int I_, int n_tiles_, int n_gblocks_, int tpw_,
-                                                        uint16_t *y_, int O_, int nw_, GemvArgs a_rest)
+__device__ __forceinline__ void gemv_b1s_body(const GemvArgs &a, int nw, unsigned bid)
 {
-    GemvArgs a = a_rest;
-    a.planes = planes_;
-    a.coeffs = coeffs_;
-    a.x = x_;
-    a.I = I_;
-    a.n_tiles = n_tiles_;
-    a.n_gblocks = n_gblocks_;
-    a.tpw = tpw_;
-    a.y = y_;
-    a.O = O_;
-
     extern __shared__ __align__(16) unsigned char smem[];
     const int lane = threadIdx.x & 63;
     const int wv = wave_id();
-    const int nw = nw_;  // wavefronts in the workgroup
     unsigned char *lds = smem + wv * B1S_WAVE_LDS;
     constexpr int TR = tile_rows(K), NP = partials_per_lane<K>();
     float *red = (float *)(smem + nw * B1S_WAVE_LDS);  // [tpw][nw][TR]
 
-    const int tile0 = blockIdx.x * a.tpw;
+    const int tile0 = bid * a.tpw;
     const int ntl = min(a.tpw, a.n_tiles - tile0);
     // MULTI: several gblocks per wavefront; otherwise exactly one (wv)
     const int n_items = MULTI ? ((a.n_gblocks - wv + nw - 1) / nw) * ntl : ntl;
@@ -333,6 +320,34 @@ __global__ void __launch_bounds__(1024) gemv_b1s_kernel(const uint4 *planes_, co
     }
 }
 
+template <int K, int D, bool MULTI, bool A8, bool IX>
+__global__ void __launch_bounds__(1024) gemv_b1s_kernel(const uint4 *planes_, const uint16_t *coeffs_,
+                                                        const uint16_t *x_, int I_, int n_tiles_, int n_gblocks_, int tpw_,
+                                                        uint16_t *y_, int O_, int nw_, GemvArgs a_rest)
+{
+    GemvArgs a = a_rest;
+    a.planes = planes_;
+    a.coeffs = coeffs_;
+    a.x = x_;
+    a.I = I_;
+    a.n_tiles = n_tiles_;
+    a.n_gblocks = n_gblocks_;
+    a.tpw = tpw_;
+    a.y = y_;
+    a.O = O_;
+    gemv_b1s_body<K, D, MULTI, A8, IX>(a, nw_, blockIdx.x);
+}
+
+// Grouped launch (binary16 activations, per-group coefficients): the
+// workgroups of every member in one grid, each bound to its member's matrix.
+template <int K, int D, bool MULTI>
+__global__ void __launch_bounds__(1024) gemv_b1s_group_kernel(int nw_, GemvArgs a_rest, GemvGroup g)
+{
+    GemvArgs a = a_rest;
+    const unsigned bid = (unsigned)bind_group_member(g, a, (int)blockIdx.x);
+    gemv_b1s_body<K, D, MULTI, false, false>(a, nw_, bid);
+}
+
 template <int K, bool A8, bool IX>
 static const void *b1s_kernel_for(bool multi, bool short_run, bool wide)
 {
@@ -356,44 +371,88 @@ static const void *b1s_kernel_for(bool multi, bool short_run, bool wide, bool a8
               : b1s_kernel_for<K, false, false>(multi, short_run, wide);
 }
 
-int launch_gemv_b1s(const Dims &d, const WeightRef &w, const uint16_t *x, uint16_t *y, bool a8,
-                    hipStream_t stream)
+// Launch shape of the streaming kernel for the (combined) shape d.
+struct B1sShape {
+    int waves, tpw, gpw;
+    bool multi, short_run, wide;
+    size_t lds;
+};
+
+static B1sShape b1s_shape(const Dims &d, bool ix)
 {
-    const int gpw = (d.n_gblocks + SBVR_B1S_MAX_WAVES - 1) / SBVR_B1S_MAX_WAVES;
+    B1sShape sh;
+    sh.gpw = (d.n_gblocks + SBVR_B1S_MAX_WAVES - 1) / SBVR_B1S_MAX_WAVES;
     // with several gblocks per wavefront, always the full 16 wavefronts: the
     // strided gblock assignment then gives every SIMD (wavefronts w, w + 4, ..)
     // the same number of gblocks to within one (8B down, 28 gblocks: 14
     // wavefronts left two SIMDs with 8 gblocks and two with 6; 9.1 -> 8.2 us;
     // 70B down 24.7 -> 22.3 us)
-    const int waves = gpw > 1 ? SBVR_B1S_MAX_WAVES : (d.n_gblocks + gpw - 1) / gpw;
+    sh.waves = sh.gpw > 1 ? SBVR_B1S_MAX_WAVES : (d.n_gblocks + sh.gpw - 1) / sh.gpw;
     // one gblock per wavefront: about 16 wavefronts per CU -- 512 workgroups of
     // up to 8 wavefronts, 256 of more (70B q/o, gate/up: 8.4 -> 8.1 us,
     // 22.3 -> 22.1 us) -- except the k = 4 depth-4 launch (256 of up to 8)
-    const bool ix = w.index != nullptr;
-    const bool wide = d.k == 4 && gpw == 1 && waves <= 8 && !ix;
-    const int groups = gpw > 1 ? SBVR_B1S_GROUPS_MULTI
-                       : wide  ? SBVR_B1S_GROUPS_WIDE
-                               : (waves > 8 ? SBVR_B1S_GROUPS / 2 : SBVR_B1S_GROUPS);
+    sh.wide = d.k == 4 && sh.gpw == 1 && sh.waves <= 8 && !ix;
+    const int groups = sh.gpw > 1 ? SBVR_B1S_GROUPS_MULTI
+                       : sh.wide  ? SBVR_B1S_GROUPS_WIDE
+                                  : (sh.waves > 8 ? SBVR_B1S_GROUPS / 2 : SBVR_B1S_GROUPS);
     // tiles per workgroup, capped so that the dynamic LDS (operand staging
     // plus the [tile][wavefront][row] sums) stays within SBVR_MAX_DYN_LDS:
     // very tall matrices get more workgroups instead
-    const size_t per_tile = (size_t)waves * d.tr * 4;
-    const int max_tpw = (int)((SBVR_MAX_DYN_LDS - (size_t)waves * B1S_WAVE_LDS) / per_tile);
-    const int tpw = min((d.n_tiles + groups - 1) / groups, max_tpw);
-    const int grid = (d.n_tiles + tpw - 1) / tpw;
+    const size_t per_tile = (size_t)sh.waves * d.tr * 4;
+    const int max_tpw = (int)((SBVR_MAX_DYN_LDS - (size_t)sh.waves * B1S_WAVE_LDS) / per_tile);
+    sh.tpw = min((d.n_tiles + groups - 1) / groups, max_tpw);
+    sh.lds = (size_t)sh.waves * B1S_WAVE_LDS + (size_t)sh.tpw * per_tile;
+    sh.multi = sh.gpw > 1;
+    sh.short_run = sh.tpw < SBVR_B1S_SHORT_TPW;
+    return sh;
+}
+
+int launch_gemv_b1s(const Dims &d, const WeightRef &w, const uint16_t *x, uint16_t *y, bool a8,
+                    hipStream_t stream)
+{
+    const bool ix = w.index != nullptr;
+    const B1sShape sh = b1s_shape(d, ix);
+    const int grid = (d.n_tiles + sh.tpw - 1) / sh.tpw;
     GemvArgs a = {(const uint4 *)w.planes, (const uint16_t *)w.coeffs, x, y, d.O, d.I, d.k,
-                  d.n_tiles, d.n_gblocks, gpw, 1, tpw, (const uint16_t *)w.index, (const uint16_t *)w.table,
+                  d.n_tiles, d.n_gblocks, sh.gpw, 1, sh.tpw, (const uint16_t *)w.index, (const uint16_t *)w.table,
                   w.n_sets};
-    const size_t lds = (size_t)waves * B1S_WAVE_LDS + (size_t)tpw * per_tile;
-    const bool multi = gpw > 1;
-    const bool short_run = tpw < SBVR_B1S_SHORT_TPW;
-    const void *fn = d.k == 4   ? b1s_kernel_for<4>(multi, short_run, wide, a8, ix)
-                     : d.k == 3 ? b1s_kernel_for<3>(multi, short_run, wide, a8, ix)
-                     : d.k == 2 ? b1s_kernel_for<2>(multi, short_run, wide, a8, ix)
-                                : b1s_kernel_for<1>(multi, short_run, wide, a8, ix);
-    int nw = waves;
+    const void *fn = d.k == 4   ? b1s_kernel_for<4>(sh.multi, sh.short_run, sh.wide, a8, ix)
+                     : d.k == 3 ? b1s_kernel_for<3>(sh.multi, sh.short_run, sh.wide, a8, ix)
+                     : d.k == 2 ? b1s_kernel_for<2>(sh.multi, sh.short_run, sh.wide, a8, ix)
+                                : b1s_kernel_for<1>(sh.multi, sh.short_run, sh.wide, a8, ix);
+    int nw = sh.waves;
     void *args[] = {&a.planes, &a.coeffs, &a.x, &a.I, &a.n_tiles, &a.n_gblocks, &a.tpw, &a.y, &a.O, &nw, &a};
-    return launch_kernel(fn, dim3(grid), dim3(64 * waves), lds, stream, args);
+    return launch_kernel(fn, dim3(grid), dim3(64 * sh.waves), sh.lds, stream, args);
+}
+
+// the same instance choice as b1s_kernel_for, for the grouped kernel
+template <int K>
+static const void *b1s_group_kernel_for(bool multi, bool short_run, bool wide)
+{
+    if constexpr (K == 4) {
+        if (wide)
+            return (const void *)gemv_b1s_group_kernel<K, SBVR_B1S_DEPTH_WIDE, false>;
+    }
+    if (!multi)
+        return (const void *)gemv_b1s_group_kernel<K, SBVR_B1S_DEPTH, false>;
+    return short_run ? (const void *)gemv_b1s_group_kernel<K, 2, true>
+                     : (const void *)gemv_b1s_group_kernel<K, SBVR_B1S_DEPTH_MULTI, true>;
+}
+
+int launch_gemv_b1s_group(const Dims &d, int n, const GemvMember *mem, hipStream_t stream)
+{
+    const B1sShape sh = b1s_shape(d, false);
+    GemvGroup g;
+    const int grid = fill_group(g, n, mem, d, sh.tpw);
+    GemvArgs a = {nullptr, nullptr, nullptr, nullptr, 0, d.I, d.k, 0, d.n_gblocks, sh.gpw, 1, sh.tpw,
+                  nullptr, nullptr, 0};
+    const void *fn = d.k == 4   ? b1s_group_kernel_for<4>(sh.multi, sh.short_run, sh.wide)
+                     : d.k == 3 ? b1s_group_kernel_for<3>(sh.multi, sh.short_run, sh.wide)
+                     : d.k == 2 ? b1s_group_kernel_for<2>(sh.multi, sh.short_run, sh.wide)
+                                : b1s_group_kernel_for<1>(sh.multi, sh.short_run, sh.wide);
+    int nw = sh.waves;
+    void *args[] = {&nw, &a, &g};
+    return launch_kernel(fn, dim3(grid), dim3(64 * sh.waves), sh.lds, stream, args);
 }
 
 }  // namespace sbvr

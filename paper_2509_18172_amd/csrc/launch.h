@@ -59,4 +59,23 @@ int launch_prefill(const Dims &d, const void *planes_dev, const void *coeffs_dev
 int launch_gemm_sbs(const Dims &d, const void *planes_dev, const void *coeffs_dev,
                     const uint16_t *X, uint16_t *Y, int B, hipStream_t stream);
 
+// Grouped batch-1 GEMV: n (<= GROUP_MAX) matrices with the same I and k, each
+// with its own weights (per-group coefficients), binary16 activations and
+// output, in one launch.  The launch shape is the one a single matrix with
+// all the members' row tiles would get; every member's row tiles start a new
+// workgroup.
+struct GemvMember {
+    int O;
+    const void *planes;
+    const void *coeffs;
+    const uint16_t *x;
+    uint16_t *y;
+};
+struct GemvGroup;
+// Fills the member table for workgroups of `tiles_per_group` row tiles and
+// returns the grid size.
+int fill_group(GemvGroup &g, int n, const GemvMember *mem, const Dims &d, int tiles_per_group);
+int launch_gemv_group(int n, const GemvMember *mem, int I, int k, hipStream_t stream);
+int launch_gemv_b1s_group(const Dims &d, int n, const GemvMember *mem, hipStream_t stream);
+
 }  // namespace sbvr
