@@ -17,10 +17,10 @@
 // the four groups, i.e. the A operands of the four instructions of an item.
 //
 // Each lane applies the coefficients of its four D rows (the planes of 1, 2 or
-// 4 tile rows) for every group, the four limb columns of a vector are summed
-// by a quad reduction, and one lane per (row, vector) adds the item's sum to
-// LDS; the workgroup sums the wavefronts in order at the end (deterministic,
-// no global workspace).
+// 4 tile rows) for every group as one chain of fused multiply-adds and adds
+// the item's (row, vector, limb) partial to LDS; at the end the workgroup sums,
+// per output, the wavefronts in order and the four limb columns of its
+// vector (deterministic, no global workspace).
 #include "device_ops.h"
 #include "launch.h"
 
@@ -37,6 +37,15 @@ namespace sbvr {
 #endif
 #ifndef SBVR_SBS_LONG_TPW
 #define SBVR_SBS_LONG_TPW 12
+#endif
+// Ring depth when a wavefront takes several gblocks (long rows) at B <= 4:
+// its item stream crosses gblocks, and the deeper ring keeps the next
+// gblock's first items in flight while its operand is built (measured at
+// B = 4: 8B down 14.0 -> 13.0 us, 70B down 40.3 -> 36.4, 70B gate/up 31.5 ->
+// 30.3; B = 2: 11.3 -> 10.9, 34.0 -> 31.6, 29.5 -> 28.7; no gain at B = 8,
+// where the VALU work per item bounds the kernel).
+#ifndef SBVR_SBS_DEPTH_MULTI_SMALL
+#define SBVR_SBS_DEPTH_MULTI_SMALL 4
 #endif
 #ifndef SBVR_SBS_MAX_WAVES
 #define SBVR_SBS_MAX_WAVES 8
@@ -420,6 +429,9 @@ static const void *sbs_kernel_kd(int nb, bool multi)
 template <int K>
 static const void *sbs_kernel_k(int nb, bool multi, bool long_ring)
 {
+    if (multi && nb <= 4)
+        return nb == 2 ? (const void *)gemm_sbs_kernel<K, 2, SBVR_SBS_DEPTH_MULTI_SMALL, true>
+                       : (const void *)gemm_sbs_kernel<K, 4, SBVR_SBS_DEPTH_MULTI_SMALL, true>;
     return long_ring ? sbs_kernel_kd<K, SBVR_SBS_DEPTH_LONG>(nb, multi)
                      : sbs_kernel_kd<K, SBVR_SBS_DEPTH_SHORT>(nb, multi);
 }

@@ -159,12 +159,13 @@ def test_small_batch_full_size(sb, O, I, B):
     assert rel_err(Y[0], y0.astype(np.float64)) <= TOL
 
 
-@pytest.mark.parametrize("B", [2, 8])
+@pytest.mark.parametrize("B", [2, 3, 4, 8])
 @pytest.mark.parametrize("O,I", SHAPES_70B)
 def test_small_batch_70b_full_size(sb, O, I, B):
-    """Llama-3-70B shapes at B = 2 and 8: the 28672-row shapes need more LDS
-    per workgroup than a launch may request unless tiles per workgroup are
-    capped."""
+    """Llama-3-70B shapes at B = 2, 3, 4 and 8 (every wavefront takes several
+    gblocks; B <= 4 runs the depth-4 ring): the 28672-row shapes need more
+    LDS per workgroup than a launch may request unless tiles per workgroup
+    are capped."""
     planes, coeffs = synth.random_sbvr(O, I, 4, seed=O + 5 * I + B)
     X = synth.activations(I, seed=B + 3 * O + synth.X_SEED_OFFSET, batch=B)
     Y = run_gemm(sb, packed(sb, planes, coeffs), X)
