@@ -74,8 +74,9 @@ roofline.mean_launch_us); --kernel-summary TRACE_CSV prints per-kernel
 duration statistics of a rocprofv3 kernel trace.
 
 --traffic-probe runs, eagerly, four launches of every projection shape (fp16
-and W4A8 activations, small batch B = 8, the coefficient-cache format, and
-the prefill decompression to binary16) and an elementwise
+and W4A8 activations, the grouped q|k|v and gate|up launches, small batch
+B = 8, the coefficient-cache format, and the prefill decompression to
+binary16) and an elementwise
 negation over 256 MiB of float32 (reads and writes 256 MiB: the counter
 calibration), for
   rocprofv3 --pmc FETCH_SIZE -- python3 bench.py --traffic-probe   (and WRITE_SIZE);
@@ -566,6 +567,11 @@ def main():
                 for li in range(L):
                     W, x, y = layers[li][name]
                     sb.gemv_a8(W, x, out=y, stream=stream)
+            for li in range(L):  # grouped launches: q|k|v and gate|up of each layer
+                for names in (("q", "k", "v"), ("gate", "up")):
+                    lay = layers[li]
+                    sb.gemv_grouped([lay[n][0] for n in names], [lay[names[0]][1]] * len(names),
+                                    outs=[lay[n][2] for n in names], stream=stream)
             for name in PROJ_ORDER:  # small batch, B = 8 vectors
                 O, I = shapes[name]
                 X8 = torch.from_numpy(synth.activations(I, seed=77, batch=8)).to(dev)
