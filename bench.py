@@ -8,7 +8,7 @@ shapes (Llama-3-70B with --model llama3-70b).  The weights of L = 32 decoder
 layers (3.93 GB at 4 bits, more than every cache) are resident in HBM; the
 timed region is one replay of a HIP graph of exactly K layer-steps on one
 stream, step i running layer i mod L's seven GEMVs, after one replay of a
-W-step warm-up graph and one untimed replay of the timed graph -- so
+W-step warm-up graph and three untimed replays of the timed graph -- so
 ms_per_step does not depend on how K relates to L.
 
 Weights are drawn directly in SBVR form (uniform bit planes, Gaussian fp16
@@ -27,7 +27,8 @@ One JSON line is printed:
                 matrix each (rows concatenated), 4 GEMVs per layer
   decode_step_grouped the 224 GEMVs on the separate weights, q, k, v and
                 gate, up each enqueued as one grouped launch
-                (sbvr_gemv_grouped): 4 launches per layer
+                (sbvr_gemv_grouped): 4 launches per layer; w4a8_*: the same
+                with SBVR-8 activations (sbvr_gemv_grouped_a8)
   per_call_us   mean duration of each projection's launch, from HIP events
                 around a graph of 64 back-to-back launches of that shape
                 cycling through >= 1 GB of distinct weight copies (median
@@ -633,7 +634,10 @@ def main():
         warm_graph = capture(step_calls(args.warmup, first=args.steps))
         timed(warm_graph.replay)
         del warm_graph
-    timed(steps_graph.replay)  # first replay of a new graph: untimed as well
+    # the first replays of a new graph are untimed as well (with a single one,
+    # the timed replay after it was at times up to 9 % slower than the rest)
+    for _ in range(3):
+        timed(steps_graph.replay)
     torch.cuda.synchronize()
     total_ms = timed(steps_graph.replay)
     ms_per_step = total_ms / args.steps
@@ -824,6 +828,21 @@ def main():
                                "mean_us_per_token": round(float(np.mean(reps)), 2),
                                "gbps": round(layer_bytes * L / (us * 1e3), 1), "replays": len(reps)}
         del grouped_graph
+        # the same with SBVR-8 activations (the paper's W4A8 decode configuration)
+        a8_calls = []
+        for li in range(L):
+            lay = layers[li]
+            for names in (("q", "k", "v"), ("o",), ("gate", "up"), ("down",)):
+                Ws, ys = [lay[n][0] for n in names], [lay[n][2] for n in names]
+                a8_calls.append(((lambda Ws, x, ys, stream: sb.gemv_grouped(Ws, [x] * len(Ws), outs=ys, stream=stream,
+                                                                            a8=True)), (Ws, lay[names[0]][1], ys)))
+        a8_graph = capture(a8_calls)
+        timed(a8_graph.replay)
+        reps = [timed(a8_graph.replay) * 1e3 for _ in range(DECODE_REPLAYS)]
+        us = float(np.median(reps))
+        decode_step_grouped["w4a8_us_per_token"] = round(us, 2)
+        decode_step_grouped["w4a8_gbps"] = round(layer_bytes * L / (us * 1e3), 1)
+        del a8_graph
 
     # ---- per-launch durations: >= 64 back-to-back launches per graph, cycling
     # through distinct weight copies totalling >= ROTATE_BYTES ----

@@ -73,7 +73,7 @@ const char *sbvr_status_string(int status);
 /* Library ABI version (major * 100 + minor); 1.01 adds sbvr_decompress,
  * 1.02 sbvr_gemv_a8, 1.03 the coefficient-cache format entry points,
  * 1.04 sbvr_encode and sbvr_decompress_indexed, 1.05 sbvr_gemm_prefill,
- * 1.06 sbvr_gemv_grouped. */
+ * 1.06 sbvr_gemv_grouped and sbvr_gemv_grouped_a8. */
 int sbvr_version(void);
 
 /*
@@ -183,6 +183,16 @@ int sbvr_gemv_a8(int O, int I, int k, const void *planes_dev, const void *coeffs
 int sbvr_gemv_grouped(int n, const int *O, int I, int k, const void *const *planes_dev,
                       const void *const *coeffs_dev, const uint16_t *const *x, uint16_t *const *y,
                       void *workspace, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * The same grouping for the W4A8 decode GEMV: n independent sbvr_gemv_a8
+ * calls (Sec. 4.3 and 4.4 with 8-bit SBVR activations, each member bit for
+ * bit its own sbvr_gemv_a8) as one kernel launch.  Arguments, ownership and
+ * errors as sbvr_gemv_grouped.
+ */
+int sbvr_gemv_grouped_a8(int n, const int *O, int I, int k, const void *const *planes_dev,
+                         const void *const *coeffs_dev, const uint16_t *const *x, uint16_t *const *y,
+                         void *workspace, size_t ws_bytes, hipStream_t stream);
 
 /*
  * Prefill GEMM on SBVR weights (the prefill design of Sec. 5.1: the weights

@@ -31,7 +31,7 @@ EXPORTED = (
     "sbvr_workspace_bytes", "sbvr_pack", "sbvr_unpack", "sbvr_gemv", "sbvr_gemm_small_batch",
     "sbvr_decompress", "sbvr_gemv_a8", "sbvr_packed_index_bytes", "sbvr_packed_table_bytes",
     "sbvr_pack_indexed", "sbvr_unpack_indexed", "sbvr_gemv_indexed", "sbvr_gemv_indexed_a8", "sbvr_encode",
-    "sbvr_decompress_indexed", "sbvr_gemm_prefill", "sbvr_gemv_grouped",
+    "sbvr_decompress_indexed", "sbvr_gemm_prefill", "sbvr_gemv_grouped", "sbvr_gemv_grouped_a8",
 )
 
 
@@ -78,6 +78,7 @@ def _load():
         "sbvr_decompress_indexed": (i32, [i32, i32, i32, i32, vp, vp, vp, vp, vp]),
         "sbvr_gemm_prefill": (i32, [i32, i32, i32, vp, vp, vp, vp, i32, vp]),
         "sbvr_gemv_grouped": (i32, [i32, vp, i32, i32, vp, vp, vp, vp, vp, sz, vp]),
+        "sbvr_gemv_grouped_a8": (i32, [i32, vp, i32, i32, vp, vp, vp, vp, vp, sz, vp]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -138,16 +139,26 @@ def sbvr_gemv_a8(O, I, k, planes_dev, coeffs_dev, x, y, workspace=None, ws_bytes
 GEMV_GROUP_MAX = 4
 
 
-def sbvr_gemv_grouped(n, O, I, k, planes_dev, coeffs_dev, x, y, workspace=None, ws_bytes=0, stream=0) -> int:
-    """O, planes_dev, coeffs_dev, x, y: sequences of n ints (out_features and
-    device pointers), marshalled into the host arrays the C call reads."""
+def _grouped(fn, n, O, I, k, planes_dev, coeffs_dev, x, y, workspace, ws_bytes, stream) -> int:
     seq = (O, planes_dev, coeffs_dev, x, y)
     if any(len(v) < n for v in seq):
         return SBVR_E_INVALID_ARG
     m = max(n, 1)
     arr_O = (C.c_int * m)(*[int(v) for v in list(O)[:n]])
     ptrs = [(C.c_void_p * m)(*[int(p) for p in list(v)[:n]]) for v in seq[1:]]
-    return _lib.sbvr_gemv_grouped(n, arr_O, I, k, *ptrs, workspace, ws_bytes, stream)
+    return fn(n, arr_O, I, k, *ptrs, workspace, ws_bytes, stream)
+
+
+def sbvr_gemv_grouped(n, O, I, k, planes_dev, coeffs_dev, x, y, workspace=None, ws_bytes=0, stream=0) -> int:
+    """O, planes_dev, coeffs_dev, x, y: sequences of n ints (out_features and
+    device pointers), marshalled into the host arrays the C call reads."""
+    return _grouped(_lib.sbvr_gemv_grouped, n, O, I, k, planes_dev, coeffs_dev, x, y, workspace, ws_bytes, stream)
+
+
+def sbvr_gemv_grouped_a8(n, O, I, k, planes_dev, coeffs_dev, x, y, workspace=None, ws_bytes=0, stream=0) -> int:
+    """As sbvr_gemv_grouped, with the W4A8 conversion of sbvr_gemv_a8."""
+    return _grouped(_lib.sbvr_gemv_grouped_a8, n, O, I, k, planes_dev, coeffs_dev, x, y, workspace, ws_bytes,
+                    stream)
 
 
 def sbvr_packed_index_bytes(O: int, I: int, k: int) -> int:
@@ -297,9 +308,10 @@ def gemv(W: PackedWeight, x, out=None, stream=None):
     return y
 
 
-def gemv_grouped(Ws, xs, outs=None, stream=None):
+def gemv_grouped(Ws, xs, outs=None, stream=None, a8=False):
     """y_i = SBVR(W_i) x_i for up to GEMV_GROUP_MAX matrices with the same I
-    and k, as one kernel launch; returns the list of fp16 [O_i] outputs."""
+    and k, as one kernel launch (a8: each as gemv_a8); returns the list of
+    fp16 [O_i] outputs."""
     Ws, xs = list(Ws), list(xs)
     assert 1 <= len(Ws) <= GEMV_GROUP_MAX and len(xs) == len(Ws)
     I, k = Ws[0].I, Ws[0].k
@@ -307,9 +319,9 @@ def gemv_grouped(Ws, xs, outs=None, stream=None):
     for W, x in zip(Ws, xs):
         _check_input(W, x, (W.I,))
     ys = [_out(None if outs is None else outs[i], (W.O,), xs[i]) for i, W in enumerate(Ws)]
-    _check(sbvr_gemv_grouped(len(Ws), [W.O for W in Ws], I, k, [W.planes.data_ptr() for W in Ws],
-                             [W.coeffs.data_ptr() for W in Ws], [x.data_ptr() for x in xs],
-                             [y.data_ptr() for y in ys], None, 0, _stream(stream)), "sbvr_gemv_grouped")
+    fn, name = (sbvr_gemv_grouped_a8, "sbvr_gemv_grouped_a8") if a8 else (sbvr_gemv_grouped, "sbvr_gemv_grouped")
+    _check(fn(len(Ws), [W.O for W in Ws], I, k, [W.planes.data_ptr() for W in Ws], [W.coeffs.data_ptr() for W in Ws],
+              [x.data_ptr() for x in xs], [y.data_ptr() for y in ys], None, 0, _stream(stream)), name)
     return ys
 
 

@@ -104,6 +104,21 @@ WeightRef indexed_weights(const void *planes, const void *index, const void *tab
     return WeightRef{planes, nullptr, index, table, n_sets};
 }
 
+int grouped_gemv(int n, const int *O, int I, int k, const void *const *planes_dev, const void *const *coeffs_dev,
+                 const uint16_t *const *x, uint16_t *const *y, size_t ws_bytes, bool a8, hipStream_t stream)
+{
+    if (n < 1 || n > SBVR_GEMV_GROUP_MAX || !O || !planes_dev || !coeffs_dev || !x || !y)
+        return SBVR_E_INVALID_ARG;
+    GemvMember mem[SBVR_GEMV_GROUP_MAX];
+    for (int i = 0; i < n; ++i) {
+        int st = check_gemv(O[i], I, k, planes_dev[i], coeffs_dev[i], x[i], y[i], 1, ws_bytes);
+        if (st != SBVR_OK)
+            return st;
+        mem[i] = GemvMember{O[i], planes_dev[i], coeffs_dev[i], x[i], y[i]};
+    }
+    return launch_gemv_group(n, mem, I, k, a8, stream);
+}
+
 }  // namespace
 
 extern "C" {
@@ -194,21 +209,21 @@ int sbvr_gemv_a8(int O, int I, int k, const void *planes_dev, const void *coeffs
     return launch_gemv_b1(make_dims(O, I, k), per_group_weights(planes_dev, coeffs_dev), x, y, true, stream);
 }
 
+
 int sbvr_gemv_grouped(int n, const int *O, int I, int k, const void *const *planes_dev,
                       const void *const *coeffs_dev, const uint16_t *const *x, uint16_t *const *y,
                       void *workspace, size_t ws_bytes, hipStream_t stream)
 {
     (void)workspace;
-    if (n < 1 || n > SBVR_GEMV_GROUP_MAX || !O || !planes_dev || !coeffs_dev || !x || !y)
-        return SBVR_E_INVALID_ARG;
-    GemvMember mem[SBVR_GEMV_GROUP_MAX];
-    for (int i = 0; i < n; ++i) {
-        int st = check_gemv(O[i], I, k, planes_dev[i], coeffs_dev[i], x[i], y[i], 1, ws_bytes);
-        if (st != SBVR_OK)
-            return st;
-        mem[i] = GemvMember{O[i], planes_dev[i], coeffs_dev[i], x[i], y[i]};
-    }
-    return launch_gemv_group(n, mem, I, k, stream);
+    return grouped_gemv(n, O, I, k, planes_dev, coeffs_dev, x, y, ws_bytes, false, stream);
+}
+
+int sbvr_gemv_grouped_a8(int n, const int *O, int I, int k, const void *const *planes_dev,
+                         const void *const *coeffs_dev, const uint16_t *const *x, uint16_t *const *y,
+                         void *workspace, size_t ws_bytes, hipStream_t stream)
+{
+    (void)workspace;
+    return grouped_gemv(n, O, I, k, planes_dev, coeffs_dev, x, y, ws_bytes, true, stream);
 }
 
 size_t sbvr_packed_index_bytes(int O, int I, int k)

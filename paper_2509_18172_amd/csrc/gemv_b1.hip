@@ -259,14 +259,14 @@ __global__ void __launch_bounds__(1024) gemv_b1_kernel(const uint4 *planes_, con
     gemv_b1_body<K, T, A8, IX>(a, blockIdx.x);
 }
 
-// Grouped launch (binary16 activations, per-group coefficients): the
+// Grouped launch (per-group coefficients; A8: SBVR-8 activations): the
 // workgroups of every member in one grid, each bound to its member's matrix.
-template <int K, int T>
+template <int K, int T, bool A8>
 __global__ void __launch_bounds__(1024) gemv_b1_group_kernel(GemvArgs a_rest, GemvGroup g)
 {
     GemvArgs a = a_rest;
     const unsigned bid = (unsigned)bind_group_member(g, a, (int)blockIdx.x);
-    gemv_b1_body<K, T, false, false>(a, bid);
+    gemv_b1_body<K, T, A8, false>(a, bid);
 }
 
 // Launch shape.  T tiles (T * TR rows) per workgroup: the most (<= 8) that still
@@ -356,18 +356,24 @@ int fill_group(GemvGroup &g, int n, const GemvMember *mem, const Dims &d, int ti
     return wg;
 }
 
-template <int K>
+template <int K, bool A8>
 static const void *b1_group_kernel_for(int T)
 {
     switch (T) {
-    case 8: return (const void *)gemv_b1_group_kernel<K, 8>;
-    case 4: return (const void *)gemv_b1_group_kernel<K, 4>;
-    case 2: return (const void *)gemv_b1_group_kernel<K, 2>;
-    default: return (const void *)gemv_b1_group_kernel<K, 1>;
+    case 8: return (const void *)gemv_b1_group_kernel<K, 8, A8>;
+    case 4: return (const void *)gemv_b1_group_kernel<K, 4, A8>;
+    case 2: return (const void *)gemv_b1_group_kernel<K, 2, A8>;
+    default: return (const void *)gemv_b1_group_kernel<K, 1, A8>;
     }
 }
 
-int launch_gemv_group(int n, const GemvMember *mem, int I, int k, hipStream_t stream)
+template <int K>
+static const void *b1_group_kernel_for(int T, bool a8)
+{
+    return a8 ? b1_group_kernel_for<K, true>(T) : b1_group_kernel_for<K, false>(T);
+}
+
+int launch_gemv_group(int n, const GemvMember *mem, int I, int k, bool a8, hipStream_t stream)
 {
     // the combined shape (every member's row tiles) selects kernel and shape
     Dims d = make_dims(mem[0].O, I, k);
@@ -377,17 +383,17 @@ int launch_gemv_group(int n, const GemvMember *mem, int I, int k, hipStream_t st
     d.n_tiles = tiles;
     d.O = tiles * d.tr;
     if (d.n_gblocks > B1_MAX_WAVES || (long)d.n_tiles * d.n_gblocks >= SBVR_B1S_MIN_BLOCKS)
-        return launch_gemv_b1s_group(d, n, mem, stream);
+        return launch_gemv_b1s_group(d, n, mem, a8, stream);
     const int T = choose_b1_tiles(d);
     const int waves = d.n_gblocks;
     GemvGroup g;
     const int grid = fill_group(g, n, mem, d, T);
     GemvArgs a = {nullptr, nullptr, nullptr, nullptr, 0, d.I, d.k, 0, d.n_gblocks, 1, 1, 0, nullptr, nullptr, 0};
     const size_t lds = (size_t)waves * B1_WAVE_LDS + (size_t)waves * T * d.tr * 4;
-    const void *fn = d.k == 4   ? b1_group_kernel_for<4>(T)
-                     : d.k == 3 ? b1_group_kernel_for<3>(T)
-                     : d.k == 2 ? b1_group_kernel_for<2>(T)
-                                : b1_group_kernel_for<1>(T);
+    const void *fn = d.k == 4   ? b1_group_kernel_for<4>(T, a8)
+                     : d.k == 3 ? b1_group_kernel_for<3>(T, a8)
+                     : d.k == 2 ? b1_group_kernel_for<2>(T, a8)
+                                : b1_group_kernel_for<1>(T, a8);
     void *args[] = {&a, &g};
     return launch_kernel(fn, dim3(grid), dim3(64 * waves), lds, stream, args);
 }

@@ -338,14 +338,14 @@ __global__ void __launch_bounds__(1024) gemv_b1s_kernel(const uint4 *planes_, co
     gemv_b1s_body<K, D, MULTI, A8, IX>(a, nw_, blockIdx.x);
 }
 
-// Grouped launch (binary16 activations, per-group coefficients): the
+// Grouped launch (per-group coefficients; A8: SBVR-8 activations): the
 // workgroups of every member in one grid, each bound to its member's matrix.
-template <int K, int D, bool MULTI>
+template <int K, int D, bool MULTI, bool A8>
 __global__ void __launch_bounds__(1024) gemv_b1s_group_kernel(int nw_, GemvArgs a_rest, GemvGroup g)
 {
     GemvArgs a = a_rest;
     const unsigned bid = (unsigned)bind_group_member(g, a, (int)blockIdx.x);
-    gemv_b1s_body<K, D, MULTI, false, false>(a, nw_, bid);
+    gemv_b1s_body<K, D, MULTI, A8, false>(a, nw_, bid);
 }
 
 template <int K, bool A8, bool IX>
@@ -426,30 +426,37 @@ int launch_gemv_b1s(const Dims &d, const WeightRef &w, const uint16_t *x, uint16
 }
 
 // the same instance choice as b1s_kernel_for, for the grouped kernel
-template <int K>
+template <int K, bool A8>
 static const void *b1s_group_kernel_for(bool multi, bool short_run, bool wide)
 {
     if constexpr (K == 4) {
         if (wide)
-            return (const void *)gemv_b1s_group_kernel<K, SBVR_B1S_DEPTH_WIDE, false>;
+            return (const void *)gemv_b1s_group_kernel<K, SBVR_B1S_DEPTH_WIDE, false, A8>;
     }
     if (!multi)
-        return (const void *)gemv_b1s_group_kernel<K, SBVR_B1S_DEPTH, false>;
-    return short_run ? (const void *)gemv_b1s_group_kernel<K, 2, true>
-                     : (const void *)gemv_b1s_group_kernel<K, SBVR_B1S_DEPTH_MULTI, true>;
+        return (const void *)gemv_b1s_group_kernel<K, SBVR_B1S_DEPTH, false, A8>;
+    return short_run ? (const void *)gemv_b1s_group_kernel<K, 2, true, A8>
+                     : (const void *)gemv_b1s_group_kernel<K, SBVR_B1S_DEPTH_MULTI, true, A8>;
 }
 
-int launch_gemv_b1s_group(const Dims &d, int n, const GemvMember *mem, hipStream_t stream)
+template <int K>
+static const void *b1s_group_kernel_for(bool multi, bool short_run, bool wide, bool a8)
+{
+    return a8 ? b1s_group_kernel_for<K, true>(multi, short_run, wide)
+              : b1s_group_kernel_for<K, false>(multi, short_run, wide);
+}
+
+int launch_gemv_b1s_group(const Dims &d, int n, const GemvMember *mem, bool a8, hipStream_t stream)
 {
     const B1sShape sh = b1s_shape(d, false);
     GemvGroup g;
     const int grid = fill_group(g, n, mem, d, sh.tpw);
     GemvArgs a = {nullptr, nullptr, nullptr, nullptr, 0, d.I, d.k, 0, d.n_gblocks, sh.gpw, 1, sh.tpw,
                   nullptr, nullptr, 0};
-    const void *fn = d.k == 4   ? b1s_group_kernel_for<4>(sh.multi, sh.short_run, sh.wide)
-                     : d.k == 3 ? b1s_group_kernel_for<3>(sh.multi, sh.short_run, sh.wide)
-                     : d.k == 2 ? b1s_group_kernel_for<2>(sh.multi, sh.short_run, sh.wide)
-                                : b1s_group_kernel_for<1>(sh.multi, sh.short_run, sh.wide);
+    const void *fn = d.k == 4   ? b1s_group_kernel_for<4>(sh.multi, sh.short_run, sh.wide, a8)
+                     : d.k == 3 ? b1s_group_kernel_for<3>(sh.multi, sh.short_run, sh.wide, a8)
+                     : d.k == 2 ? b1s_group_kernel_for<2>(sh.multi, sh.short_run, sh.wide, a8)
+                                : b1s_group_kernel_for<1>(sh.multi, sh.short_run, sh.wide, a8);
     int nw = sh.waves;
     void *args[] = {&nw, &a, &g};
     return launch_kernel(fn, dim3(grid), dim3(64 * sh.waves), sh.lds, stream, args);

@@ -75,7 +75,8 @@ struct GemvGroup;
 // Fills the member table for workgroups of `tiles_per_group` row tiles and
 // returns the grid size.
 int fill_group(GemvGroup &g, int n, const GemvMember *mem, const Dims &d, int tiles_per_group);
-int launch_gemv_group(int n, const GemvMember *mem, int I, int k, hipStream_t stream);
-int launch_gemv_b1s_group(const Dims &d, int n, const GemvMember *mem, hipStream_t stream);
+// a8: activations converted online to SBVR-8 (every member)
+int launch_gemv_group(int n, const GemvMember *mem, int I, int k, bool a8, hipStream_t stream);
+int launch_gemv_b1s_group(const Dims &d, int n, const GemvMember *mem, bool a8, hipStream_t stream);
 
 }  // namespace sbvr

@@ -1,5 +1,6 @@
-"""The grouped batch-1 GEMV (sbvr_gemv_grouped): several GEMVs with the same
-inner dimension and plane count in one launch.
+"""The grouped batch-1 GEMV (sbvr_gemv_grouped, and sbvr_gemv_grouped_a8 for
+SBVR-8 activations): several GEMVs with the same inner dimension and plane
+count in one launch.
 
   * Every member's output equals, bit for bit, the sbvr_gemv of its own
     arguments (the per-row arithmetic depends only on I and k), and meets the
@@ -91,6 +92,29 @@ def test_grouped_matches_separate_and_oracle(sb, Os, I, k, shared_x):
         assert err <= TOL, (Os, i, err)
 
 
+@pytest.mark.parametrize("Os,I,k", [((4096, 1024, 1024), 4096, 4), ((14336, 14336), 4096, 4),
+                                     ((4096, 4096), 14336, 4), ((1, 17, 300, 1001), 640, 3), ((33, 70), 2560, 2)])
+def test_grouped_a8_matches_separate_and_oracle(sb, Os, I, k):
+    """W4A8 members: each bit for bit its own sbvr_gemv_a8, and within the
+    gate of the oracle's W4A8 GEMV (the exact product with the SBVR-8
+    activations)."""
+    log(f"grouped a8 {Os} x {I} k={k}")
+    mats, Ws, xs = members(sb, Os, I, k, seed=900 + I + k, shared_x=False)
+    xd = [dev(x) for x in xs]
+    ys = sb.gemv_grouped(Ws, xd, a8=True)
+    sep = [sb.gemv_a8(W, x) for W, x in zip(Ws, xd)]
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(len(Os) + 7 * I)
+    for i, ((planes, coeffs), O) in enumerate(zip(mats, Os)):
+        got = ys[i].cpu().numpy()
+        assert np.array_equal(got.view(np.uint16), sep[i].cpu().numpy().view(np.uint16)), (Os, i)
+        rows = np.unique(np.r_[0, O - 1, rng.integers(0, O, min(O, 96))])
+        y_ref = oracle.sbvr_gemv_w4a8(planes, coeffs, xs[i], rows=rows)
+        err = rel_err(got[rows].astype(np.float64), y_ref)
+        log(f"  member {i} ({O} rows): err {err:.3e}")
+        assert err <= TOL, (Os, i, err)
+
+
 def test_grouped_oracle_encoded_members(sb):
     """Members encoded from Gaussian weights with outliers by the oracle
     (Algorithm 1, k = 4), every row checked."""
@@ -128,6 +152,11 @@ def test_grouped_error_paths(sb):
     torch.cuda.synchronize()
     assert all(bool((y == 7.0).all()) for y in ys)  # nothing was written
     assert g(2, O, I, k, P, Cf, X, Y) == sb.SBVR_OK
+    ga = sb.sbvr_gemv_grouped_a8
+    assert ga(0, O, I, k, P, Cf, X, Y) == sb.SBVR_E_INVALID_ARG
+    assert ga(2, O, I, 5, P, Cf, X, Y) == sb.SBVR_E_UNSUPPORTED
+    assert ga(2, O, I, k, P, Cf, [X[0], X[0] + 8], Y) == sb.SBVR_E_ALIGNMENT
+    assert ga(2, O, I, k, P, Cf, X, Y) == sb.SBVR_OK
 
 
 def test_grouped_graph_replays_match_eager(sb):
