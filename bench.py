@@ -131,8 +131,9 @@ def parse():
     ap.add_argument("--headline-only", action="store_true",
                     help="only the timed steps, the dominant kernel's event-timed launches and the decode step "
                          "(the run whose kernel statistics are compared with the headline)")
-    ap.add_argument("--kernel-summary", metavar="KERNEL_TRACE_CSV",
-                    help="print per-dispatch duration statistics from a rocprofv3 kernel trace and exit")
+    ap.add_argument("--kernel-summary", nargs="+", metavar="PATH",
+                    help="KERNEL_TRACE_CSV [BENCH_JSON]: print per-dispatch duration statistics from a rocprofv3 "
+                         "kernel trace (with the traced run's own JSON line: its per-launch times) and exit")
     ap.add_argument("--k", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
@@ -313,29 +314,63 @@ def counter_summary(a_csv: str, b_csv: str) -> str:
     return "\n".join(lines)
 
 
-def kernel_summary(trace_csv: str) -> str:
+def kernel_summary(trace_csv: str, bench_json: str = None) -> str:
     """Markdown table of a rocprofv3 kernel trace: dispatches of the SBVR
     kernels grouped by kernel instance, workgroup size and grid size (threads),
-    with count and mean / median / min / max duration (end - start timestamp)."""
+    with count and mean / median / min / max duration (end - start timestamp),
+    and the same over the back-to-back dispatches -- those that started when
+    the dispatch before them (any kernel) ended, as every launch of a timed
+    graph does when nothing holds the queue; the tracer itself delays some
+    dispatches, and those start on an idle GPU.  With the traced run's own
+    JSON line (bench_json), the record also carries that run's per-launch
+    times of the batch-1 instances (step_launch_us), the live measurement
+    taken under the same tracer."""
     import numpy as np
-    groups = {}
+    disp = []
     with open(trace_csv, newline="") as f:
         for row in csv.DictReader(f):
-            name = row["Kernel_Name"]
-            if "sbvr" not in name:
-                continue
-            key = (short_kernel_name(name), int(row["Workgroup_Size_X"]), int(row["Grid_Size_X"]))
-            groups.setdefault(key, []).append(int(row["End_Timestamp"]) - int(row["Start_Timestamp"]))
-    lines = ["| kernel | workgroup | grid | calls | mean ns | median ns | min ns | max ns |",
-             "|---|---:|---:|---:|---:|---:|---:|---:|"]
+            disp.append((int(row["Start_Timestamp"]), int(row["End_Timestamp"]), row["Kernel_Name"],
+                         int(row["Workgroup_Size_X"]), int(row["Grid_Size_X"])))
+    disp.sort()
+    groups, b2b = {}, {}
+    prev_end = None
+    for start, end, name, wg, grid in disp:
+        back_to_back = prev_end is not None and start <= prev_end
+        prev_end = end if prev_end is None else max(prev_end, end)
+        if "sbvr" not in name:
+            continue
+        key = (short_kernel_name(name), wg, grid)
+        groups.setdefault(key, []).append(end - start)
+        if back_to_back:
+            b2b.setdefault(key, []).append(end - start)
+    traced_live = {}
+    if bench_json:
+        with open(bench_json) as fh:
+            line = json.loads([ln for ln in fh.read().splitlines() if ln.startswith("{")][-1])
+        shapes = line["config"]["shapes"]
+        k = int(re.search(r"SBVR k=(\d+)", line["config"]["workload"]).group(1))
+        for proj, us in line.get("step_launch_us", {}).items():
+            traced_live.setdefault(b1_kernel_instance(*shapes[proj], k), []).append(us)
+    lines = ["| kernel | workgroup | grid | calls | mean ns | median ns | min ns | max ns | back-to-back calls | "
+             "back-to-back mean ns | back-to-back median ns |",
+             "|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|"]
     rec = {"source_sha256": kernel_source_digest(), "kernels": {}}
-    for (kname, wg, grid), d in sorted(groups.items(), key=lambda kv: -sum(kv[1])):
+    for key, d in sorted(groups.items(), key=lambda kv: -sum(kv[1])):
+        kname, wg, grid = key
         a = np.array(d, dtype=np.float64)
+        bb = np.array(b2b.get(key, []), dtype=np.float64)
+        bb_cols = f"{bb.size} | {bb.mean():.0f} | {np.median(bb):.0f}" if bb.size else "0 | - | -"
         lines.append(f"| `{kname}` | {wg} | {grid} | {a.size} | {a.mean():.0f} | {np.median(a):.0f} | "
-                     f"{a.min():.0f} | {a.max():.0f} |")
+                     f"{a.min():.0f} | {a.max():.0f} | {bb_cols} |")
         if kname.startswith("gemv_b1") and kname not in rec["kernels"]:  # the most-timed grid of each instance
-            rec["kernels"][kname] = {"workgroup": wg, "grid": grid, "calls": int(a.size),
-                                     "mean_ns": round(float(a.mean()), 1), "median_ns": round(float(np.median(a)), 1)}
+            r = {"workgroup": wg, "grid": grid, "calls": int(a.size),
+                 "mean_ns": round(float(a.mean()), 1), "median_ns": round(float(np.median(a)), 1)}
+            if bb.size:
+                r.update({"b2b_calls": int(bb.size), "b2b_mean_ns": round(float(bb.mean()), 1),
+                          "b2b_median_ns": round(float(np.median(bb)), 1)})
+            if kname in traced_live:
+                r["traced_live_us"] = round(float(np.mean(traced_live[kname])), 3)
+            rec["kernels"][kname] = r
     lines += ["", "rocprof-record: " + json.dumps(rec, sort_keys=True)]
     return "\n".join(lines)
 
@@ -497,7 +532,7 @@ def main():
         print(traffic_summary(*args.traffic_summary))
         return
     if args.kernel_summary:
-        print(kernel_summary(args.kernel_summary))
+        print(kernel_summary(*args.kernel_summary[:2]))
         return
     if args.prefill_summary:
         print(prefill_summary(args.prefill_summary))
@@ -716,6 +751,16 @@ def main():
                                "mean_over_live": round(prof_us / dom_us, 4),
                                "median_over_live": round(med_us / dom_us, 4),
                                "record": f"profiles/{ROCPROF_RECORD} ({prof['calls']} dispatches, grid {prof['grid']})"}
+        if "b2b_mean_ns" in prof:  # dispatches that started when the one before them ended
+            bm, bmed = prof["b2b_mean_ns"] / 1e3, prof["b2b_median_ns"] / 1e3
+            roofline["rocprof"]["back_to_back"] = {
+                "calls": prof["b2b_calls"], "mean_launch_us": round(bm, 3), "median_launch_us": round(bmed, 3),
+                "frac_mean": round(bytes_per_launch / (bm * 1e3) / PEAK_GBPS, 4),
+                "frac_median": round(bytes_per_launch / (bmed * 1e3) / PEAK_GBPS, 4),
+                "mean_over_live": round(bm / dom_us, 4), "median_over_live": round(bmed / dom_us, 4)}
+        if "traced_live_us" in prof:  # the traced run's own per-launch time, under the same tracer
+            roofline["rocprof"]["traced_live_us"] = prof["traced_live_us"]
+            roofline["rocprof"]["mean_over_traced_live"] = round(prof_us / prof["traced_live_us"], 4)
     step_launch_us = {n: round(float(np.mean(launch_times[n])), 3) for n in PROJ_ORDER}
 
     decode_graph = capture([gemv_call(*layers[li][n]) for li in range(L) for n in PROJ_ORDER])

@@ -1,6 +1,7 @@
 """Host-side logic of bench.py (no GPU): kernel-instance naming and the
 counter-record summary."""
 import csv
+import json
 import os
 import sys
 
@@ -96,26 +97,41 @@ def test_more_than_one_gpu_is_refused():
 
 def test_kernel_summary_groups_dispatches(tmp_path):
     """--kernel-summary: per (instance, workgroup, grid) mean and median of
-    end - start, and the machine-readable record the bench reads back."""
+    end - start, over all dispatches and over the back-to-back ones (started
+    when the dispatch before them, of any kernel, ended), the traced run's
+    own per-launch times, and the machine-readable record the bench reads
+    back."""
     cols = ["Kind", "Kernel_Name", "Start_Timestamp", "End_Timestamp", "Workgroup_Size_X", "Grid_Size_X"]
     gate = "void sbvr::gemv_b1s_kernel<4, 4, false, false, false>(HIP_vector_type<unsigned int, 4u> const*)"
     kv = "void sbvr::gemv_b1_kernel<4, 1, false, false>(HIP_vector_type<unsigned int, 4u> const*)"
-    rows = [(gate, 1000, 8000, 512, 131072), (gate, 9000, 16200, 512, 131072), (gate, 20000, 27400, 512, 131072),
-            (kv, 30000, 32600, 512, 131072), ("other_kernel(int)", 0, 5, 64, 64)]
+    # gate 2 starts when the other kernel ends, gate 3 when gate 2 ends: back to
+    # back; gate 1 and the k/v launch start after a gap
+    rows = [(gate, 1000, 8000, 512, 131072), ("other_kernel(int)", 8500, 9000, 64, 64),
+            (gate, 9000, 16200, 512, 131072), (gate, 16200, 23600, 512, 131072),
+            (kv, 30000, 32600, 512, 131072)]
     path = tmp_path / "trace.csv"
     with open(path, "w", newline="") as fh:
         w = csv.writer(fh)
         w.writerow(cols)
         for name, a, b, wg, grid in rows:
             w.writerow(["KERNEL_DISPATCH", name, a, b, wg, grid])
-    text = bench.kernel_summary(str(path))
-    assert "| `gemv_b1s_kernel<4, 4, false, false, false>` | 512 | 131072 | 3 | 7200 | 7200 | 7000 | 7400 |" in text
+    shapes = {"q": [4096, 4096], "k": [1024, 4096], "v": [1024, 4096], "o": [4096, 4096], "gate": [14336, 4096],
+              "up": [14336, 4096], "down": [4096, 14336]}
+    line = {"config": {"workload": "llama3-8b decode-layer projections; SBVR k=4, group 128", "shapes": shapes},
+            "step_launch_us": {"q": 3.8, "k": 2.6, "v": 2.6, "o": 3.8, "gate": 7.5, "up": 7.3, "down": 7.7}}
+    js = tmp_path / "bench.json"
+    js.write_text("some log line\n" + json.dumps(line) + "\n")
+    text = bench.kernel_summary(str(path), str(js))
+    assert ("| `gemv_b1s_kernel<4, 4, false, false, false>` | 512 | 131072 | 3 | 7200 | 7200 | 7000 | 7400 | "
+            "2 | 7300 | 7300 |") in text
+    assert "| `gemv_b1_kernel<4, 1, false, false>` | 512 | 131072 | 1 | 2600 | 2600 | 2600 | 2600 | 0 | - | - |" in text
     assert "other_kernel" not in text
-    rec = [line for line in text.splitlines() if line.startswith("rocprof-record:")]
-    import json
+    rec = [ln for ln in text.splitlines() if ln.startswith("rocprof-record:")]
     r = json.loads(rec[0].split(":", 1)[1])
     assert r["kernels"]["gemv_b1s_kernel<4, 4, false, false, false>"] == {
-        "workgroup": 512, "grid": 131072, "calls": 3, "mean_ns": 7200.0, "median_ns": 7200.0}
+        "workgroup": 512, "grid": 131072, "calls": 3, "mean_ns": 7200.0, "median_ns": 7200.0,
+        "b2b_calls": 2, "b2b_mean_ns": 7300.0, "b2b_median_ns": 7300.0, "traced_live_us": 7.4}
+    assert r["kernels"]["gemv_b1_kernel<4, 1, false, false>"]["traced_live_us"] == 2.6
     assert r["source_sha256"] == bench.kernel_source_digest()
 
 
