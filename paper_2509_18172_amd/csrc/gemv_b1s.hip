@@ -90,6 +90,13 @@ constexpr int B1S_WAVE_LDS = 2048 + 256;
 // -amdgpu-kernarg-preload-count), so neither the first loads nor the LDS
 // waits before the matrix-core work sit behind a kernel-argument fetch (a
 // scalar load shares the LDS wait counter); the rest are read from the struct.
+// a * b rounded to binary32 on its own: never fused with a later addition
+__device__ __forceinline__ float mul_rounded(float a, float b)
+{
+#pragma clang fp contract(off)
+    return a * b;
+}
+
 // The kernel body for workgroup `bid` (of nw wavefronts) of the matrix in `a`.
 template <int K, int D, bool MULTI, bool A8, bool IX>
 __device__ __forceinline__ void gemv_b1s_body(const GemvArgs &a, int nw, unsigned bid)
@@ -284,9 +291,13 @@ __device__ __forceinline__ void gemv_b1s_body(const GemvArgs &a, int nw, unsigne
                 d = mfma_fp4_fp8<A8>(fp4_operand(pw.w), Bq[3], d);
                 float part[NP];
                 apply_coefs<K>(C[j], d, part);
+                // the scaled partial is rounded before the row sum (no fused
+                // multiply-add with a neighbour's term), as in the one-shot
+                // kernel: with SBVR-8 activations the scale is not a power of
+                // two, and both kernels then give the same bits
 #pragma unroll
                 for (int p = 0; p < NP; ++p)
-                    part[p] = row16_sum(part[p] * inv_scale);
+                    part[p] = row16_sum(mul_rounded(part[p], inv_scale));
                 if ((lane & 15) == 0) {
                     float *r = red_w + cur_i * nw * TR;
 #pragma unroll

@@ -115,6 +115,25 @@ def test_grouped_a8_matches_separate_and_oracle(sb, Os, I, k):
         assert err <= TOL, (Os, i, err)
 
 
+@pytest.mark.parametrize("a8", [False, True])
+@pytest.mark.parametrize("Os", [(4096, 14336, 14336), (2048, 1024, 28672), (1024, 30000)])
+def test_grouped_members_cross_kernel_families(sb, Os, a8):
+    """Members small enough for the one-shot kernel on their own, grouped with
+    large ones so that the launch runs the streaming kernel: every member still
+    gives the bits of its own call, with fp16 and with SBVR-8 activations (the
+    streaming kernel rounds each scaled partial before its row sum, as the
+    one-shot kernel does)."""
+    I, k = 4096, 4
+    log(f"grouped across kernel families {Os} a8={a8}")
+    mats, Ws, xs = members(sb, Os, I, k, seed=77 + sum(Os), shared_x=False)
+    xd = [dev(x) for x in xs]
+    ys = sb.gemv_grouped(Ws, xd, a8=a8)
+    sep = [(sb.gemv_a8 if a8 else sb.gemv)(W, x) for W, x in zip(Ws, xd)]
+    torch.cuda.synchronize()
+    for i, O in enumerate(Os):
+        assert torch.equal(ys[i].view(torch.int16), sep[i].view(torch.int16)), (Os, a8, i)
+
+
 def test_grouped_oracle_encoded_members(sb):
     """Members encoded from Gaussian weights with outliers by the oracle
     (Algorithm 1, k = 4), every row checked."""

@@ -11,7 +11,10 @@ activations:
   - sbvr_gemv_a8 against the oracle's W4A8 result (SBVR-8 activations);
   - sbvr_decompress bit for bit against rounding the oracle's exact decoding;
   - the coefficient-cache format (a random table and index) against the
-    oracle's gathered-coefficient GEMV.
+    oracle's gathered-coefficient GEMV;
+  - grouped launches (sbvr_gemv_grouped / _a8) of 1..4 members with random
+    row counts and one shared I and k: every member bit for bit its own
+    sbvr_gemv / sbvr_gemv_a8 call, and within the gate of the oracle.
 The launch shape (one-shot or streaming kernel, tiles and gblocks per
 workgroup, ring depth) follows from O and I, so the draws cover ragged row
 tiles, ragged gblocks and every kernel variant of these sizes.
@@ -118,3 +121,24 @@ def test_random_shapes_coefficient_cache(sb, shape, sets_per_ten):
     y = sb.gemv_indexed(Wi, dev(x))
     torch.cuda.synchronize()
     assert rel_err(y.cpu().numpy(), oracle.sbvr_gemv_indexed(planes, index, table, x)) <= TOL
+
+
+@SETTINGS
+@given(rows=st.lists(st.integers(1, 3000), min_size=1, max_size=4), g=st.integers(1, 64), k=st.integers(1, 4),
+       a8=st.booleans())
+def test_random_grouped_launches(sb, rows, g, k, a8):
+    I = 128 * g
+    seed = sum(rows) * 7 + I + k + int(a8)
+    print(f"grouped {rows} x {I} k={k} a8={a8}", flush=True)
+    mats = [synth.random_sbvr(O, I, k, seed=seed + 11 * i) for i, O in enumerate(rows)]
+    Ws = [sb.pack(dev(p.view(np.int32)), dev(c.view(np.int16))) for p, c in mats]
+    xs = [synth.activations(I, seed=seed + i + synth.X_SEED_OFFSET) for i in range(len(rows))]
+    xd = [dev(x) for x in xs]
+    ys = sb.gemv_grouped(Ws, xd, a8=a8)
+    sep = [(sb.gemv_a8 if a8 else sb.gemv)(W, x) for W, x in zip(Ws, xd)]
+    torch.cuda.synchronize()
+    ref = oracle.sbvr_gemv_w4a8 if a8 else oracle.sbvr_gemv
+    for i, (planes, coeffs) in enumerate(mats):
+        got = ys[i].cpu().numpy()
+        assert np.array_equal(got.view(np.uint16), sep[i].cpu().numpy().view(np.uint16)), (rows, I, k, a8, i)
+        assert rel_err(got, ref(planes, coeffs, xs[i])) <= TOL, (rows, I, k, a8, i)
