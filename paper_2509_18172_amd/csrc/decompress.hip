@@ -3,7 +3,10 @@
 // binary16 so that a dense matrix-core GEMM can consume it.  A sum of at most
 // four binary16 values is exact in binary64 (53-bit significand), so rounding
 // it once to binary16 (to nearest, ties to even) gives the correctly rounded
-// weight -- the same as rounding the exact decoded value.
+// weight -- the same as rounding the exact decoded value.  When the
+// coefficients' exponents span at most 11 the sum is exact in binary32 as
+// well and the hardware conversion rounds it (the common case; binary64
+// otherwise).
 //
 // A (tile, gblock) block of the device format is TR rows x 512 columns.  Each
 // of its TR x 4 (row, group) pairs has 2^k distinct decoded values (the subset
@@ -101,11 +104,27 @@ __global__ void __launch_bounds__(1024) decompress_kernel(Dims d, const uint32_t
                     c[i] = cp[i];
             }
         }
-        double s = 0.0;  // exact: at most K binary16 terms
+        uint32_t cw[K];
 #pragma unroll
         for (int i = 0; i < K; ++i)
-            s += ((sub >> i) & 1) ? (double)half_bits_to_float(c[i]) : 0.0;
-        lut[u][r * ROW_E + lb * NSUB + sub] = f64_to_f16_rne(s);
+            cw[i] = c[i];
+        const bool exact32 = f16_sums_exact_in_f32<K>(cw);
+        uint16_t val;
+        if (__builtin_amdgcn_ballot_w64(!exact32) == 0 || exact32) {
+            // binary32: the sum is exact, one hardware rounding to binary16
+            float s = 0.f;
+#pragma unroll
+            for (int i = 0; i < K; ++i)
+                s += ((sub >> i) & 1) ? half_bits_to_float(c[i]) : 0.f;
+            val = __half_as_ushort(__float2half_rn(s));
+        } else {
+            double s = 0.0;  // exact: at most K binary16 terms
+#pragma unroll
+            for (int i = 0; i < K; ++i)
+                s += ((sub >> i) & 1) ? (double)half_bits_to_float(c[i]) : 0.0;
+            val = f64_to_f16_rne(s);
+        }
+        lut[u][r * ROW_E + lb * NSUB + sub] = val;
     }
 
     uint32_t w[NB][K];

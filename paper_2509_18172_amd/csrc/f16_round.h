@@ -1,5 +1,6 @@
 // Exact binary64 -> binary16 rounding on the device, shared by the
-// decompression and encoding kernels.
+// decompression, prefill and encoding kernels, and the test for when binary32
+// subset sums are exact.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -42,6 +43,32 @@ __device__ __forceinline__ uint16_t f64_to_f16_rne(double x)
         return (uint16_t)(sign | (uint32_t)(E + 15) << 10 | (uint32_t)(q & 0x3ff));
     }
     return (uint16_t)(sign | (uint32_t)q);  // q == 0x400 is the smallest normal
+}
+
+// Unbiased exponent of a binary16 bit pattern (subnormals as -14).
+__device__ __forceinline__ int f16_exp(uint32_t h)
+{
+    const int e = (int)((h >> 10) & 0x1f);
+    return e == 0 ? -14 : e - 15;
+}
+
+// True when the subset sums of these k binary16 values are exact in binary32:
+// every value is a multiple of 2^(emin - 10) below 2^(emax + 1), so a sum of
+// at most four needs at most emax - emin + 13 significant bits, <= 24 when the
+// nonzero values' exponents span at most 11 (then one hardware rounding of
+// the binary32 sum to binary16 is the correctly rounded result).
+template <int K>
+__device__ __forceinline__ bool f16_sums_exact_in_f32(const uint32_t *c)
+{
+    int emax = -30, emin = 30;
+#pragma unroll
+    for (int i = 0; i < K; ++i) {
+        if (c[i] & 0x7fffu) {
+            emax = max(emax, f16_exp(c[i]));
+            emin = min(emin, f16_exp(c[i]));
+        }
+    }
+    return emax - emin <= 11;
 }
 
 }  // namespace sbvr

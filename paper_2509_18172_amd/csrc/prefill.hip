@@ -61,12 +61,6 @@ struct PrefillArgs {
     int S;                                    // K-slices per workgroup (a power of two)
 };
 
-__device__ __forceinline__ int f16_exp(uint32_t h)  // unbiased exponent, subnormals as -14
-{
-    const int e = (int)((h >> 10) & 0x1f);
-    return e == 0 ? -14 : e - 15;
-}
-
 // LDS: per K-slice two activation tiles of 16 BTT token rows (PF_XROW bytes
 // each: the group's 128 binary16 values), then per wavefront its 16 rows x
 // 2^k subset-sum table.  The K-slice reduction reuses the front afterwards.
