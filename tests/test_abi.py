@@ -89,6 +89,29 @@ def test_small_batch_validation():
     assert f(4, k=7) == sb.SBVR_E_UNSUPPORTED
 
 
+@pytest.mark.parametrize("name", ["sbvr_gemv_grouped", "sbvr_gemv_grouped_a8"])
+def test_grouped_validation(name):
+    """Every member is validated before anything is launched; the first
+    failing member's status is returned."""
+    f = getattr(sb, name)
+
+    def g(n=2, O=(16, 32), I=256, k=4, P=(FAKE, FAKE), Cf=(FAKE, FAKE), X=(FAKE, FAKE), Y=(FAKE, FAKE)):
+        return f(n, list(O), I, k, list(P), list(Cf), list(X), list(Y))
+    assert g(n=0) == sb.SBVR_E_INVALID_ARG
+    assert g(n=5, O=(16,) * 5, P=(FAKE,) * 5, Cf=(FAKE,) * 5, X=(FAKE,) * 5, Y=(FAKE,) * 5) == sb.SBVR_E_INVALID_ARG
+    assert g(O=(16, 0)) == sb.SBVR_E_INVALID_ARG
+    assert g(I=130) == sb.SBVR_E_INVALID_ARG
+    assert g(k=5) == sb.SBVR_E_UNSUPPORTED
+    assert g(P=(FAKE, 0)) == sb.SBVR_E_INVALID_ARG
+    assert g(Y=(0, FAKE)) == sb.SBVR_E_INVALID_ARG
+    assert g(X=(FAKE, FAKE + 2)) == sb.SBVR_E_ALIGNMENT
+    assert g(Cf=(FAKE + 8, FAKE)) == sb.SBVR_E_ALIGNMENT
+    # the first failing member decides: member 0 misaligned, member 1 k-independent shape error
+    assert g(O=(16, 0), P=(FAKE + 4, FAKE)) == sb.SBVR_E_ALIGNMENT
+    # host arrays shorter than n are refused by the binding
+    assert f(3, [16, 16], 256, 4, [FAKE] * 3, [FAKE] * 3, [FAKE] * 3, [FAKE] * 3) == sb.SBVR_E_INVALID_ARG
+
+
 def test_pack_validation():
     P = lambda **kw: sb.sbvr_pack(kw.get("O", 8), kw.get("I", 256), kw.get("k", 3), kw.get("pc", FAKE),
                                   kw.get("cc", FAKE), kw.get("pd", FAKE), kw.get("cd", FAKE), 0)
