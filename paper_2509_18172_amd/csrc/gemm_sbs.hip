@@ -232,14 +232,33 @@ __global__ void __launch_bounds__(512) gemm_sbs_kernel(GemvArgs a)
         P[j] = buf_load16(prs, p_lane + po);
         C[j] = buf_coef_groups<K>(crs, c_lane + co);
     };
-    // The lane's eight activations of gblock gb for every vector present;
-    // lanes past I (ragged end) and vectors >= B read zero.
+    // The lane's eight activations of gblock gb for every vector.  One gblock
+    // per wavefront: vectors >= B load the last vector again (their limbs are
+    // staged but no operand reads them), and lanes past I (ragged end) read a
+    // valid address and are zeroed -- only in a gblock that is not full, a
+    // wavefront-uniform test -- so the loads need no branches (measured: q/o
+    // at B = 2 / 4 / 8 5.0 -> 4.7, 5.9 -> 5.6, 8.1 -> 7.7 us).  Several
+    // gblocks per wavefront (the next gblock's load sits in the stream): lanes
+    // past I and vectors >= B load nothing and read zero, which measured faster
+    // there (8B down at B = 2 11.5 against 12.1 us, 70B down 32.2 against 34.0).
     auto load_x = [&](uint4 *X, int gb) {
         const int e = gb * (GB * GROUP) + lane * 8;
-        const bool in = e < a.I;
+        if constexpr (MULTI) {
+            const bool in = e < a.I;
 #pragma unroll
-        for (int b = 0; b < NB; ++b)
-            X[b] = (in && b < B) ? *(const uint4 *)(a.x + (size_t)b * a.I + e) : make_uint4(0u, 0u, 0u, 0u);
+            for (int b = 0; b < NB; ++b)
+                X[b] = (in && b < B) ? *(const uint4 *)(a.x + (size_t)b * a.I + e) : make_uint4(0u, 0u, 0u, 0u);
+        } else {
+            const int ec = min(e, a.I - 8);
+#pragma unroll
+            for (int b = 0; b < NB; ++b)
+                X[b] = *(const uint4 *)(a.x + (size_t)min(b, B - 1) * a.I + ec);
+            if ((gb + 1) * (GB * GROUP) > a.I) {
+#pragma unroll
+                for (int b = 0; b < NB; ++b)
+                    X[b] = e < a.I ? X[b] : make_uint4(0u, 0u, 0u, 0u);
+            }
+        }
     };
 
     uint4 Xc[NB];
