@@ -117,7 +117,9 @@ def test_decode_step_graph_against_oracle(sb):
     stream, issued the way the benchmark issues its decode step
     (sbvr_gemv with preallocated outputs).  After three replays (with eager
     work between them) every output is checked against the oracle on sampled
-    rows, first and last included, and each replay must give the same bits."""
+    rows, first and last included, and each replay must give the same bits.
+    The same GEMVs captured as grouped launches (q|k|v and gate|up of each
+    layer in one launch) must reproduce those bits."""
     stream = torch.cuda.Stream()
     calls, refs = [], []
     for layer in range(2):
@@ -168,3 +170,27 @@ def test_decode_step_graph_against_oracle(sb):
         worst = max(worst, e)
         assert e <= TOL, (what, e)
     log(f"decode graph: {len(calls)} GEMVs in one graph, 3 replays identical, worst sampled err {worst:.3e}")
+
+    # the same 21 GEMVs as the grouped decode step issues them (q|k|v and
+    # gate|up of each layer as one sbvr_gemv_grouped launch, 12 launches): the
+    # graph's outputs must be the bits checked above
+    names = list(synth.PROJ)
+    groups = [("q", "k", "v"), ("o",), ("gate", "up"), ("down",)]
+    launches = []
+    for base in (0, 7, 14):
+        for grp in groups:
+            launches.append([calls[base + names.index(n)] for n in grp])
+    g2 = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g2, stream=stream):
+        for members in launches:
+            sb.gemv_grouped([m[0] for m in members], [m[1] for m in members], outs=[m[2] for m in members],
+                            stream=stream)
+    for rep in range(2):
+        for _, _, y in calls:
+            y.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g2.replay()
+        torch.cuda.synchronize()
+        for (what, _, _), (_, _, y), want in zip(refs, calls, first):
+            assert np.array_equal(y.cpu().numpy().view(np.uint16), want), (what, rep)
+    log(f"grouped decode graph: {len(launches)} launches, the same bits on 2 replays")
