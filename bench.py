@@ -63,7 +63,10 @@ One JSON line is printed:
   llama3_70b    per projection of the Llama-3-70B shapes, same timing
   encoder       sbvr_encode (Algorithm 1 on the GPU, the 1024-entry grid) on an
                 fp32 q/o-shaped matrix: seconds and groups per second, and the
-                CPU oracle's encoder on a sample of its rows
+                CPU oracle's encoder on a sample of its rows; `cached`: the
+                same with the encoder cache of Sec. 4.2 (sbvr_encode_cached, 64
+                sets per row): time, hit rate, mean error over the exhaustive
+                search's, distinct coefficient sets with and without it
   cpu_baseline  the CPU oracle (binary64 decompress + GEMV) on layer 0's seven
                 GEMVs, bounded to ~10 s of work, in the same unit, on all host
                 threads; one_core: the same oracle on one thread over the q
@@ -1137,6 +1140,21 @@ def main():
         groups = O * (I // 128)
         encoder = {"shape": [O, I], "k": k, "groups": groups, "entries_per_group": 1024,
                    "gpu_s": round(sec, 4), "gpu_groups_per_s": round(groups / sec)}
+        # the encoder cache of Sec. 4.2 (64 sets per row): time, hit rate, the
+        # error against the exhaustive search, and the distinct coefficient
+        # sets (the indexed format's table) with and without it
+        with torch.cuda.stream(stream):
+            _, c0, m0 = sb.encode(Wd, k, want_mse=True, stream=stream)
+            _, cc, mc, hc = sb.encode_cached(Wd, k, 64, stream=stream)
+        torch.cuda.synchronize()
+        reps = [timed(lambda: sb.encode_cached(Wd, k, 64, stream=stream)) * 1e-3 for _ in range(3)]
+        sec_c = float(np.median(reps))
+        n_sets = lambda c: int(torch.unique(c.reshape(-1, k), dim=0).shape[0])
+        encoder["cached"] = {"cache_slots": 64, "gpu_s": round(sec_c, 4), "gpu_groups_per_s": round(groups / sec_c),
+                             "hit_rate": round(float(hc.float().mean()), 4),
+                             "mse_over_exhaustive": round(float(mc.mean() / m0.mean()), 4),
+                             "distinct_sets": n_sets(cc), "distinct_sets_exhaustive": n_sets(c0)}
+        del c0, m0, cc, mc, hc
         if not args.no_cpu_baseline:
             import oracle
             rows = 128

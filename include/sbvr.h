@@ -73,7 +73,7 @@ const char *sbvr_status_string(int status);
 /* Library ABI version (major * 100 + minor); 1.01 adds sbvr_decompress,
  * 1.02 sbvr_gemv_a8, 1.03 the coefficient-cache format entry points,
  * 1.04 sbvr_encode and sbvr_decompress_indexed, 1.05 sbvr_gemm_prefill,
- * 1.06 sbvr_gemv_grouped and sbvr_gemv_grouped_a8. */
+ * 1.06 sbvr_gemv_grouped and sbvr_gemv_grouped_a8, 1.07 sbvr_encode_cached. */
 int sbvr_version(void);
 
 /*
@@ -313,6 +313,36 @@ int sbvr_decompress_indexed(int O, int I, int k, int n_sets, const void *planes_
 int sbvr_encode(int O, int I, int k, const float *W, int n_ratio1, int n_ratio2, int n_scale, int n_bias,
                 int normalise, uint32_t *planes_canon, uint16_t *coeffs_canon, double *mse,
                 hipStream_t stream);
+
+#define SBVR_ENCODE_CACHE_MAX 64
+
+/*
+ * The encoder with the cache of Sec. 4.2 (last paragraph and its footnote):
+ * before the full search, a group tries the coefficient sets that the search
+ * chose for earlier groups, and keeps one if its error is below the moving
+ * average of the quantization error; groups that hit share their set with an
+ * earlier group, which also shrinks the coefficient cache of the indexed
+ * format (sbvr_pack_indexed).  Each row of W is encoded on its own, its
+ * groups in index order:
+ *   - the cache holds the coefficient sets the full search chose for the
+ *     row's last cache_slots searched groups (the oldest is replaced first;
+ *     the (fp16(mean), 0, ...) fallback is not cached);
+ *   - every held set is scored on the group with the search's MSE; the
+ *     smallest (the oldest set among equal ones) is taken, with each weight's
+ *     nearest-subset-sum pattern, if it is strictly below the mean MSE of
+ *     the row's earlier groups (binary64 sum in group order over their count);
+ *   - otherwise the group runs the search of sbvr_encode, and its set enters
+ *     the cache.
+ * The first group of a row always searches; cache_slots = 0 gives exactly
+ * sbvr_encode's output.  Arguments as sbvr_encode, plus
+ *   cache_slots  0 .. SBVR_ENCODE_CACHE_MAX (else SBVR_E_INVALID_ARG).
+ *   hits         uint8 [O][G] (output): 1 where the group took a cached set,
+ *                0 where it searched; or NULL.
+ * Rows are independent (one wavefront each), a row's groups sequential.
+ */
+int sbvr_encode_cached(int O, int I, int k, const float *W, int n_ratio1, int n_ratio2, int n_scale, int n_bias,
+                       int normalise, int cache_slots, uint32_t *planes_canon, uint16_t *coeffs_canon,
+                       double *mse, uint8_t *hits, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -89,6 +89,8 @@ def _lib():
             "oracle_encode_group": (C.c_double, [dp, C.c_int, C.c_int, P(_Params), u16p, u8p, ip]),
             "oracle_encode_matrix": (C.c_int, [C.c_int, C.c_int, C.c_int, fp, P(_Params), C.c_int,
                                                u32p, u16p, dp]),
+            "oracle_encode_matrix_cached": (C.c_int, [C.c_int, C.c_int, C.c_int, fp, P(_Params), C.c_int,
+                                                      C.c_int, u32p, u16p, dp, u8p]),
             "oracle_decompress": (None, [C.c_int, C.c_int, C.c_int, u32p, u16p, dp]),
             "oracle_gemv_dense": (None, [C.c_int, C.c_int, dp, dp, dp]),
             "oracle_sbvr_gemv": (C.c_int, [C.c_int, C.c_int, C.c_int, u32p, u16p, u16p, C.c_int,
@@ -218,6 +220,31 @@ def encode_matrix(W: np.ndarray, K: int, params: SearchParams = DEFAULT, nthread
     if rc < 0:
         raise ValueError(f"oracle_encode_matrix rejected shape {O}x{I}, K={K}")
     return (planes, coeffs, mse) if want_mse else (planes, coeffs)
+
+
+ENCODER_CACHE_MAX = 64
+
+
+def encode_matrix_cached(W: np.ndarray, K: int, slots: int, params: SearchParams = DEFAULT,
+                         nthreads: int = 0):
+    """The encoder with the cache of Sec. 4.2 (reading R14): per row, the
+    coefficient sets of its last `slots` searched groups are tried first and
+    the best one is kept when its MSE is below the mean MSE of the row's
+    earlier groups.  Returns (planes, coeffs, mse [O][G], hits uint8 [O][G])."""
+    W = np.ascontiguousarray(W, dtype=np.float32)
+    O, I = W.shape
+    G = I // GROUP
+    planes = np.zeros((O, G, K, 4), dtype=np.uint32)
+    coeffs = np.zeros((O, G, K), dtype=np.uint16)
+    mse = np.zeros((O, G))
+    hits = np.zeros((O, G), dtype=np.uint8)
+    p = params.c()
+    rc = _lib().oracle_encode_matrix_cached(O, I, K, _ptr(W, C.c_float), C.byref(p), int(slots), int(nthreads),
+                                            _ptr(planes, C.c_uint32), _ptr(coeffs, C.c_uint16),
+                                            _ptr(mse, C.c_double), _ptr(hits, C.c_uint8))
+    if rc < 0:
+        raise ValueError(f"oracle_encode_matrix_cached rejected shape {O}x{I}, K={K}, slots={slots}")
+    return planes, coeffs, mse, hits
 
 
 # --------------------------------------------------------------------------

@@ -48,6 +48,19 @@
  *       are binary32, the default floating-point type of the PyTorch and
  *       CUDA implementation Sec. 5.1 describes (binary16 activations
  *       promoted to it), with correctly rounded division.
+ *   R14 Encoder cache (Sec. 4.2, last paragraph and footnote), a separate
+ *       entry point; the plain encoder searches every group.  Scope: one
+ *       cache and one moving average per weight row, over its groups in
+ *       index order (rows are independent).  The cache holds the coefficient
+ *       sets (the evaluated (r, s, b) of Eq. 4) that the full search chose
+ *       for the row's last `slots` searched groups, oldest replaced first;
+ *       an R6 fallback adds nothing.  Before searching, every cached set is
+ *       scored on the group with Algorithm 1's MSE; the smallest (the oldest
+ *       set on ties) is used, with the bitvector assignment of Sec. 4.2, if
+ *       it is strictly below the moving average of the quantization error,
+ *       read as the mean MSE of all the row's earlier groups (cache hits
+ *       included): binary64 sum in group order over their count.  The first
+ *       group of a row always searches; slots = 0 is the plain encoder.
  */
 #include <math.h>
 #include <pthread.h>
@@ -385,6 +398,140 @@ int oracle_encode_matrix(int O, int I, int K, const float *W, const oracle_param
                         total * i / nt, total * (i + 1) / nt};
         jobs[i] = j;
         pthread_create(&th[i], NULL, encode_worker, &jobs[i]);
+    }
+    for (int i = 0; i < nt; ++i)
+        pthread_join(th[i], NULL);
+    free(th);
+    free(jobs);
+    return nt;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Encoder with the cache of Sec. 4.2 (last paragraph and its footnote;     */
+/* reading R14): before the full search, the coefficient sets the search    */
+/* chose for earlier groups are tried, and one is kept if its error is      */
+/* below the moving average of the quantization error.                      */
+/* ------------------------------------------------------------------------ */
+
+#define ORACLE_CACHE_MAX 64
+
+/* Bitvector assignment of Sec. 4.2 for a given coefficient set: every
+ * element takes the pattern of its nearest subset sum (R5). */
+static void assign_codes(const double *D, int n, const uint16_t *coeffs, int K, uint8_t *codes)
+{
+    double sums[1 << KMAX];
+    oracle_subset_sums(coeffs, K, sums);
+    for (int j = 0; j < n; ++j)
+        codes[j] = (uint8_t)oracle_nearest(sums, K, D[j]);
+}
+
+static void store_group(const uint8_t *codes, const uint16_t *c, int K, uint32_t *pl, uint16_t *cf)
+{
+    memset(pl, 0, sizeof(uint32_t) * (size_t)K * 4);
+    for (int j = 0; j < GROUP; ++j)
+        for (int i = 0; i < K; ++i)
+            if ((codes[j] >> i) & 1)
+                pl[i * 4 + j / 32] |= 1u << (j % 32);
+    memcpy(cf, c, sizeof(uint16_t) * (size_t)K);
+}
+
+/* One row's G groups in index order.  hit_out[g] = 1 where the group took a
+ * cached set, 0 where it ran Algorithm 1. */
+static void encode_row_cached(const float *Wrow, int I, int K, const oracle_params *p, int slots,
+                              uint32_t *planes, uint16_t *coeffs, double *mse_out, uint8_t *hit_out)
+{
+    int G = I / GROUP;
+    uint16_t cache[ORACLE_CACHE_MAX][KMAX];
+    int n_cached = 0; /* sets held, at most slots */
+    long n_ins = 0;   /* sets inserted so far; the next one replaces slot n_ins % slots */
+    double mse_sum = 0.0;
+    double D[GROUP];
+    uint8_t codes[GROUP];
+    for (int g = 0; g < G; ++g) {
+        for (int j = 0; j < GROUP; ++j)
+            D[j] = (double)Wrow[(long)g * GROUP + j];
+        uint16_t c[KMAX];
+        double mse = 0.0;
+        int hit = 0;
+        if (g > 0 && n_cached > 0) {
+            double avg = mse_sum / (double)g; /* mean error of the row's earlier groups */
+            double best = INFINITY;
+            int best_slot = -1;
+            for (int a = 0; a < n_cached; ++a) { /* oldest first: ties keep the older set */
+                int slot = (int)((n_ins - n_cached + a) % slots);
+                double m = oracle_entry_mse(D, GROUP, cache[slot], K);
+                if (m < best) {
+                    best = m;
+                    best_slot = slot;
+                }
+            }
+            if (best < avg) {
+                hit = 1;
+                mse = best;
+                memcpy(c, cache[best_slot], sizeof(uint16_t) * (size_t)K);
+                assign_codes(D, GROUP, c, K, codes);
+            }
+        }
+        if (!hit) {
+            int entry = -1;
+            mse = oracle_encode_group(D, GROUP, K, p, c, codes, &entry);
+            if (entry >= 0 && slots > 0) { /* R6 fallbacks are not entries: not cached */
+                memcpy(cache[n_ins % slots], c, sizeof(uint16_t) * (size_t)K);
+                ++n_ins;
+                if (n_cached < slots)
+                    ++n_cached;
+            }
+        }
+        store_group(codes, c, K, planes + (long)g * K * 4, coeffs + (long)g * K);
+        if (mse_out)
+            mse_out[g] = mse;
+        if (hit_out)
+            hit_out[g] = (uint8_t)hit;
+        mse_sum += mse;
+    }
+}
+
+typedef struct {
+    int I, K, slots;
+    const float *W;
+    const oracle_params *p;
+    uint32_t *planes;
+    uint16_t *coeffs;
+    double *mse;
+    uint8_t *hits;
+    long begin, end; /* row range */
+} cached_job;
+
+static void *encode_cached_worker(void *arg)
+{
+    cached_job *jb = (cached_job *)arg;
+    long G = jb->I / GROUP;
+    for (long o = jb->begin; o < jb->end; ++o)
+        encode_row_cached(jb->W + o * (long)jb->I, jb->I, jb->K, jb->p, jb->slots,
+                          jb->planes + o * G * jb->K * 4, jb->coeffs + o * G * jb->K,
+                          jb->mse ? jb->mse + o * G : NULL, jb->hits ? jb->hits + o * G : NULL);
+    return NULL;
+}
+
+/* Whole matrix, rows in parallel (each row's groups in order).  slots = 0
+ * gives the plain encoder's result.  Returns the thread count, -1 on a bad
+ * shape or slot count. */
+int oracle_encode_matrix_cached(int O, int I, int K, const float *W, const oracle_params *p, int slots,
+                                int nthreads, uint32_t *planes, uint16_t *coeffs, double *mse_out,
+                                uint8_t *hit_out)
+{
+    if (O < 1 || I < GROUP || I % GROUP || K < 1 || K > KMAX || slots < 0 || slots > ORACLE_CACHE_MAX)
+        return -1;
+    int nt = resolve_threads(nthreads);
+    if (nt > O)
+        nt = O;
+    pthread_t *th = (pthread_t *)malloc(sizeof(pthread_t) * (size_t)nt);
+    cached_job *jobs = (cached_job *)malloc(sizeof(cached_job) * (size_t)nt);
+    for (int i = 0; i < nt; ++i) {
+        cached_job j = {I, K, slots, W, p, planes, coeffs, mse_out, hit_out,
+                        (long)O * i / nt, (long)O * (i + 1) / nt};
+        jobs[i] = j;
+        pthread_create(&th[i], NULL, encode_cached_worker, &jobs[i]);
     }
     for (int i = 0; i < nt; ++i)
         pthread_join(th[i], NULL);

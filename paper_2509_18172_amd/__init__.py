@@ -32,6 +32,7 @@ EXPORTED = (
     "sbvr_decompress", "sbvr_gemv_a8", "sbvr_packed_index_bytes", "sbvr_packed_table_bytes",
     "sbvr_pack_indexed", "sbvr_unpack_indexed", "sbvr_gemv_indexed", "sbvr_gemv_indexed_a8", "sbvr_encode",
     "sbvr_decompress_indexed", "sbvr_gemm_prefill", "sbvr_gemv_grouped", "sbvr_gemv_grouped_a8",
+    "sbvr_encode_cached",
 )
 
 
@@ -75,6 +76,7 @@ def _load():
         "sbvr_gemv_indexed": (i32, [i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, sz, vp]),
         "sbvr_gemv_indexed_a8": (i32, [i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, sz, vp]),
         "sbvr_encode": (i32, [i32, i32, i32, vp, i32, i32, i32, i32, i32, vp, vp, vp, vp]),
+        "sbvr_encode_cached": (i32, [i32, i32, i32, vp, i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp]),
         "sbvr_decompress_indexed": (i32, [i32, i32, i32, i32, vp, vp, vp, vp, vp]),
         "sbvr_gemm_prefill": (i32, [i32, i32, i32, vp, vp, vp, vp, i32, vp]),
         "sbvr_gemv_grouped": (i32, [i32, vp, i32, i32, vp, vp, vp, vp, vp, sz, vp]),
@@ -137,6 +139,7 @@ def sbvr_gemv_a8(O, I, k, planes_dev, coeffs_dev, x, y, workspace=None, ws_bytes
 
 
 GEMV_GROUP_MAX = 4
+ENCODE_CACHE_MAX = 64
 
 
 def _grouped(fn, n, O, I, k, planes_dev, coeffs_dev, x, y, workspace, ws_bytes, stream) -> int:
@@ -197,6 +200,12 @@ def sbvr_encode(O, I, k, W, n_ratio1, n_ratio2, n_scale, n_bias, normalise, plan
                 mse=None, stream=0) -> int:
     return _lib.sbvr_encode(O, I, k, W, n_ratio1, n_ratio2, n_scale, n_bias, normalise, planes_canon,
                             coeffs_canon, mse, stream)
+
+
+def sbvr_encode_cached(O, I, k, W, n_ratio1, n_ratio2, n_scale, n_bias, normalise, cache_slots, planes_canon,
+                       coeffs_canon, mse=None, hits=None, stream=0) -> int:
+    return _lib.sbvr_encode_cached(O, I, k, W, n_ratio1, n_ratio2, n_scale, n_bias, normalise, cache_slots,
+                                   planes_canon, coeffs_canon, mse, hits, stream)
 
 
 def sbvr_decompress(O, I, k, planes_dev, coeffs_dev, W, stream=0) -> int:
@@ -426,6 +435,25 @@ def encode(W, k: int, n_ratio1: int = 8, n_ratio2: int = 8, n_scale: int = 16, n
     _check(sbvr_encode(O, I, k, W.data_ptr(), n_ratio1, n_ratio2, n_scale, n_bias, int(normalise), planes.data_ptr(),
                        coeffs.data_ptr(), mse.data_ptr() if want_mse else None, _stream(stream)), "sbvr_encode")
     return (planes, coeffs, mse) if want_mse else (planes, coeffs)
+
+
+def encode_cached(W, k: int, cache_slots: int = ENCODE_CACHE_MAX, n_ratio1: int = 8, n_ratio2: int = 8,
+                  n_scale: int = 16, n_bias: int = 4, normalise: bool = True, stream=None):
+    """encode() with the encoder cache of Sec. 4.2 (per row, the sets of its
+    last cache_slots searched groups tried first): returns (planes, coeffs,
+    mse float64 [O][G], hits uint8 [O][G]) device tensors."""
+    torch = _torch()
+    assert W.dtype == torch.float32 and W.is_contiguous() and W.dim() == 2 and W.is_cuda
+    O, I = W.shape
+    G = I // GROUP
+    planes = torch.empty((O, G, k, 4), dtype=torch.int32, device=W.device)
+    coeffs = torch.empty((O, G, k), dtype=torch.int16, device=W.device)
+    mse = torch.empty((O, G), dtype=torch.float64, device=W.device)
+    hits = torch.empty((O, G), dtype=torch.uint8, device=W.device)
+    _check(sbvr_encode_cached(O, I, k, W.data_ptr(), n_ratio1, n_ratio2, n_scale, n_bias, int(normalise),
+                              int(cache_slots), planes.data_ptr(), coeffs.data_ptr(), mse.data_ptr(),
+                              hits.data_ptr(), _stream(stream)), "sbvr_encode_cached")
+    return planes, coeffs, mse, hits
 
 
 def gemm_prefill(W: PackedWeight, X, out=None, stream=None):

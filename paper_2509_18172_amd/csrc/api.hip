@@ -136,7 +136,7 @@ const char *sbvr_status_string(int status)
     }
 }
 
-int sbvr_version(void) { return 106; }
+int sbvr_version(void) { return 107; }
 
 size_t sbvr_packed_plane_bytes(int O, int I, int k)
 {
@@ -284,8 +284,9 @@ int sbvr_gemv_indexed_a8(int O, int I, int k, int n_sets, const void *planes_dev
                           true, stream);
 }
 
-int sbvr_encode(int O, int I, int k, const float *W, int n_ratio1, int n_ratio2, int n_scale, int n_bias,
-                int normalise, uint32_t *planes_canon, uint16_t *coeffs_canon, double *mse, hipStream_t stream)
+namespace {
+int check_encode(int O, int I, int k, const float *W, int n_ratio1, int n_ratio2, int n_scale, int n_bias,
+                 int normalise, uint32_t *planes_canon, uint16_t *coeffs_canon, double *mse)
 {
     int st = check_shape(O, I, k);
     if (st != SBVR_OK)
@@ -298,8 +299,33 @@ int sbvr_encode(int O, int I, int k, const float *W, int n_ratio1, int n_ratio2,
         return SBVR_E_INVALID_ARG;
     if (!aligned(W, 4) || !aligned(planes_canon, 16) || !aligned(coeffs_canon, 2) || (mse && !aligned(mse, 8)))
         return SBVR_E_ALIGNMENT;
+    return SBVR_OK;
+}
+}  // namespace
+
+int sbvr_encode(int O, int I, int k, const float *W, int n_ratio1, int n_ratio2, int n_scale, int n_bias,
+                int normalise, uint32_t *planes_canon, uint16_t *coeffs_canon, double *mse, hipStream_t stream)
+{
+    int st = check_encode(O, I, k, W, n_ratio1, n_ratio2, n_scale, n_bias, normalise, planes_canon, coeffs_canon,
+                          mse);
+    if (st != SBVR_OK)
+        return st;
     return launch_encode(O, I, k, W, n_ratio1, n_ratio2, n_scale, n_bias, normalise, planes_canon, coeffs_canon,
                          mse, stream);
+}
+
+int sbvr_encode_cached(int O, int I, int k, const float *W, int n_ratio1, int n_ratio2, int n_scale, int n_bias,
+                       int normalise, int cache_slots, uint32_t *planes_canon, uint16_t *coeffs_canon, double *mse,
+                       uint8_t *hits, hipStream_t stream)
+{
+    int st = check_encode(O, I, k, W, n_ratio1, n_ratio2, n_scale, n_bias, normalise, planes_canon, coeffs_canon,
+                          mse);
+    if (st != SBVR_OK)
+        return st;
+    if (cache_slots < 0 || cache_slots > SBVR_ENCODE_CACHE_MAX)
+        return SBVR_E_INVALID_ARG;
+    return launch_encode_cached(O, I, k, W, n_ratio1, n_ratio2, n_scale, n_bias, normalise, cache_slots,
+                                planes_canon, coeffs_canon, mse, hits, stream);
 }
 
 int sbvr_decompress(int O, int I, int k, const void *planes_dev, const void *coeffs_dev, uint16_t *W,

@@ -38,6 +38,8 @@
 #include "f16_round.h"
 #include "launch.h"
 
+#include <climits>
+
 namespace sbvr {
 
 constexpr int ENC_THREADS = 64;  // one wavefront per group
@@ -154,24 +156,37 @@ struct EncodeArgs {
     int n_ratio1, n_ratio2, n_scale, n_bias, normalise;
 };
 
+// A wavefront's LDS for one group: the group's values (read as broadcasts)
+// and the search's exchange slots.
+struct EncodeLds {
+    double D[GROUP];
+    double best_mse_l[ENC_THREADS];
+    int best_e_l[ENC_THREADS];
+    double q_pair[2];
+};
+
 template <int K>
-__global__ void __launch_bounds__(ENC_THREADS) encode_kernel(EncodeArgs a)
+struct GroupChoice {
+    uint16_t c[K];
+    double mse;
+    int entry;  // index in the grid, -1 for the no-admissible-entry fallback
+};
+
+__device__ __forceinline__ int wave_min_int(int v)
 {
-    __shared__ double D[GROUP];
-    __shared__ double best_mse_l[ENC_THREADS];
-    __shared__ int best_e_l[ENC_THREADS];
-    __shared__ double q_pair[2];
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1)
+        v = min(v, __shfl_xor(v, off));
+    return v;
+}
+
+// Algorithm 1 over the group in L.D (d0, d1: the lane's elements lane and
+// lane + 64).  Every lane returns the same choice.
+template <int K>
+__device__ GroupChoice<K> search_group(const EncodeArgs &a, EncodeLds &L, double d0, double d1)
+{
     const int lane = threadIdx.x;
-    const int G = a.I / GROUP;
-    const size_t grp = blockIdx.x;
-    const size_t o = grp / G, g = grp % G;
-    const float *src = a.W + o * (size_t)a.I + g * GROUP;
-
-    const double d0 = (double)src[lane], d1 = (double)src[lane + 64];
-    D[lane] = d0;
-    D[lane + 64] = d1;
-    __syncthreads();
-
+    const double *D = L.D;
     // statistics in element order (every lane, from broadcast reads)
     double mn = D[0], mx = D[0], sum = 0.0;
     for (int j = 0; j < GROUP; ++j) {
@@ -197,12 +212,12 @@ __global__ void __launch_bounds__(ENC_THREADS) encode_kernel(EncodeArgs a)
             r1 += (v < d1) || (v == d1 && j < lane + 64);
         }
         if (r0 == lo || r0 == lo + 1)
-            q_pair[r0 - lo] = d0;
+            L.q_pair[r0 - lo] = d0;
         if (r1 == lo || r1 == lo + 1)
-            q_pair[r1 - lo] = d1;
+            L.q_pair[r1 - lo] = d1;
     }
     __syncthreads();
-    const double q95 = q_pair[0] + frac * (q_pair[1] - q_pair[0]);
+    const double q95 = L.q_pair[0] + frac * (L.q_pair[1] - L.q_pair[0]);
 
     const double s_max = 1.1 * (mx - mn);
     const double s_min = 2.0 * q95;
@@ -291,37 +306,50 @@ __global__ void __launch_bounds__(ENC_THREADS) encode_kernel(EncodeArgs a)
         }
         shared_best = wave_min_f64(fmin(shared_best, best_mse));
     }
-    best_mse_l[lane] = best_mse;
-    best_e_l[lane] = best_e;
+    L.best_mse_l[lane] = best_mse;
+    L.best_e_l[lane] = best_e;
     __syncthreads();
     // smallest error, lowest entry index among equal errors
     double m = __builtin_inf();
     int be = -1;
     for (int l = 0; l < ENC_THREADS; ++l) {
-        const int e = best_e_l[l];
-        const double v = best_mse_l[l];
+        const int e = L.best_e_l[l];
+        const double v = L.best_mse_l[l];
         if (e >= 0 && (be < 0 || v < m || (v == m && e < be))) {
             m = v;
             be = e;
         }
     }
 
-    uint16_t c[K];
+    GroupChoice<K> out;
     if (be >= 0) {
         double r, s, b;
         entry_rsb(be, r, s, b);
-        entry_coeffs<K>(r, s, b, a.normalise != 0, c);
+        entry_coeffs<K>(r, s, b, a.normalise != 0, out.c);
     } else {  // no admissible entry
-        c[0] = f64_to_f16_rne(avg);
+        out.c[0] = f64_to_f16_rne(avg);
 #pragma unroll
         for (int i = 1; i < K; ++i)
-            c[i] = 0;
+            out.c[i] = 0;
+        double sums[1 << K];
+        subset_sums<K>(out.c, sums);
+        m = entry_mse<K>(D, sums);
     }
+    out.mse = m;
+    out.entry = be;
+    return out;
+}
+
+// The bitvector assignment for coefficient set c (each of the lane's two
+// elements takes the pattern of its nearest subset sum) and the group's
+// stores: plane i by lane i, the coefficients, the MSE by lane 0.
+template <int K>
+__device__ __forceinline__ void store_group(const EncodeArgs &a, size_t grp, const uint16_t *c, double d0,
+                                            double d1, double mse)
+{
+    const int lane = threadIdx.x;
     double sums[1 << K];
     subset_sums<K>(c, sums);
-    if (be < 0)
-        m = entry_mse<K>(D, sums);
-
     double dd;
     const int p0 = nearest<K>(sums, d0, dd), p1 = nearest<K>(sums, d1, dd);
 #pragma unroll
@@ -334,7 +362,104 @@ __global__ void __launch_bounds__(ENC_THREADS) encode_kernel(EncodeArgs a)
         }
     }
     if (lane == 0 && a.mse)
-        a.mse[grp] = m;
+        a.mse[grp] = mse;
+}
+
+template <int K>
+__global__ void __launch_bounds__(ENC_THREADS) encode_kernel(EncodeArgs a)
+{
+    __shared__ EncodeLds L;
+    const int lane = threadIdx.x;
+    const int G = a.I / GROUP;
+    const size_t grp = blockIdx.x;
+    const size_t o = grp / G, g = grp % G;
+    const float *src = a.W + o * (size_t)a.I + g * GROUP;
+
+    const double d0 = (double)src[lane], d1 = (double)src[lane + 64];
+    L.D[lane] = d0;
+    L.D[lane + 64] = d1;
+    __syncthreads();
+    const GroupChoice<K> r = search_group<K>(a, L, d0, d1);
+    store_group<K>(a, grp, r.c, d0, d1, r.mse);
+}
+
+// The encoder with the cache of Sec. 4.2 (last paragraph and its footnote):
+// one wavefront per row, its groups in index order.  Lane s holds cache slot
+// s (a coefficient set the full search chose for one of the row's last
+// `slots` searched groups, and that group's insertion number; the oldest set
+// is replaced first).  For each group every held set is scored with the
+// search's MSE (one set per lane, the elements in order); the smallest --
+// the oldest among equal ones -- is taken if it is strictly below the mean
+// MSE of the row's earlier groups (binary64 sum in group order over their
+// count), otherwise the full search runs and its choice enters the cache
+// (the no-admissible-entry fallback does not).  The first group of a row
+// always searches; with slots = 0 the result is the plain encoder's.
+template <int K>
+__global__ void __launch_bounds__(ENC_THREADS) encode_cached_kernel(EncodeArgs a, int slots, uint8_t *hits)
+{
+    __shared__ EncodeLds L;
+    const int lane = threadIdx.x;
+    const int G = a.I / GROUP;
+    const size_t o = blockIdx.x;
+    uint16_t cs[K];  // this lane's cached set
+#pragma unroll
+    for (int i = 0; i < K; ++i)
+        cs[i] = 0;
+    int seq = INT_MAX;             // its insertion number
+    int n_cached = 0, n_ins = 0;   // wavefront-uniform
+    double mse_sum = 0.0;          // wavefront-uniform
+    for (int g = 0; g < G; ++g) {
+        const size_t grp = o * G + g;
+        const float *src = a.W + o * (size_t)a.I + (size_t)g * GROUP;
+        const double d0 = (double)src[lane], d1 = (double)src[lane + 64];
+        __syncthreads();  // the previous group's reads of L are done
+        L.D[lane] = d0;
+        L.D[lane + 64] = d1;
+        __syncthreads();
+        bool hit = false;
+        uint16_t c[K];
+        double mse = 0.0;
+        if (g > 0 && n_cached > 0) {
+            const double avg = mse_sum / (double)g;
+            double m = __builtin_inf();
+            if (lane < n_cached) {
+                double sums[1 << K];
+                subset_sums<K>(cs, sums);
+                m = entry_mse<K>(L.D, sums);
+            }
+            const double best = wave_min_f64(m);
+            if (best < avg) {  // wavefront-uniform
+                const int oldest = wave_min_int(lane < n_cached && m == best ? seq : INT_MAX);
+                const int wl = __ffsll((unsigned long long)__ballot(lane < n_cached && seq == oldest)) - 1;
+#pragma unroll
+                for (int i = 0; i < K; ++i)
+                    c[i] = (uint16_t)__shfl((int)cs[i], wl);
+                mse = best;
+                hit = true;
+            }
+        }
+        if (!hit) {
+            const GroupChoice<K> r = search_group<K>(a, L, d0, d1);
+#pragma unroll
+            for (int i = 0; i < K; ++i)
+                c[i] = r.c[i];
+            mse = r.mse;
+            if (r.entry >= 0 && slots > 0) {
+                if (lane == n_ins % slots) {
+#pragma unroll
+                    for (int i = 0; i < K; ++i)
+                        cs[i] = c[i];
+                    seq = n_ins;
+                }
+                ++n_ins;
+                n_cached = min(n_cached + 1, slots);
+            }
+        }
+        store_group<K>(a, grp, c, d0, d1, mse);
+        if (lane == 0 && hits)
+            hits[grp] = hit ? 1 : 0;
+        mse_sum += mse;
+    }
 }
 
 int launch_encode(int O, int I, int k, const float *W, int n_ratio1, int n_ratio2, int n_scale, int n_bias,
@@ -348,6 +473,19 @@ int launch_encode(int O, int I, int k, const float *W, int n_ratio1, int n_ratio
                               : (const void *)encode_kernel<1>;
     void *args[] = {&a};
     return launch_kernel(fn, dim3((unsigned)groups), dim3(ENC_THREADS), 0, stream, args);
+}
+
+int launch_encode_cached(int O, int I, int k, const float *W, int n_ratio1, int n_ratio2, int n_scale, int n_bias,
+                         int normalise, int slots, uint32_t *planes, uint16_t *coeffs, double *mse, uint8_t *hits,
+                         hipStream_t stream)
+{
+    EncodeArgs a = {W, planes, coeffs, mse, O, I, n_ratio1, n_ratio2, n_scale, n_bias, normalise};
+    const void *fn = k == 4   ? (const void *)encode_cached_kernel<4>
+                     : k == 3 ? (const void *)encode_cached_kernel<3>
+                     : k == 2 ? (const void *)encode_cached_kernel<2>
+                              : (const void *)encode_cached_kernel<1>;
+    void *args[] = {&a, &slots, &hits};
+    return launch_kernel(fn, dim3((unsigned)O), dim3(ENC_THREADS), 0, stream, args);
 }
 
 }  // namespace sbvr

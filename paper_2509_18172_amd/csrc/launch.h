@@ -54,6 +54,9 @@ int launch_unpack_indexed(const Dims &d, int n_sets, const void *planes_dev, con
 int launch_decompress(const Dims &d, const WeightRef &w, uint16_t *W, hipStream_t stream);
 int launch_encode(int O, int I, int k, const float *W, int n_ratio1, int n_ratio2, int n_scale, int n_bias,
                   int normalise, uint32_t *planes, uint16_t *coeffs, double *mse, hipStream_t stream);
+int launch_encode_cached(int O, int I, int k, const float *W, int n_ratio1, int n_ratio2, int n_scale, int n_bias,
+                         int normalise, int slots, uint32_t *planes, uint16_t *coeffs, double *mse, uint8_t *hits,
+                         hipStream_t stream);
 int launch_prefill(const Dims &d, const void *planes_dev, const void *coeffs_dev, const uint16_t *X, uint16_t *Y,
                    int T, hipStream_t stream);
 int launch_gemm_sbs(const Dims &d, const void *planes_dev, const void *coeffs_dev,

@@ -200,6 +200,14 @@ def test_new_entry_points_validation():
     assert enc(W=None) == sb.SBVR_E_INVALID_ARG
     assert enc(W=FAKE + 2) == sb.SBVR_E_ALIGNMENT
     assert enc(m=FAKE + 4) == sb.SBVR_E_ALIGNMENT
+    encc = lambda **kw: sb.sbvr_encode_cached(4, 256, kw.get("k", 4), kw.get("W", FAKE), 8, 8, 16, 4, 1,
+                                              kw.get("slots", 4), FAKE, FAKE, kw.get("m", None), None, 0)
+    assert encc(slots=65) == sb.SBVR_E_INVALID_ARG
+    assert encc(slots=-1) == sb.SBVR_E_INVALID_ARG
+    assert encc(k=9) == sb.SBVR_E_UNSUPPORTED
+    assert encc(W=None) == sb.SBVR_E_INVALID_ARG
+    assert encc(W=FAKE + 2) == sb.SBVR_E_ALIGNMENT
+    assert encc(m=FAKE + 4) == sb.SBVR_E_ALIGNMENT
 
 
 def test_read_probe_loads_and_rejects_bad_arguments():

@@ -133,3 +133,110 @@ def test_encoder_bit_exact_random_shapes_and_grids(sb, O, G, k, grid, normalise,
     W = synth.weights(O, 128 * G, 2.0 ** sigma_exp, seed=O * 1009 + G * 31 + k + sigma_exp + 64,
                       outlier_frac=0.01 if outliers else 0.0)
     assert_same(sb, W, k, params, what=f"{params} sigma=2^{sigma_exp}")
+
+
+# ---------------------------------------------------------------------------
+# The encoder with the cache of Sec. 4.2 (sbvr_encode_cached) against the
+# oracle's cached encoder, bit for bit: planes, coefficients, MSE and the
+# hit flags.
+# ---------------------------------------------------------------------------
+
+def gpu_encode_cached(sb, W, k, slots, params=oracle.DEFAULT):
+    Wd = torch.from_numpy(np.ascontiguousarray(W, dtype=np.float32)).cuda()
+    planes, coeffs, mse, hits = sb.encode_cached(Wd, k, slots, params.n_ratio1, params.n_ratio2, params.n_scale,
+                                                 params.n_bias, params.normalise)
+    torch.cuda.synchronize()
+    return (planes.cpu().numpy().view(np.uint32), coeffs.cpu().numpy().view(np.uint16), mse.cpu().numpy(),
+            hits.cpu().numpy())
+
+
+def assert_same_cached(sb, W, k, slots, params=oracle.DEFAULT, what="", rows=None):
+    """rows: compare only these rows, encoded by the oracle on their own (rows
+    are independent under the cache's per-row scope)."""
+    p, c, m, h = gpu_encode_cached(sb, W, k, slots, params)
+    if rows is not None:
+        p, c, m, h = p[rows], c[rows], m[rows], h[rows]
+        W = W[rows]
+    p_ref, c_ref, m_ref, h_ref = oracle.encode_matrix_cached(W, k, slots, params)
+    bad = np.flatnonzero((c != c_ref).any(axis=-1).reshape(-1) | (p != p_ref).any(axis=(-1, -2)).reshape(-1))
+    assert bad.size == 0, (what, "groups differ", bad[:8])
+    assert np.array_equal(m.view(np.uint64), m_ref.view(np.uint64)), what
+    assert np.array_equal(h, h_ref), what
+    print(f"encode_cached {what} {W.shape} k={k} slots={slots}: identical, hit rate {h.mean():.3f}", flush=True)
+    return h
+
+
+@pytest.mark.parametrize("k,slots", [(4, 64), (4, 3), (3, 1), (2, 8), (1, 64), (4, 17)])
+def test_cached_encoder_bit_exact(sb, k, slots):
+    W = synth.weights(24, 2048, 0.02, seed=synth.seed_for(2, k, slots), outlier_frac=0.001)
+    h = assert_same_cached(sb, W, k, slots, what="N(0, 0.02^2) + outliers")
+    assert h.any()
+
+
+def test_cached_encoder_zero_slots_is_sbvr_encode(sb):
+    W = synth.weights(16, 1024, 0.02, seed=17, outlier_frac=0.001)
+    p, c, m, h = gpu_encode_cached(sb, W, 4, 0)
+    p0, c0, m0 = gpu_encode(sb, W, 4)
+    assert np.array_equal(p, p0) and np.array_equal(c, c0) and np.array_equal(m.view(np.uint64), m0.view(np.uint64))
+    assert not h.any()
+
+
+def test_cached_encoder_degenerate_rows_and_grids(sb):
+    rng = np.random.default_rng(3)
+    groups = [np.zeros(128), np.full(128, 0.0125), rng.standard_normal(128) * 0.02,
+              rng.standard_normal(128) * 1e30, rng.standard_normal(128) * 0.02, np.zeros(128),
+              rng.standard_normal(128) * 0.02, np.full(128, -3.5), np.tile(rng.standard_normal(64) * 0.02, 2)]
+    W = np.stack([np.concatenate(groups), np.concatenate(groups[::-1])]).astype(np.float32)
+    for k in (1, 2, 4):
+        for slots in (1, 4, 64):
+            assert_same_cached(sb, W, k, slots, what="degenerate groups")
+    W2 = synth.weights(6, 1536, 0.015, seed=29)
+    for params in (oracle.SearchParams(normalise=False), oracle.SearchParams(2, 2, 3, 1),
+                   oracle.SearchParams(5, 4, 13, 3)):
+        assert_same_cached(sb, W2, 3, 5, params, what=str(params))
+    # three identical groups: no hit (the cached set scores exactly the mean)
+    D = synth.weights(1, 128, 0.02, seed=5)[0]
+    h = assert_same_cached(sb, np.tile(D, 3)[None, :].astype(np.float32), 4, 8, what="identical groups")
+    assert not h.any()
+
+
+def test_cached_encoder_full_size_and_indexed_gemv(sb):
+    """Llama-3-8B q/o (4096 x 4096) and gate (14336 x 4096) weights, N(0, 0.02^2)
+    with 0.1 % outliers, encoded whole on the GPU: sampled rows (first and
+    last included) bit-identical to the oracle's cached encoder on those rows.
+    The q/o encoding then goes, as the paper intends, into the coefficient
+    cache of the indexed format (distinct sets <= searched groups) and through
+    sbvr_gemv_indexed against the oracle's exact GEMV."""
+    rng = np.random.default_rng(44)
+    for O, I in ((4096, 4096), (14336, 4096)):
+        W = synth.weights(O, I, 0.02, seed=synth.seed_for(1, 0, O), outlier_frac=0.001)
+        rows = np.unique(np.r_[0, O - 1, rng.integers(0, O, 22)])
+        assert_same_cached(sb, W, 4, 64, rows=rows, what="full-size sample")
+    O, I = 4096, 4096
+    W = synth.weights(O, I, 0.02, seed=synth.seed_for(1, 0, O), outlier_frac=0.001)
+    p, c, m, h = gpu_encode_cached(sb, W, 4, 64)
+    index, table = oracle.coefficient_cache(c)
+    misses = int((h == 0).sum())
+    print(f"q/o: hit rate {h.mean():.3f}, {table.shape[0]} distinct sets for {misses} searched groups", flush=True)
+    assert table.shape[0] <= misses
+    Wi = sb.pack_indexed(torch.from_numpy(p.view(np.int32)).cuda(), torch.from_numpy(index.view(np.int16)).cuda(),
+                         torch.from_numpy(table.view(np.int16)).cuda())
+    x = synth.activations(I, seed=61)
+    y = sb.gemv_indexed(Wi, torch.from_numpy(x).cuda()).cpu().numpy().astype(np.float64)
+    rows = np.unique(np.r_[0, O - 1, rng.integers(0, O, 96)])
+    y_ref = oracle.sbvr_gemv_indexed(p, index, table, x, rows=rows)
+    assert np.abs(y[rows] - y_ref).max() / np.abs(y_ref).max() <= 1e-3
+
+
+def test_cached_encoder_error_paths(sb):
+    W = torch.zeros((4, 256), dtype=torch.float32, device="cuda")
+    planes = torch.empty((4, 2, 4, 4), dtype=torch.int32, device="cuda")
+    coeffs = torch.empty((4, 2, 4), dtype=torch.int16, device="cuda")
+    p, c, w = planes.data_ptr(), coeffs.data_ptr(), W.data_ptr()
+    f = sb.sbvr_encode_cached
+    assert f(4, 256, 4, w, 8, 8, 16, 4, 1, 64, p, c, None, None, 0) == 0
+    assert f(4, 256, 4, w, 8, 8, 16, 4, 1, 65, p, c, None, None, 0) == sb.SBVR_E_INVALID_ARG
+    assert f(4, 256, 4, w, 8, 8, 16, 4, 1, -1, p, c, None, None, 0) == sb.SBVR_E_INVALID_ARG
+    assert f(4, 256, 5, w, 8, 8, 16, 4, 1, 4, p, c, None, None, 0) == sb.SBVR_E_UNSUPPORTED
+    assert f(4, 256, 4, w + 2, 8, 8, 16, 4, 1, 4, p, c, None, None, 0) == sb.SBVR_E_ALIGNMENT
+    torch.cuda.synchronize()
