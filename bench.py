@@ -113,7 +113,7 @@ sys.path.insert(0, ROOT)
 
 PEAK_GBPS = 8000.0
 PROJ_ORDER = ("q", "k", "v", "o", "gate", "up", "down")
-PREFILL_TOKENS = (1, 16, 64, 128, 512)  # prompt lengths of the fused prefill GEMM timings
+PREFILL_TOKENS = (1, 16, 64, 128, 256, 512)  # prompt lengths of the fused prefill GEMM timings
 TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "hbm_traffic_llama3-8b_k4.md")
 ROCPROF_RECORD = "sbvr_gemv_llama3-8b_headline_kernel_stats.md"
 CALIB_BYTES = 256 << 20
@@ -416,7 +416,7 @@ def prefill_summary(trace_csv: str) -> str:
         dec, lib, fus = segs[6 * i + 3: 6 * i + 6]
         d = np.mean([x for x, n in dec if "decompress_kernel" in n]) / 1e3
         lb = sum(x for x, n in lib if "sbvr::" not in n) / PREFILL_PROBE_CALLS / 1e3
-        fu = np.mean([x for x, n in fus if "prefill_kernel" in n]) / 1e3
+        fu = np.mean([x for x, n in fus if "prefill_kernel" in n or "prefill_long_kernel" in n]) / 1e3
         lines.append(f"| {label} | {T} | {d:.1f} | {lb:.1f} | {d + lb:.1f} | {fu:.1f} |")
         rec[f"{label} T={T}"] = {"decompress_us": round(d, 2), "library_us": round(lb, 2), "fused_us": round(fu, 2)}
     lines += ["", "prefill-record: " + json.dumps(rec, sort_keys=True)]

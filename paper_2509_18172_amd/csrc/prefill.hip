@@ -292,6 +292,294 @@ __global__ void __launch_bounds__(64 * PF_WAVES) prefill_kernel(PrefillArgs a)
         }
 }
 
+// ---------------------------------------------------------------------------
+// Long prompts: v_mfma_f32_32x32x16_f16.  The kernel above reads a 16-token
+// activation operand from LDS for every 16 x 16 product, and each wavefront
+// decodes its weights for at most 128 tokens; past about a hundred tokens the
+// LDS reads and the decoding bound it.  Here a wavefront owns RT column tiles
+// of 32 weight rows and TT token tiles of 32: each activation operand read
+// meets 32 RT rows and each decoded weight 32 TT tokens.  A workgroup of
+// PL_WAVES wavefronts holds R = PL_WAVES / S row groups times S K-slices
+// (their partial sums added through LDS in a fixed order, as above).  Per
+// group a wavefront builds the subset-sum tables of its 32 RT rows (lane: row
+// lane % 32, half of the subsets), then per 16-element step each lane looks
+// up the eight elements 8 (lane / 32) .. +7 of each of its rows (the device
+// bit layout holds them as bits v, v + 4, .., v + 28 of one plane word, v =
+// 2 (step % 2) + lane / 32) and issues RT x TT instructions (operand A: 32
+// tokens x 16 values, lane: token lane % 32, values 8 (lane / 32) ..; operand
+// B: the decoded weights, lane: row lane % 32, the same values).  Result
+// register j of a lane holds token 8 (j / 4) + 4 (lane / 32) + j % 4 of the
+// tile, row lane % 32.
+// ---------------------------------------------------------------------------
+constexpr int PL_WAVES = 8;
+// activation chunks (16 bytes) per thread and group: the launcher keeps
+// S TT <= PL_XPT (a K-slice's 512 / S threads load 512 TT chunks)
+constexpr int PL_XPT = 4;
+// instructions per step and wavefront (RT TT) at most: the RT TT x 16
+// accumulators of 2 x 2 and 1 x 4 fit the 256 registers of a wavefront at two
+// per SIMD; 2 x 4 would spill
+constexpr int PL_TILE_MAX = 4;
+
+typedef float v16f __attribute__((ext_vector_type(16)));
+
+__host__ __device__ constexpr int pl_xtile(int tt) { return 32 * tt * PF_XROW; }
+
+template <int K, int RT, int TT>
+__global__ void __launch_bounds__(64 * PL_WAVES) prefill_long_kernel(PrefillArgs a)
+{
+    constexpr int TR = tile_rows(K), NSUB = 1 << K;
+    constexpr int LROW = NSUB + PF_LUT_PAD;
+    constexpr int LUT_B = 32 * RT * LROW * 2;  // a wavefront's tables
+    constexpr int XT = pl_xtile(TT);
+    constexpr int XCH = 32 * TT * 16;
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int lane = threadIdx.x & 63, w = wave_id();
+    const int S = a.S, R = PL_WAVES / S;
+    const int ks_id = w % S, rg = w / S;  // K-slice and row group of this wavefront
+    const int n = lane & 31, kh = lane >> 5;
+    unsigned char *xbuf = smem + (size_t)ks_id * 2 * XT;
+    uint16_t *lut = (uint16_t *)(smem + (size_t)S * 2 * XT + w * LUT_B);
+    const int o_base = (blockIdx.x * R + rg) * 32 * RT, t_base = blockIdx.y * 32 * TT;
+    const int g0 = ks_id * a.gps;
+    const int rows_dev = a.n_tiles * TR;
+
+    v16f acc[RT][TT];
+#pragma unroll
+    for (int q = 0; q < RT; ++q)
+#pragma unroll
+        for (int tt = 0; tt < TT; ++tt)
+#pragma unroll
+            for (int e = 0; e < 16; ++e)
+                acc[q][tt][e] = 0.f;
+
+    // the lane's decode rows (row lane % 32 of each column tile)
+    int tile[RT], rr[RT];
+    bool row_ok[RT];
+#pragma unroll
+    for (int q = 0; q < RT; ++q) {
+        const int o = min(o_base + 32 * q + n, rows_dev - 1);
+        row_ok[q] = o_base + 32 * q + n < rows_dev;
+        tile[q] = o / TR;
+        rr[q] = o % TR;
+    }
+    struct GroupLoads {
+        uint4 slot[RT][K];
+        uint16_t c[RT][K];
+    };
+    auto load_group = [&](int g, GroupLoads &L) {
+        const int gb = g / GB, b = g % GB;
+#pragma unroll
+        for (int q = 0; q < RT; ++q) {
+            const size_t blk = (size_t)tile[q] * a.n_gblocks + gb;
+            const uint4 *sp = (const uint4 *)(a.planes + blk * plane_block_words(K)) + (b * TR + rr[q]) * K;
+#pragma unroll
+            for (int i = 0; i < K; ++i)
+                L.slot[q][i] = sp[i];
+            const uint16_t *cp = a.coeffs + blk * coeff_block_entries(K) + coeff_entry(K, rr[q], b, 0);
+#pragma unroll
+            for (int i = 0; i < K; ++i)
+                L.c[q][i] = cp[i];
+        }
+    };
+    // a group's activation tile, loaded by the K-slice's R wavefronts: 16
+    // consecutive threads read one token's 256 bytes (tokens past T read zero)
+    const int xthr = rg * 64 + lane, nxthr = R * 64;
+    auto load_x = [&](int g, uint4 *v) {
+#pragma unroll
+        for (int q = 0; q < PL_XPT; ++q) {
+            const int ch = xthr + q * nxthr;
+            v[q] = make_uint4(0u, 0u, 0u, 0u);
+            const int t = t_base + ch / 16;
+            if (ch < XCH && t < a.T)
+                v[q] = *(const uint4 *)(a.X + (size_t)t * a.I + (size_t)g * GROUP + (ch % 16) * 8);
+        }
+    };
+    auto store_x = [&](unsigned char *buf, const uint4 *v) {
+#pragma unroll
+        for (int q = 0; q < PL_XPT; ++q) {
+            const int ch = xthr + q * nxthr;
+            if (ch < XCH)
+                *(uint4 *)(buf + (ch / 16) * PF_XROW + (ch % 16) * 16) = v[q];
+        }
+    };
+
+    GroupLoads cur, nxt;
+    uint4 xv[PL_XPT];
+    if (g0 < a.G) {
+        load_group(g0, cur);
+        load_x(g0, xv);
+        store_x(xbuf, xv);
+    }
+    __syncthreads();
+    for (int j = 0; j < a.gps; ++j) {
+        const int g = g0 + j;
+        const bool more = j + 1 < a.gps && g + 1 < a.G;
+        if (more) {
+            load_group(g + 1, nxt);
+            load_x(g + 1, xv);  // stored after this group's products
+        }
+        if (g < a.G) {
+            // ---- subset-sum tables of the wavefront's rows for group g (lane:
+            // row lane % 32 of each column tile, subsets PER * (lane / 32) ..) ----
+            constexpr int PER = NSUB / 2, LOGPER = K - 1;
+            const int p0 = PER * kh;
+#pragma unroll
+            for (int q = 0; q < RT; ++q) {
+                uint32_t c[K];
+#pragma unroll
+                for (int i = 0; i < K; ++i)
+                    c[i] = row_ok[q] ? (uint32_t)cur.c[q][i] : 0u;
+                int emax = -30, emin = 30;
+#pragma unroll
+                for (int i = 0; i < K; ++i) {
+                    if (c[i] & 0x7fffu) {
+                        emax = max(emax, f16_exp(c[i]));
+                        emin = min(emin, f16_exp(c[i]));
+                    }
+                }
+                uint16_t *lrow = lut + (32 * q + n) * LROW + p0;
+                // binary32 sums (exact when the coefficients span at most 12
+                // binades: every subset sum then has at most 24 significant
+                // bits), one rounding to binary16; entry p0 + e takes its top
+                // bit from the lane and the others from e
+                auto table32 = [&]() {
+                    float cf[K];
+#pragma unroll
+                    for (int i = 0; i < K; ++i)
+                        cf[i] = half_bits_to_float(c[i]);
+                    const float hi = kh ? cf[K - 1] : 0.f;
+#pragma unroll
+                    for (int e = 0; e < PER; ++e) {
+                        float sum = hi;
+#pragma unroll
+                        for (int i = 0; i < LOGPER; ++i)
+                            if ((e >> i) & 1)
+                                sum += cf[i];
+                        lrow[e] = __half_as_ushort(__float2half_rn(sum));
+                    }
+                };
+                const bool wide = emax - emin > 11;
+                if (__builtin_amdgcn_ballot_w64(wide) == 0) {
+                    table32();  // no lane needs binary64 (wavefront-uniform branch)
+                } else if (!wide) {
+                    table32();
+                } else {
+#pragma unroll
+                    for (int e = 0; e < PER; ++e) {
+                        const int p = p0 + e;
+                        double sum = 0.0;  // exact: at most K binary16 terms
+#pragma unroll
+                        for (int i = 0; i < K; ++i)
+                            sum += ((p >> i) & 1) ? (double)half_bits_to_float(c[i]) : 0.0;
+                        lrow[e] = f64_to_f16_rne(sum);
+                    }
+                }
+            }
+            // the tables are read by other lanes of this wavefront only: its
+            // LDS writes complete before the reads below (in order within a
+            // wavefront)
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+
+            const unsigned char *xt = xbuf + (j & 1) * XT;
+#pragma unroll
+            for (int st = 0; st < 8; ++st) {
+                const int v = 2 * (st & 1) + kh;
+                v8h Bw[RT];
+#pragma unroll
+                for (int q = 0; q < RT; ++q) {
+                    uint32_t pat = 0u;  // nibble p: subset index of element 16 st + 8 kh + p
+#pragma unroll
+                    for (int i = 0; i < K; ++i) {
+                        const uint4 sl = cur.slot[q][i];
+                        const int wi = st >> 1;
+                        const uint32_t word = wi == 0 ? sl.x : (wi == 1 ? sl.y : (wi == 2 ? sl.z : sl.w));
+                        pat |= ((word >> v) & 0x11111111u) << i;
+                    }
+                    // byte b of e2 / o2: byte offset of nibble 2b / 2b+1's entry
+                    const uint32_t e2 = (pat & 0x0F0F0F0Fu) << 1, o2 = (pat >> 3) & 0x1E1E1E1Eu;
+                    const uint32_t Lbase = lds_addr(lut + (32 * q + n) * LROW);
+                    const uint32_t ad[8] = {add_byte<0>(Lbase, e2), add_byte<0>(Lbase, o2), add_byte<1>(Lbase, e2),
+                                            add_byte<1>(Lbase, o2), add_byte<2>(Lbase, e2), add_byte<2>(Lbase, o2),
+                                            add_byte<3>(Lbase, e2), add_byte<3>(Lbase, o2)};
+                    auto at = [&](int i) {
+                        return *(const __attribute__((address_space(3))) _Float16 *)(uintptr_t)ad[i];
+                    };
+                    Bw[q] = v8h{at(0), at(1), at(2), at(3), at(4), at(5), at(6), at(7)};
+                }
+#pragma unroll
+                for (int tt = 0; tt < TT; ++tt) {
+                    // token 32 tt + n, elements 16 st + 8 kh .. +7
+                    const uint4 av = *(const uint4 *)(xt + (32 * tt + n) * PF_XROW + (2 * st + kh) * 16);
+#pragma unroll
+                    for (int q = 0; q < RT; ++q)
+                        acc[q][tt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(v8h, av), Bw[q],
+                                                                            acc[q][tt], 0, 0, 0);
+                }
+            }
+        }
+        if (more) {
+            // the other buffer was last read before the previous barrier
+            store_x(xbuf + ((j + 1) & 1) * XT, xv);
+            cur = nxt;
+        }
+        __syncthreads();
+    }
+
+    // ---- the S K-slices of each row group summed in a fixed order (halving
+    // tree through LDS; slot of K-slice s of row group rg: rg * S/2 + s) ----
+    constexpr int NV = RT * TT * 16;  // values per lane
+    float *red = (float *)smem;       // [R][S / 2][NV][64 lanes]
+    for (int half = S / 2; half >= 1; half /= 2) {
+        if (ks_id >= half && ks_id < 2 * half) {
+            float *dst = red + ((size_t)rg * (S / 2) + (ks_id - half)) * (NV * 64);
+#pragma unroll
+            for (int q = 0; q < RT; ++q)
+#pragma unroll
+                for (int tt = 0; tt < TT; ++tt)
+#pragma unroll
+                    for (int e = 0; e < 16; ++e)
+                        dst[((q * TT + tt) * 16 + e) * 64 + lane] = acc[q][tt][e];
+        }
+        __syncthreads();
+        if (ks_id < half) {
+            const float *src = red + ((size_t)rg * (S / 2) + ks_id) * (NV * 64);
+#pragma unroll
+            for (int q = 0; q < RT; ++q)
+#pragma unroll
+                for (int tt = 0; tt < TT; ++tt)
+#pragma unroll
+                    for (int e = 0; e < 16; ++e)
+                        acc[q][tt][e] += src[((q * TT + tt) * 16 + e) * 64 + lane];
+        }
+        __syncthreads();
+    }
+    if (ks_id != 0)
+        return;
+#pragma unroll
+    for (int q = 0; q < RT; ++q) {
+        const int oo = o_base + 32 * q + n;
+#pragma unroll
+        for (int tt = 0; tt < TT; ++tt)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const int t = t_base + 32 * tt + 8 * (e / 4) + 4 * kh + e % 4;
+                if (oo < a.O && t < a.T)
+                    a.Y[(size_t)t * a.O + oo] = __half_as_ushort(__float2half_rn(acc[q][tt][e]));
+            }
+    }
+}
+
+template <int K>
+static const void *prefill_long_kernel_for(int rt, int tt)
+{
+    if (rt == 2)
+        return tt == 2 ? (const void *)prefill_long_kernel<K, 2, 2> : (const void *)prefill_long_kernel<K, 2, 1>;
+    return tt == 4 ? (const void *)prefill_long_kernel<K, 1, 4>
+                   : (tt == 2 ? (const void *)prefill_long_kernel<K, 1, 2> : (const void *)prefill_long_kernel<K, 1, 1>);
+}
+
 template <int K>
 static const void *prefill_kernel_for(int btt)
 {
@@ -315,9 +603,104 @@ static const void *prefill_kernel_for(int btt)
 // 1 .. 512 tokens.
 constexpr int PF_CUS = 256;
 
+// Prompts of at least this many tokens run the long-prompt kernel.
+#ifndef SBVR_PF_LONG_MIN_T
+#define SBVR_PF_LONG_MIN_T 96
+#endif
+// ... and its grid has at least this many workgroups (else the kernel above)
+#ifndef SBVR_PF_LONG_MIN_WG
+#define SBVR_PF_LONG_MIN_WG 192
+#endif
+// Sweeps: a fixed long-kernel shape (column tiles, token tiles, K-slices);
+// 0 lets the rule below choose.
+#ifndef SBVR_PF_LONG_RT
+#define SBVR_PF_LONG_RT 0
+#endif
+#ifndef SBVR_PF_LONG_TT
+#define SBVR_PF_LONG_TT 0
+#endif
+#ifndef SBVR_PF_LONG_S
+#define SBVR_PF_LONG_S 0
+#endif
+
+static size_t prefill_long_lds(int k, int rt, int tt, int S)
+{
+    const size_t front = (size_t)S * 2 * pl_xtile(tt);
+    const size_t red = (size_t)(PL_WAVES / S) * (S / 2) * rt * tt * 16 * 64 * 4;
+    return (front > red ? front : red) + (size_t)PL_WAVES * 32 * rt * ((1u << k) + PF_LUT_PAD) * 2;
+}
+
+// Long-prompt launch shape: among the (RT, TT, S) whose LDS fits, the grids
+// that fit one round of the 256 CUs win, and among those the most workgroups,
+// then the largest tile per wavefront (RT TT); when none fits, the fewest
+// workgroups.  Returns the workgroup count (0: no shape fits).
+struct LongShape {
+    int rt, tt, S, wg;
+};
+
+static LongShape prefill_long_shape(const Dims &d, int T)
+{
+    LongShape b = {0, 0, 0, 0};
+    for (int r = 1; r <= 2; ++r)
+        for (int t = 1; t <= 4; t *= 2)
+            for (int sk = 1; sk <= PL_WAVES && sk <= d.G && sk * t <= PL_XPT; sk *= 2) {
+                if (r * t > PL_TILE_MAX)
+                    continue;
+                if (SBVR_PF_LONG_RT && r != SBVR_PF_LONG_RT)
+                    continue;
+                if (SBVR_PF_LONG_TT && t != SBVR_PF_LONG_TT)
+                    continue;
+                if (SBVR_PF_LONG_S && sk != SBVR_PF_LONG_S)
+                    continue;
+                if (prefill_long_lds(d.k, r, t, sk) > PF_LDS_MAX)
+                    continue;
+                const int rows = 32 * r * (PL_WAVES / sk);
+                const int wg = (d.O + rows - 1) / rows * ((T + 32 * t - 1) / (32 * t));
+                const bool fits = wg <= PF_CUS, best_fits = b.wg > 0 && b.wg <= PF_CUS;
+                bool take;
+                if (b.rt == 0)
+                    take = true;
+                else if (fits != best_fits)
+                    take = fits;
+                else if (wg != b.wg)
+                    take = fits ? wg > b.wg : wg < b.wg;
+                else
+                    take = r * t > b.rt * b.tt;
+                if (take)
+                    b = {r, t, sk, wg};
+            }
+    return b;
+}
+
+static int launch_prefill_long(const Dims &d, const LongShape &sh, const void *planes_dev, const void *coeffs_dev,
+                               const uint16_t *X, uint16_t *Y, int T, hipStream_t stream)
+{
+    const int rows = 32 * sh.rt * (PL_WAVES / sh.S);
+    const int gx = (d.O + rows - 1) / rows, gy = (T + 32 * sh.tt - 1) / (32 * sh.tt);
+    PrefillArgs a = {(const uint32_t *)planes_dev, (const uint16_t *)coeffs_dev, X, Y, d.O, d.I, T, d.n_tiles,
+                     d.n_gblocks, d.G, (d.G + sh.S - 1) / sh.S, sh.S};
+    const void *fn = d.k == 4   ? prefill_long_kernel_for<4>(sh.rt, sh.tt)
+                     : d.k == 3 ? prefill_long_kernel_for<3>(sh.rt, sh.tt)
+                     : d.k == 2 ? prefill_long_kernel_for<2>(sh.rt, sh.tt)
+                                : prefill_long_kernel_for<1>(sh.rt, sh.tt);
+    void *args[] = {&a};
+    return launch_kernel(fn, dim3(gx, gy), dim3(64 * PL_WAVES), prefill_long_lds(d.k, sh.rt, sh.tt, sh.S), stream,
+                         args);
+}
+
 int launch_prefill(const Dims &d, const void *planes_dev, const void *coeffs_dev, const uint16_t *X, uint16_t *Y,
                    int T, hipStream_t stream)
 {
+    // the long-prompt kernel where its grid fills most of the chip (measured:
+    // faster there -- Llama-3-8B gate at 128 / 256 / 512 tokens 66.6 / 122 /
+    // 167 us -> 60.6 / 94 / 132, down at 512 216 -> 187, q/o 66 -> 57 --,
+    // slower for a 1024-row matrix at 128 tokens, whose best long grid has 64
+    // workgroups: 16.2 -> 27.5 us)
+    if (T >= SBVR_PF_LONG_MIN_T) {
+        const LongShape sh = prefill_long_shape(d, T);
+        if (sh.wg >= SBVR_PF_LONG_MIN_WG)
+            return launch_prefill_long(d, sh, planes_dev, coeffs_dev, X, Y, T, stream);
+    }
     int btt = 0, S = 0, best_wg = 0;
     for (int bt = 1; bt <= 8; bt *= 2) {
         if (bt > 1 && 16 * (bt / 2) >= T)  // a smaller tile already covers the prompt

@@ -105,7 +105,7 @@ def test_prefill_ragged(sb, O, I, k, T):
 
 
 @pytest.mark.parametrize("O,I", [(14336, 4096), (4096, 14336), (1024, 4096)])
-@pytest.mark.parametrize("T", [64, 512])
+@pytest.mark.parametrize("T", [64, 128, 512])
 def test_prefill_full_size_sampled(sb, O, I, T):
     """Llama-3-8B projection shapes at the benchmark's prompt lengths, on
     sampled rows (first and last included) and every token."""
@@ -113,6 +113,57 @@ def test_prefill_full_size_sampled(sb, O, I, T):
     X = synth.activations(I, seed=T + O, batch=T)
     rows = np.unique(np.r_[0, O - 1, np.random.default_rng(T).integers(0, O, 62)])
     check(run(sb, packed(sb, planes, coeffs), X), X, planes, coeffs, rows=rows, what=f"full {O}x{I} T={T}")
+
+
+# The long-prompt kernel (32 x 32 instructions; it runs from 96 tokens where
+# its grid has >= 192 workgroups): one case per launch shape the rule picks
+# -- (column tiles, token tiles, K-slices) = (1,1,1), (1,1,2), (1,1,4),
+# (1,2,1), (1,2,2), (1,4,1), (2,1,4), (2,2,2) in this order -- with ragged row
+# and token counts and k = 1..4.
+LONG_CASES = [(1500, 128, 1, 1000), (6144, 256, 2, 100), (1500, 512, 3, 256), (8192, 128, 4, 333),
+              (6144, 256, 1, 200), (6144, 128, 3, 1000), (6144, 512, 2, 100), (8192, 256, 4, 333)]
+
+
+@pytest.mark.parametrize("O,I,k,T", LONG_CASES)
+def test_prefill_long_prompt_shapes(sb, O, I, k, T):
+    """Sampled rows, every token, against the product the prefill path
+    defines, X times the binary16-rounded weights (binary64); and against the
+    exact weights where a row has at least 512 terms.  (With a single group
+    the rounding of the weights and of the output alone reach the gate: for
+    8192 x 128, k = 4, T = 333 the binary64 product of the rounded weights,
+    rounded to binary16, is 1.016e-3 from the exact-weight result.)"""
+    planes, coeffs = synth.random_sbvr(O, I, k, seed=O + 5 * I + k + T)
+    W = packed(sb, planes, coeffs)
+    X = synth.activations(I, seed=O + T + 1, batch=T)
+    rows = np.unique(np.r_[0, O - 1, np.random.default_rng(O + T).integers(0, O, 62)])
+    Y = run(sb, W, X)
+    y16 = X.astype(np.float64) @ fp16_weights(planes, coeffs, rows).T
+    worst = max(rel_err(Y[t, rows], y16[t]) for t in range(T))
+    log(f"prefill long {O}x{I} k={k} T={T}: worst per-token err vs binary16 weights {worst:.3e}")
+    assert worst <= TOL, worst
+    if I >= 512:
+        check(Y, X, planes, coeffs, rows=rows, what=f"long {O}x{I} k={k} T={T}")
+
+
+def test_prefill_long_prompt_weights_bit_exact(sb):
+    """The long-prompt kernel multiplies the correctly rounded binary16
+    weights: unit tokens for the first 128 columns (T = 128, one K-slice
+    shape) and for all 512 (T = 512, another), ordinary and wide coefficient
+    spans (the binary64 table path)."""
+    O, I, k = 4096, 512, 4
+    planes, coeffs = synth.random_sbvr(O, I, k, seed=77)
+    W = packed(sb, planes, coeffs)
+    check_unit_tokens(sb, W, planes, coeffs, np.arange(128), what="long T=128")
+    check_unit_tokens(sb, W, planes, coeffs, np.arange(I), what="long T=512")
+    c = coeffs.view(np.float16).copy()
+    c[::2, :, 3] = np.float16(3e-6) * np.sign(c[::2, :, 3]).astype(np.float16)
+    c[1::4, :, 0] = np.float16(1500.0)
+    coeffs = c.view(np.uint16)
+    W = packed(sb, planes, coeffs)
+    check_unit_tokens(sb, W, planes, coeffs, np.arange(I), what="long wide span")
+    X = synth.activations(I, seed=78, batch=512, scale=0.05)
+    rows = np.unique(np.r_[0, O - 1, np.random.default_rng(79).integers(0, O, 62)])
+    check(run(sb, W, X), X, planes, coeffs, rows=rows, what="long wide span")
 
 
 def test_prefill_wide_coefficient_span(sb):
