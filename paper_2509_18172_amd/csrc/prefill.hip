@@ -483,10 +483,15 @@ __global__ void __launch_bounds__(64 * PL_WAVES) prefill_long_kernel(PrefillArgs
             __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 
             const unsigned char *xt = xbuf + (j & 1) * XT;
-#pragma unroll
-            for (int st = 0; st < 8; ++st) {
+            // Operands of step st: the lane's eight weights of each of its
+            // rows (table lookups) and its activation fragment of each token
+            // tile.  Software-pipelined: step st + 1's LDS reads are issued
+            // before step st's products, so their latency overlaps the
+            // matrix-core work instead of stalling every instruction.
+            v8h Bw[2][RT];
+            uint4 Av[2][TT];
+            auto load_step = [&](int st, v8h *bw, uint4 *av) {
                 const int v = 2 * (st & 1) + kh;
-                v8h Bw[RT];
 #pragma unroll
                 for (int q = 0; q < RT; ++q) {
                     uint32_t pat = 0u;  // nibble p: subset index of element 16 st + 8 kh + p
@@ -506,17 +511,25 @@ __global__ void __launch_bounds__(64 * PL_WAVES) prefill_long_kernel(PrefillArgs
                     auto at = [&](int i) {
                         return *(const __attribute__((address_space(3))) _Float16 *)(uintptr_t)ad[i];
                     };
-                    Bw[q] = v8h{at(0), at(1), at(2), at(3), at(4), at(5), at(6), at(7)};
+                    bw[q] = v8h{at(0), at(1), at(2), at(3), at(4), at(5), at(6), at(7)};
                 }
 #pragma unroll
-                for (int tt = 0; tt < TT; ++tt) {
-                    // token 32 tt + n, elements 16 st + 8 kh .. +7
-                    const uint4 av = *(const uint4 *)(xt + (32 * tt + n) * PF_XROW + (2 * st + kh) * 16);
+                for (int tt = 0; tt < TT; ++tt)  // token 32 tt + n, elements 16 st + 8 kh .. +7
+                    av[tt] = *(const uint4 *)(xt + (32 * tt + n) * PF_XROW + (2 * st + kh) * 16);
+            };
+            load_step(0, Bw[0], Av[0]);
+#pragma unroll
+            for (int st = 0; st < 8; ++st) {
+                if (st + 1 < 8)
+                    load_step(st + 1, Bw[(st + 1) & 1], Av[(st + 1) & 1]);
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int tt = 0; tt < TT; ++tt)
 #pragma unroll
                     for (int q = 0; q < RT; ++q)
-                        acc[q][tt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(v8h, av), Bw[q],
-                                                                            acc[q][tt], 0, 0, 0);
-                }
+                        acc[q][tt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(v8h, Av[st & 1][tt]),
+                                                                            Bw[st & 1][q], acc[q][tt], 0, 0, 0);
+                __builtin_amdgcn_sched_barrier(0);
             }
         }
         if (more) {
