@@ -116,14 +116,21 @@ __global__ void __launch_bounds__(64 * PF_WAVES) prefill_kernel(PrefillArgs a)
     // consecutive threads read one token's 256 bytes (tokens past T read as
     // zero)
     const int xthr = rt * 64 + lane, nxthr = R * 64;
+    // (no per-lane branch: chunks past the tile or the prompt read the last
+    // token and are zeroed; rounds past the chunks of the tile's tokens, the
+    // same for every thread of the workgroup, are skipped)
+    const int x_rounds = (min(XCH, (a.T - t_base) * 16) + nxthr - 1) / nxthr;
     auto load_x = [&](int g, uint4 *v) {
 #pragma unroll
         for (int q = 0; q < XPT; ++q) {
-            const int ch = xthr + q * nxthr;
             v[q] = make_uint4(0u, 0u, 0u, 0u);
-            const int t = t_base + ch / 16;
-            if (ch < XCH && t < a.T)
-                v[q] = *(const uint4 *)(a.X + (size_t)t * a.I + (size_t)g * GROUP + (ch % 16) * 8);
+            if (q < x_rounds) {
+                const int ch = xthr + q * nxthr;
+                const int t = t_base + ch / 16;
+                const uint4 r =
+                    *(const uint4 *)(a.X + (size_t)min(t, a.T - 1) * a.I + (size_t)g * GROUP + (ch % 16) * 8);
+                v[q] = ch < XCH && t < a.T ? r : make_uint4(0u, 0u, 0u, 0u);
+            }
         }
     };
     auto store_x = [&](unsigned char *buf, const uint4 *v) {
@@ -137,21 +144,24 @@ __global__ void __launch_bounds__(64 * PF_WAVES) prefill_kernel(PrefillArgs a)
 
     // every wavefront of the workgroup runs gps steps (groups past G are
     // skipped but keep the barriers aligned)
+    // Every load is issued unconditionally (past the K-slice's last group the
+    // current or last group is loaded again and not used): with no branch
+    // around them the compiler's load counters stay exact through the loop,
+    // so the next group's loads overlap this group's products instead of
+    // being waited for before its table build.
     GroupLoads cur, nxt;
     uint4 xv[XPT];
-    if (g0 < a.G) {
-        load_group(g0, cur);
-        load_x(g0, xv);
-        store_x(xbuf, xv);
-    }
+    const int g_first = min(g0, a.G - 1);
+    load_group(g_first, cur);
+    load_x(g_first, xv);
+    store_x(xbuf, xv);
     __syncthreads();
     for (int j = 0; j < a.gps; ++j) {
         const int g = g0 + j;
         const bool more = j + 1 < a.gps && g + 1 < a.G;
-        if (more) {
-            load_group(g + 1, nxt);
-            load_x(g + 1, xv);  // stored after this group's products
-        }
+        const int gn = more ? g + 1 : min(g, a.G - 1);
+        load_group(gn, nxt);
+        load_x(gn, xv);  // stored after this group's products
         if (g < a.G) {
             // ---- subset-sum table of the 16 rows for group g (lane: row n,
             // subsets NSUB/4 * kq ..; all of them for k < 2) ----
@@ -247,11 +257,9 @@ __global__ void __launch_bounds__(64 * PF_WAVES) prefill_kernel(PrefillArgs a)
                 }
             }
         }
-        if (more) {
-            // the other buffer was last read before the previous barrier
-            store_x(xbuf + ((j + 1) & 1) * XT, xv);
-            cur = nxt;
-        }
+        // the other buffer was last read before the previous barrier
+        store_x(xbuf + ((j + 1) & 1) * XT, xv);
+        cur = nxt;
         __syncthreads();
     }
 
@@ -384,14 +392,21 @@ __global__ void __launch_bounds__(64 * PL_WAVES) prefill_long_kernel(PrefillArgs
     // a group's activation tile, loaded by the K-slice's R wavefronts: 16
     // consecutive threads read one token's 256 bytes (tokens past T read zero)
     const int xthr = rg * 64 + lane, nxthr = R * 64;
+    // (no per-lane branch: chunks past the tile or the prompt read the last
+    // token and are zeroed; rounds past the chunks of the tile's tokens, the
+    // same for every thread of the workgroup, are skipped)
+    const int x_rounds = (min(XCH, (a.T - t_base) * 16) + nxthr - 1) / nxthr;
     auto load_x = [&](int g, uint4 *v) {
 #pragma unroll
         for (int q = 0; q < PL_XPT; ++q) {
-            const int ch = xthr + q * nxthr;
             v[q] = make_uint4(0u, 0u, 0u, 0u);
-            const int t = t_base + ch / 16;
-            if (ch < XCH && t < a.T)
-                v[q] = *(const uint4 *)(a.X + (size_t)t * a.I + (size_t)g * GROUP + (ch % 16) * 8);
+            if (q < x_rounds) {
+                const int ch = xthr + q * nxthr;
+                const int t = t_base + ch / 16;
+                const uint4 r =
+                    *(const uint4 *)(a.X + (size_t)min(t, a.T - 1) * a.I + (size_t)g * GROUP + (ch % 16) * 8);
+                v[q] = ch < XCH && t < a.T ? r : make_uint4(0u, 0u, 0u, 0u);
+            }
         }
     };
     auto store_x = [&](unsigned char *buf, const uint4 *v) {
@@ -403,21 +418,24 @@ __global__ void __launch_bounds__(64 * PL_WAVES) prefill_long_kernel(PrefillArgs
         }
     };
 
+    // Every load is issued unconditionally (past the K-slice's last group the
+    // current or last group is loaded again and not used): with no branch
+    // around them the compiler's load counters stay exact through the loop,
+    // so the next group's loads overlap this group's products instead of
+    // being waited for before its table build.
     GroupLoads cur, nxt;
     uint4 xv[PL_XPT];
-    if (g0 < a.G) {
-        load_group(g0, cur);
-        load_x(g0, xv);
-        store_x(xbuf, xv);
-    }
+    const int g_first = min(g0, a.G - 1);
+    load_group(g_first, cur);
+    load_x(g_first, xv);
+    store_x(xbuf, xv);
     __syncthreads();
     for (int j = 0; j < a.gps; ++j) {
         const int g = g0 + j;
         const bool more = j + 1 < a.gps && g + 1 < a.G;
-        if (more) {
-            load_group(g + 1, nxt);
-            load_x(g + 1, xv);  // stored after this group's products
-        }
+        const int gn = more ? g + 1 : min(g, a.G - 1);
+        load_group(gn, nxt);
+        load_x(gn, xv);  // stored after this group's products
         if (g < a.G) {
             // ---- subset-sum tables of the wavefront's rows for group g (lane:
             // row lane % 32 of each column tile, subsets PER * (lane / 32) ..) ----
@@ -532,11 +550,9 @@ __global__ void __launch_bounds__(64 * PL_WAVES) prefill_long_kernel(PrefillArgs
                 __builtin_amdgcn_sched_barrier(0);
             }
         }
-        if (more) {
-            // the other buffer was last read before the previous barrier
-            store_x(xbuf + ((j + 1) & 1) * XT, xv);
-            cur = nxt;
-        }
+        // the other buffer was last read before the previous barrier
+        store_x(xbuf + ((j + 1) & 1) * XT, xv);
+        cur = nxt;
         __syncthreads();
     }
 

@@ -240,3 +240,18 @@ def test_cached_encoder_error_paths(sb):
     assert f(4, 256, 5, w, 8, 8, 16, 4, 1, 4, p, c, None, None, 0) == sb.SBVR_E_UNSUPPORTED
     assert f(4, 256, 4, w + 2, 8, 8, 16, 4, 1, 4, p, c, None, None, 0) == sb.SBVR_E_ALIGNMENT
     torch.cuda.synchronize()
+
+
+@settings(max_examples=25, deadline=None, derandomize=True, database=None,
+          suppress_health_check=[HealthCheck.function_scoped_fixture, HealthCheck.too_slow])
+@given(O=st.integers(1, 24), G=st.integers(1, 12), k=st.integers(1, 4), slots=st.integers(0, 64),
+       grid=st.tuples(st.integers(1, 9), st.integers(1, 9), st.integers(1, 20), st.integers(1, 6)),
+       normalise=st.booleans(), sigma_exp=st.integers(-12, 2), outliers=st.booleans())
+def test_cached_encoder_bit_exact_random(sb, O, G, k, slots, grid, normalise, sigma_exp, outliers):
+    """Random shapes, cache sizes, search grids, weight scales and outlier
+    mixes: planes, coefficients, MSE and hit flags identical to the oracle's
+    cached encoder."""
+    params = oracle.SearchParams(grid[0], grid[1], grid[2], grid[3], normalise=normalise)
+    W = synth.weights(O, 128 * G, 2.0 ** sigma_exp, seed=O * 977 + G * 37 + k + slots + sigma_exp + 64,
+                      outlier_frac=0.01 if outliers else 0.0)
+    assert_same_cached(sb, W, k, slots, params, what=f"{params} sigma=2^{sigma_exp}")
