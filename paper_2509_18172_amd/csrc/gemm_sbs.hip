@@ -212,7 +212,15 @@ __global__ void __launch_bounds__(512) gemm_sbs_kernel(GemvArgs a)
     int pf_i = 0, pf_gb = wv;
     uint4 P[D];
     CoefGroups<K> C[D];
-    auto issue = [&](int j) {
+    // Slot j's planes for the next item of the stream; returns the byte
+    // offset of that item's coefficients, loaded by issue_c.  The loop
+    // reloads a slot's coefficients only after the item's last use of its old
+    // ones: loading them with the planes kept both sets live, and the compiler
+    // then rotated the ring through register copies at every loop latch,
+    // behind a wait for all outstanding loads (measured, interleaved runs:
+    // 8B gate at B = 2 / 4 / 8 9.99 / 10.83 / 14.70 -> 9.71 / 10.49 / 14.41
+    // us, 70B gate at B = 4 35.2 -> 32.3; down and q/o within 1 %).
+    auto issue_p = [&](int j) {
         unsigned po, co;
         if constexpr (MULTI) {
             po = co = BUF_OOB;
@@ -230,8 +238,10 @@ __global__ void __launch_bounds__(512) gemm_sbs_kernel(GemvArgs a)
             ++pf_i;
         }
         P[j] = buf_load16(prs, p_lane + po);
-        C[j] = buf_coef_groups<K>(crs, c_lane + co);
+        return co;
     };
+    auto issue_c = [&](int j, unsigned co) { C[j] = buf_coef_groups<K>(crs, c_lane + co); };
+    auto issue = [&](int j) { issue_c(j, issue_p(j)); };
     // The lane's eight activations of gblock gb for every vector.  One gblock
     // per wavefront: vectors >= B load the last vector again (their limbs are
     // staged but no operand reads them), and lanes past I (ragged end) read a
@@ -378,7 +388,7 @@ __global__ void __launch_bounds__(512) gemm_sbs_kernel(GemvArgs a)
                     d[g][st] = mfma_fp4_fp8<false>(A, Bop[st][g], v4f{0.f, 0.f, 0.f, 0.f});
             }
             const CoefGroups<K> cr = C[j];
-            issue(j);
+            const unsigned co_next = issue_p(j);
 #pragma unroll
             for (int st = 0; st < NS; ++st) {
                 // the lane's (tile row, vector, limb) partials of the item:
@@ -401,6 +411,7 @@ __global__ void __launch_bounds__(512) gemm_sbs_kernel(GemvArgs a)
                     }
                 }
             }
+            issue_c(j, co_next);
             if (valid) {
                 if (++cur_i == ntl && MULTI) {
                     cur_i = 0;
