@@ -118,10 +118,11 @@ def test_prefill_full_size_sampled(sb, O, I, T):
 # The long-prompt kernel (32 x 32 instructions; it runs from 96 tokens where
 # its grid has >= 192 workgroups): one case per launch shape the rule picks
 # -- (column tiles, token tiles, K-slices) = (1,1,1), (1,1,2), (1,1,4),
-# (1,2,1), (1,2,2), (1,4,1), (2,1,4), (2,2,2) in this order -- with ragged row
-# and token counts and k = 1..4.
+# (1,2,1), (1,2,2), (1,4,1), (2,1,4), (2,2,2), then (1,4,1) with 240
+# workgroups and (2,1,2) -- with ragged row and token counts and k = 1..4.
 LONG_CASES = [(1500, 128, 1, 1000), (6144, 256, 2, 100), (1500, 512, 3, 256), (8192, 128, 4, 333),
-              (6144, 256, 1, 200), (6144, 128, 3, 1000), (6144, 512, 2, 100), (8192, 256, 4, 333)]
+              (6144, 256, 1, 200), (6144, 128, 3, 1000), (6144, 512, 2, 100), (8192, 256, 4, 333),
+              (12288, 128, 2, 640), (12288, 256, 3, 160)]
 
 
 @pytest.mark.parametrize("O,I,k,T", LONG_CASES)
@@ -149,7 +150,11 @@ def test_prefill_long_prompt_weights_bit_exact(sb):
     """The long-prompt kernel multiplies the correctly rounded binary16
     weights: unit tokens for the first 128 columns (T = 128, one K-slice
     shape) and for all 512 (T = 512, another), ordinary and wide coefficient
-    spans (the binary64 table path)."""
+    spans (the binary64 table path); and all 512 columns of a 12288-row
+    matrix (the 1 x 4 x 1 shape)."""
+    O12, I12 = 12288, 512
+    planes, coeffs = synth.random_sbvr(O12, I12, 4, seed=76)
+    check_unit_tokens(sb, packed(sb, planes, coeffs), planes, coeffs, np.arange(I12), what="long 1x4 T=512")
     O, I, k = 4096, 512, 4
     planes, coeffs = synth.random_sbvr(O, I, k, seed=77)
     W = packed(sb, planes, coeffs)
