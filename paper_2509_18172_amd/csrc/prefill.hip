@@ -29,9 +29,9 @@
 // The plane slots, coefficients and activations of the next group are loaded
 // while the current one is decoded.
 // Bound: the decoding (about 300 vector instructions per wavefront and group,
-// whatever BTT is) for prompts up to a few hundred tokens; BTT = 8 amortises
-// it over 128 tokens, and past that the weights are decoded once per 128
-// tokens.
+// whatever BTT is); BTT = 8 amortises it over 128 tokens.  From 96 tokens,
+// where its grid fills the chip, the long-prompt kernel further down runs
+// instead (32 x 32 products, 32-row column tiles).
 #include "device_ops.h"
 #include "lds_lookup.h"
 #include "f16_round.h"
