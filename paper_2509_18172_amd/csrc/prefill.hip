@@ -320,9 +320,14 @@ __global__ void __launch_bounds__(64 * PF_WAVES) prefill_kernel(PrefillArgs a)
 // tile, row lane % 32.
 // ---------------------------------------------------------------------------
 constexpr int PL_WAVES = 8;
-// activation chunks (16 bytes) per thread and group: the launcher keeps
-// S TT <= PL_XPT (a K-slice's 512 / S threads load 512 TT chunks)
-constexpr int PL_XPT = 4;
+// activation chunks (16 bytes) per thread and group: S TT (a K-slice's
+// 512 / S threads load 512 TT chunks).  The launcher keeps S TT <= 8 for one
+// column tile of 64 or 128 tokens (so that its products can split K four and
+// two ways) and <= 4 otherwise; a kernel instance holds 4 or 8 chunks (XPT),
+// 4 whenever S TT allows (the 8-chunk build of the same shape measured 3-5 %
+// slower; 2 x 2 tiles with 8 chunks and four K-slices, 5-10 % slower than
+// 1 x 2 tiles with two)
+__host__ __device__ constexpr int pl_xpt(int tt) { return tt == 1 ? 4 : 8; }
 // instructions per step and wavefront (RT TT) at most: the RT TT x 16
 // accumulators of 2 x 2 and 1 x 4 fit the 256 registers of a wavefront at two
 // per SIMD; 2 x 4 would spill
@@ -332,7 +337,7 @@ typedef float v16f __attribute__((ext_vector_type(16)));
 
 __host__ __device__ constexpr int pl_xtile(int tt) { return 32 * tt * PF_XROW; }
 
-template <int K, int RT, int TT>
+template <int K, int RT, int TT, int XPT>
 __global__ void __launch_bounds__(64 * PL_WAVES) prefill_long_kernel(PrefillArgs a)
 {
     constexpr int TR = tile_rows(K), NSUB = 1 << K;
@@ -398,7 +403,7 @@ __global__ void __launch_bounds__(64 * PL_WAVES) prefill_long_kernel(PrefillArgs
     const int x_rounds = (min(XCH, (a.T - t_base) * 16) + nxthr - 1) / nxthr;
     auto load_x = [&](int g, uint4 *v) {
 #pragma unroll
-        for (int q = 0; q < PL_XPT; ++q) {
+        for (int q = 0; q < XPT; ++q) {
             v[q] = make_uint4(0u, 0u, 0u, 0u);
             if (q < x_rounds) {
                 const int ch = xthr + q * nxthr;
@@ -411,7 +416,7 @@ __global__ void __launch_bounds__(64 * PL_WAVES) prefill_long_kernel(PrefillArgs
     };
     auto store_x = [&](unsigned char *buf, const uint4 *v) {
 #pragma unroll
-        for (int q = 0; q < PL_XPT; ++q) {
+        for (int q = 0; q < XPT; ++q) {
             const int ch = xthr + q * nxthr;
             if (ch < XCH)
                 *(uint4 *)(buf + (ch / 16) * PF_XROW + (ch % 16) * 16) = v[q];
@@ -424,7 +429,7 @@ __global__ void __launch_bounds__(64 * PL_WAVES) prefill_long_kernel(PrefillArgs
     // so the next group's loads overlap this group's products instead of
     // being waited for before its table build.
     GroupLoads cur, nxt;
-    uint4 xv[PL_XPT];
+    uint4 xv[XPT];
     const int g_first = min(g0, a.G - 1);
     load_group(g_first, cur);
     load_x(g_first, xv);
@@ -601,12 +606,16 @@ __global__ void __launch_bounds__(64 * PL_WAVES) prefill_long_kernel(PrefillArgs
 }
 
 template <int K>
-static const void *prefill_long_kernel_for(int rt, int tt)
+static const void *prefill_long_kernel_for(int rt, int tt, int S)
 {
+    const bool wide = S * tt > 4;
     if (rt == 2)
-        return tt == 2 ? (const void *)prefill_long_kernel<K, 2, 2> : (const void *)prefill_long_kernel<K, 2, 1>;
-    return tt == 4 ? (const void *)prefill_long_kernel<K, 1, 4>
-                   : (tt == 2 ? (const void *)prefill_long_kernel<K, 1, 2> : (const void *)prefill_long_kernel<K, 1, 1>);
+        return tt == 2 ? (const void *)prefill_long_kernel<K, 2, 2, 4> : (const void *)prefill_long_kernel<K, 2, 1, 4>;
+    if (tt == 4)
+        return wide ? (const void *)prefill_long_kernel<K, 1, 4, 8> : (const void *)prefill_long_kernel<K, 1, 4, 4>;
+    if (tt == 2)
+        return wide ? (const void *)prefill_long_kernel<K, 1, 2, 8> : (const void *)prefill_long_kernel<K, 1, 2, 4>;
+    return (const void *)prefill_long_kernel<K, 1, 1, 4>;
 }
 
 template <int K>
@@ -661,7 +670,9 @@ static size_t prefill_long_lds(int k, int rt, int tt, int S)
 
 // Long-prompt launch shape: among the (RT, TT, S) whose LDS fits, the grids
 // that fit one round of the 256 CUs win, and among those the most workgroups,
-// then the largest tile per wavefront (RT TT); when none fits, the fewest
+// then the widest token tile (each weight is decoded once per token tile),
+// then 4 activation chunks per thread over 8, then the largest tile per
+// wavefront (RT TT); when none fits, the fewest
 // workgroups.  Returns the workgroup count (0: no shape fits).
 struct LongShape {
     int rt, tt, S, wg;
@@ -672,8 +683,10 @@ static LongShape prefill_long_shape(const Dims &d, int T)
     LongShape b = {0, 0, 0, 0};
     for (int r = 1; r <= 2; ++r)
         for (int t = 1; t <= 4; t *= 2)
-            for (int sk = 1; sk <= PL_WAVES && sk <= d.G && sk * t <= PL_XPT; sk *= 2) {
+            for (int sk = 1; sk <= PL_WAVES && sk <= d.G && sk * t <= pl_xpt(t); sk *= 2) {
                 if (r * t > PL_TILE_MAX)
+                    continue;
+                if (r == 2 && sk * t > 4)  // two column tiles: 4 chunks per thread only
                     continue;
                 if (SBVR_PF_LONG_RT && r != SBVR_PF_LONG_RT)
                     continue;
@@ -693,6 +706,10 @@ static LongShape prefill_long_shape(const Dims &d, int T)
                     take = fits;
                 else if (wg != b.wg)
                     take = fits ? wg > b.wg : wg < b.wg;
+                else if (t != b.tt)
+                    take = t > b.tt;
+                else if ((sk * t <= 4) != (b.S * b.tt <= 4))
+                    take = sk * t <= 4;
                 else
                     take = r * t > b.rt * b.tt;
                 if (take)
@@ -708,10 +725,10 @@ static int launch_prefill_long(const Dims &d, const LongShape &sh, const void *p
     const int gx = (d.O + rows - 1) / rows, gy = (T + 32 * sh.tt - 1) / (32 * sh.tt);
     PrefillArgs a = {(const uint32_t *)planes_dev, (const uint16_t *)coeffs_dev, X, Y, d.O, d.I, T, d.n_tiles,
                      d.n_gblocks, d.G, (d.G + sh.S - 1) / sh.S, sh.S};
-    const void *fn = d.k == 4   ? prefill_long_kernel_for<4>(sh.rt, sh.tt)
-                     : d.k == 3 ? prefill_long_kernel_for<3>(sh.rt, sh.tt)
-                     : d.k == 2 ? prefill_long_kernel_for<2>(sh.rt, sh.tt)
-                                : prefill_long_kernel_for<1>(sh.rt, sh.tt);
+    const void *fn = d.k == 4   ? prefill_long_kernel_for<4>(sh.rt, sh.tt, sh.S)
+                     : d.k == 3 ? prefill_long_kernel_for<3>(sh.rt, sh.tt, sh.S)
+                     : d.k == 2 ? prefill_long_kernel_for<2>(sh.rt, sh.tt, sh.S)
+                                : prefill_long_kernel_for<1>(sh.rt, sh.tt, sh.S);
     void *args[] = {&a};
     return launch_kernel(fn, dim3(gx, gy), dim3(64 * PL_WAVES), prefill_long_lds(d.k, sh.rt, sh.tt, sh.S), stream,
                          args);

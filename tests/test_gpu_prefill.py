@@ -118,11 +118,12 @@ def test_prefill_full_size_sampled(sb, O, I, T):
 # The long-prompt kernel (32 x 32 instructions; it runs from 96 tokens where
 # its grid has >= 192 workgroups): one case per launch shape the rule picks
 # -- (column tiles, token tiles, K-slices) = (1,1,1), (1,1,2), (1,1,4),
-# (1,2,1), (1,2,2), (1,4,1), (2,1,4), (2,2,2), then (1,4,1) with 240
-# workgroups and (2,1,2) -- with ragged row and token counts and k = 1..4.
+# (1,2,1), (1,2,2), (1,4,1), (1,2,4) and (1,4,2) (8 activation chunks per
+# thread), (2,1,4), (2,2,2), then (1,4,1) with 240 workgroups and (2,1,2) --
+# with ragged row and token counts and k = 1..4.
 LONG_CASES = [(1500, 128, 1, 1000), (6144, 256, 2, 100), (1500, 512, 3, 256), (8192, 128, 4, 333),
               (6144, 256, 1, 200), (6144, 128, 3, 1000), (6144, 512, 2, 100), (8192, 256, 4, 333),
-              (12288, 128, 2, 640), (12288, 256, 3, 160)]
+              (3000, 512, 1, 256), (12288, 256, 2, 300), (12288, 128, 2, 640), (12288, 256, 3, 160)]
 
 
 @pytest.mark.parametrize("O,I,k,T", LONG_CASES)
