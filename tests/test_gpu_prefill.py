@@ -104,11 +104,14 @@ def test_prefill_ragged(sb, O, I, k, T):
     check_unit_tokens(sb, W, planes, coeffs, cols, what=f"ragged {O}x{I} k={k}")
 
 
-@pytest.mark.parametrize("O,I", [(14336, 4096), (4096, 14336), (1024, 4096)])
-@pytest.mark.parametrize("T", [64, 128, 512])
+@pytest.mark.parametrize("O,I", [(14336, 4096), (4096, 14336), (4096, 4096), (1024, 4096), (8192, 8192)])
+@pytest.mark.parametrize("T", [64, 128, 256, 512])
 def test_prefill_full_size_sampled(sb, O, I, T):
-    """Llama-3-8B projection shapes at the benchmark's prompt lengths, on
-    sampled rows (first and last included) and every token."""
+    """Llama-3-8B projection shapes (and the 70B q/o shape) at the
+    benchmark's prompt lengths, on sampled rows (first and last included) and
+    every token; 256 tokens runs the long-prompt kernel with 8 activation
+    chunks per thread (4096 rows: 64-token tiles over four K-slices; 14336
+    rows: 128-token tiles over two)."""
     planes, coeffs = synth.random_sbvr(O, I, 4, seed=O + 7 * I)
     X = synth.activations(I, seed=T + O, batch=T)
     rows = np.unique(np.r_[0, O - 1, np.random.default_rng(T).integers(0, O, 62)])
